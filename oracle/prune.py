@@ -1,0 +1,207 @@
+"""Oracle: block-structured pruning masks and canonical packing (numpy, fp64).
+
+TEST INFRASTRUCTURE ONLY - the product path never imports this module.
+
+Paper passages followed:
+* Sec. 4.1.1 (block-based pruning): the weight matrix is split into equal
+  blocks and rows / columns are pruned independently inside each block.
+* Sec. 4.2: the GEMM form of layer i, W_i in R^{P x Q (x Kh x Kw)}, split into
+  J blocks; Eq. 2 uses the rows of each block as groups, Eq. 3 the columns,
+  each measured by its squared Frobenius norm.
+* Sec. 5.1: one-shot pruning by weight magnitude.
+* Sec. 4.4: a 1x1 block is unstructured pruning, the whole matrix as one block
+  is structured (filter / channel) pruning.
+* Sec. 6 (tables): the compression rate is the parameter reduction factor.
+
+Readings where the paper is silent (each listed in the design notes):
+* kept groups per block = ceil(extent / rate) with an integer rate;
+* ties in the group score go to the lower index;
+* scores are accumulated in fp64 in ascending order (the squares of fp32 /
+  bf16 values are exact in fp64, so the order is the only rounding choice);
+* blocks are anchored at (0, 0); a ragged last block keeps
+  ceil(its own extent / rate);
+* a block size of 0 means the whole extent.
+
+Pins: tests/test_oracle_prune.py (brute-force subset enumeration, invariants,
+ties, ragged edges, scale invariance, hand-derived golden masks).
+"""
+
+from __future__ import annotations
+
+import numpy as np
+
+ROW, COL, UNSTRUCTURED, DENSE = 0, 1, 2, 3
+
+
+def kept_count(extent: int, rate: int) -> int:
+    """ceil(extent / rate) in integers."""
+    return (int(extent) + int(rate) - 1) // int(rate)
+
+
+def block_ranges(extent: int, b: int):
+    """Half-open ranges of the blocks along one dimension (b = 0: whole)."""
+    if b == 0 or b >= extent:
+        return [(0, int(extent))]
+    return [(s, min(s + b, extent)) for s in range(0, extent, b)]
+
+
+def as_f64(w_stored: np.ndarray, dtype: str) -> np.ndarray:
+    """Exact fp64 value of stored fp32 values or bf16 bit patterns."""
+    if dtype == "f32":
+        return np.asarray(w_stored, dtype=np.float32).astype(np.float64)
+    if dtype == "bf16":
+        u = np.asarray(w_stored, dtype=np.uint16).astype(np.uint32) << np.uint32(16)
+        return u.view(np.float32).astype(np.float64)
+    raise ValueError(dtype)
+
+
+def group_scores(block: np.ndarray, regularity: int) -> np.ndarray:
+    """Squared Frobenius norm of every column (COL) or row (ROW) of one block.
+
+    Eqs. 2-3 group a block's weights by row / column; the score is the sum of
+    squares, accumulated sequentially in ascending index order in fp64
+    (np.cumsum is a left-to-right running sum; its last entry is the total).
+    """
+    sq = block * block
+    if regularity == COL:
+        return np.cumsum(sq, axis=0)[-1]
+    if regularity == ROW:
+        return np.cumsum(sq, axis=1)[:, -1]
+    raise ValueError(regularity)
+
+
+def top_k(scores: np.ndarray, k: int) -> np.ndarray:
+    """Indices of the k largest scores, ties to the lower index (stable)."""
+    order = np.argsort(-scores, kind="stable")
+    return np.sort(order[:k])
+
+
+def prune_mask(wg: np.ndarray, bh: int, bw: int, regularity: int, rate: int) -> np.ndarray:
+    """Mask (uint8, R x C) of the kept weights of a GEMM-form fp64 matrix."""
+    wg = np.asarray(wg, dtype=np.float64)
+    R, C = wg.shape
+    mask = np.zeros((R, C), dtype=np.uint8)
+    if regularity == DENSE:
+        mask[:] = 1
+        return mask
+    if regularity == UNSTRUCTURED:
+        return unstructured_mask(wg, rate)
+    for r0, r1 in block_ranges(R, bh):
+        for c0, c1 in block_ranges(C, bw):
+            blk = wg[r0:r1, c0:c1]
+            s = group_scores(blk, regularity)
+            if regularity == COL:
+                keep = top_k(s, kept_count(c1 - c0, rate))
+                mask[r0:r1, c0 + keep] = 1
+            else:
+                keep = top_k(s, kept_count(r1 - r0, rate))
+                mask[r0 + keep, c0:c1] = 1
+    return mask
+
+
+def unstructured_mask(wg: np.ndarray, rate: int) -> np.ndarray:
+    """Magnitude pruning over the whole layer: keep ceil(R*C/rate) entries
+    with the largest |w|, ties to the smaller flat index p*C + q."""
+    R, C = wg.shape
+    a = np.abs(np.asarray(wg, dtype=np.float64)).reshape(-1)
+    k = kept_count(R * C, rate)
+    keep = np.argsort(-a, kind="stable")[:k]
+    m = np.zeros(R * C, dtype=np.uint8)
+    m[keep] = 1
+    return m.reshape(R, C)
+
+
+def mask_is_valid(mask: np.ndarray, bh: int, bw: int, regularity: int, rate: int) -> bool:
+    """True iff the mask has the block structure of the scheme: every block
+    keeps whole columns (COL) or whole rows (ROW), exactly ceil(extent/rate)."""
+    mask = np.asarray(mask, dtype=np.uint8)
+    R, C = mask.shape
+    if not np.all((mask == 0) | (mask == 1)):
+        return False
+    if regularity == DENSE:
+        return bool(np.all(mask == 1))
+    if regularity == UNSTRUCTURED:
+        return int(mask.sum()) == kept_count(R * C, rate)
+    for r0, r1 in block_ranges(R, bh):
+        for c0, c1 in block_ranges(C, bw):
+            blk = mask[r0:r1, c0:c1]
+            if regularity == COL:
+                if not np.all(blk == blk[0:1, :]):
+                    return False
+                if int(blk[0].sum()) != kept_count(c1 - c0, rate):
+                    return False
+            else:
+                if not np.all(blk == blk[:, 0:1]):
+                    return False
+                if int(blk[:, 0].sum()) != kept_count(r1 - r0, rate):
+                    return False
+    return True
+
+
+def pack(w_stored: np.ndarray, mask: np.ndarray, bh: int, bw: int, regularity: int, rate: int) -> dict:
+    """Canonical packing of a masked GEMM-form matrix (stored dtype kept as is).
+
+    COL: for block-row i, ``indices[rowptr[i]:rowptr[i+1]]`` are its kept
+         columns, block by block left to right, ascending inside a block (so
+         ascending overall); ``values[rowptr[i]*bh + p*len + t]`` is
+         W[i*bh + p, indices[rowptr[i] + t]].
+    ROW: for block (i, j) in row-major order, ``indices[rowptr[b]:rowptr[b+1]]``
+         are its kept rows ascending; its values are rows of the block,
+         ``[t][q_local]``, stored one block after the other.
+    DENSE / UNSTRUCTURED: no indices, ``values`` = W * mask, R x C.
+    """
+    w_stored = np.asarray(w_stored)
+    mask = np.asarray(mask, dtype=np.uint8)
+    R, C = mask.shape
+    if regularity in (DENSE, UNSTRUCTURED):
+        vals = np.where(mask == 1, w_stored, np.zeros_like(w_stored))
+        return {"indices": np.zeros(0, np.int32), "rowptr": np.zeros(0, np.int32),
+                "values": vals.reshape(-1).copy()}
+    idx, ptr, vals = [], [0], []
+    if regularity == COL:
+        for r0, r1 in block_ranges(R, bh):
+            kept = np.nonzero(mask[r0])[0].astype(np.int32)
+            idx.append(kept)
+            ptr.append(ptr[-1] + len(kept))
+            vals.append(w_stored[r0:r1][:, kept].reshape(-1))
+    else:
+        for r0, r1 in block_ranges(R, bh):
+            for c0, c1 in block_ranges(C, bw):
+                kept = (r0 + np.nonzero(mask[r0:r1, c0])[0]).astype(np.int32)
+                idx.append(kept)
+                ptr.append(ptr[-1] + len(kept))
+                vals.append(w_stored[kept][:, c0:c1].reshape(-1))
+    return {"indices": np.concatenate(idx).astype(np.int32),
+            "rowptr": np.asarray(ptr, dtype=np.int32),
+            "values": np.concatenate(vals)}
+
+
+def unpack(packed: dict, R: int, C: int, bh: int, bw: int, regularity: int, like: np.ndarray) -> np.ndarray:
+    """Inverse of ``pack``: the masked dense matrix in the stored dtype."""
+    out = np.zeros((R, C), dtype=np.asarray(like).dtype)
+    vals, idx, ptr = packed["values"], packed["indices"], packed["rowptr"]
+    if regularity in (DENSE, UNSTRUCTURED):
+        return vals.reshape(R, C).copy()
+    off = 0
+    if regularity == COL:
+        for i, (r0, r1) in enumerate(block_ranges(R, bh)):
+            kept = idx[ptr[i]:ptr[i + 1]]
+            n = (r1 - r0) * len(kept)
+            out[r0:r1][:, kept] = vals[off:off + n].reshape(r1 - r0, len(kept))
+            off += n
+    else:
+        b = 0
+        for r0, r1 in block_ranges(R, bh):
+            for c0, c1 in block_ranges(C, bw):
+                kept = idx[ptr[b]:ptr[b + 1]]
+                n = len(kept) * (c1 - c0)
+                out[kept, c0:c1] = vals[off:off + n].reshape(len(kept), c1 - c0)
+                off += n
+                b += 1
+    return out
+
+
+def gemm_form(w: np.ndarray) -> np.ndarray:
+    """(Cout, Cin, kh, kw) -> (Cout, Cin*kh*kw) with column q = (c*kh + r)*kw + s."""
+    w = np.asarray(w)
+    return w.reshape(w.shape[0], -1)
