@@ -1,0 +1,155 @@
+/*
+ * bsp.h - block-structured pruned conv / FC inference on AMD MI355X (gfx950).
+ *
+ * The pruning regularity is the paper's block-based scheme (Sec. 4.1.1): the
+ * GEMM-form weight matrix of a layer (rows = output filters, columns =
+ * Cin*kh*kw with column q = (c*kh + r)*kw + s, Sec. 4.2) is cut into blocks
+ * of bh x bw, and inside every block whole columns (BSP_COL) or whole rows
+ * (BSP_ROW) are removed.  The group measure is the squared Frobenius norm of
+ * a block's column / row (Eqs. 2-3), selected one-shot by magnitude
+ * (Sec. 5.1).  A block size of 0 means the whole extent, so a whole-matrix
+ * block is structured (filter / channel) pruning (Sec. 4.4).
+ *
+ * Conventions for every entry point
+ *  - Pointers named w, mask, values, indices, rowptr, dev_tiles, x, y, bias
+ *    are DEVICE pointers owned by the caller.  The library keeps no state
+ *    between calls and owns no memory after a call returns.
+ *  - `stream` is a hipStream_t passed as void* (NULL = legacy default stream).
+ *    Calls are asynchronous on it unless stated otherwise.
+ *  - Arguments are validated before anything is launched; on an argument
+ *    error nothing is written and a negative status is returned.  A launch
+ *    failure returns BSP_EDEVICE.  Faults inside kernels surface at the
+ *    caller's next synchronisation.
+ *  - Kept groups per block = ceil(extent / rate) with an integer rate >= 1;
+ *    ties in the score go to the lower index; scores are summed in fp64 in
+ *    ascending index order; blocks are anchored at (0, 0) and a ragged last
+ *    block keeps ceil(its own extent / rate).
+ *  - No exceptions cross this interface.  Calls on different streams may run
+ *    concurrently.
+ */
+#ifndef BSP_H
+#define BSP_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    BSP_OK = 0,
+    BSP_EINVAL = -1,        /* bad argument, shape or null pointer            */
+    BSP_EUNSUPPORTED = -2,  /* valid request this library does not implement  */
+    BSP_EDEVICE = -3,       /* HIP launch / copy / allocation failure          */
+    BSP_EMASK = -4          /* mask given to bsp_pack lacks the block structure */
+} bsp_status;
+
+typedef enum { BSP_F32 = 0, BSP_BF16 = 1 } bsp_dtype;
+
+typedef enum {
+    BSP_ROW = 0,            /* whole rows removed inside each block   (Eq. 2) */
+    BSP_COL = 1,            /* whole columns removed inside each block (Eq. 3) */
+    BSP_UNSTRUCTURED = 2,   /* magnitude top-k over the whole layer (Sec. 2.1.1) */
+    BSP_DENSE = 3           /* nothing removed                                 */
+} bsp_regularity;
+
+typedef struct {
+    int32_t rows, cols;     /* GEMM form: rows = Cout / out_features,
+                               cols = Cin*kh*kw / in_features                 */
+    int32_t bh, bw;         /* block size; 0 => whole extent                  */
+    int32_t regularity;     /* bsp_regularity                                  */
+    int32_t rate;           /* integer >= 1; kept per block = ceil(extent/rate);
+                               UNSTRUCTURED keeps ceil(rows*cols/rate)         */
+} bsp_scheme;
+
+/* Convolution geometry: dilation 1, groups 1, NCHW activations, OIHW weights. */
+typedef struct {
+    int32_t n, cin, h, w, kh, kw, stride_h, stride_w, pad_h, pad_w;
+} bsp_conv_shape;
+
+/* Sizes (in elements, and bytes for dev_tiles) of the buffers bsp_pack fills.
+ * Host-only, pure.  conv_or_null selects the conv layout (its n is ignored);
+ * NULL means a linear layer.  The canonical arrays are
+ *   COL: values = nnz, indices = n_block_rows * kept_per_row, rowptr = n_block_rows + 1
+ *   ROW: values = nnz, indices = kept rows summed over blocks, rowptr = n_blocks + 1
+ *   DENSE / UNSTRUCTURED: values = rows * cols, indices = rowptr = 0. */
+bsp_status bsp_packed_sizes(const bsp_scheme *scheme, const bsp_conv_shape *conv_or_null,
+                            bsp_dtype wdt, int64_t *n_values, int64_t *n_indices,
+                            int64_t *n_rowptr, int64_t *dev_tile_bytes);
+
+/* Prune (Sec. 4.1.1 with the group norms of Eqs. 2-3, one-shot magnitude
+ * selection of Sec. 5.1): w is the GEMM-form weight matrix, row-major
+ * rows x cols, of dtype wdt; mask (rows x cols bytes, row-major) receives 1
+ * for kept and 0 for removed weights.  Async.  The whole-layer magnitude
+ * ranking of BSP_UNSTRUCTURED allocates a small scratch buffer on `stream`
+ * (stream-ordered) and frees it before returning. */
+bsp_status bsp_prune(const bsp_scheme *scheme, bsp_dtype wdt, const void *w, uint8_t *mask,
+                     void *stream);
+
+/* Pack the masked weights (the compact storage idea of Sec. 4.3, in this
+ * library's own layout).  SYNCHRONOUS: checks on the device that the mask
+ * has the block structure of the scheme with exactly ceil(extent/rate) kept
+ * groups per block and returns BSP_EMASK otherwise (outputs then unspecified).
+ *   values / indices / rowptr: the canonical packing
+ *     COL: for block-row i, indices[rowptr[i] .. rowptr[i+1]) are its kept
+ *          columns in ascending order; values[rowptr[i]*bh + p*len + t] =
+ *          W[i*bh + p][indices[rowptr[i] + t]] (len = rowptr[i+1]-rowptr[i]).
+ *     ROW: for block b = i*n_block_cols + j, indices[rowptr[b] .. rowptr[b+1])
+ *          are its kept rows ascending; its values are those rows restricted
+ *          to the block's columns, [t][q_local], blocks stored in order b.
+ *     DENSE / UNSTRUCTURED: values = W * mask (rows x cols); indices and
+ *          rowptr are not written (may be NULL).
+ *   dev_tiles: the kernels' private layout (pre-decoded gather offsets for
+ *     the given conv geometry, MFMA-ordered weight tiles, channel-chunk
+ *     table), dev_tile_bytes from bsp_packed_sizes.  It is only valid for the
+ *     same scheme, dtype and geometry (conv_or_null) at bsp_conv2d /
+ *     bsp_linear time; a mismatch is detected on the device and the output
+ *     is filled with NaN.
+ * Returns BSP_EUNSUPPORTED when one 32-wide step of a kept-column list spans
+ * more input channels than one LDS stage holds (only possible for very
+ * sparse whole-width column blocks of 1x1 convs). */
+bsp_status bsp_pack(const bsp_scheme *scheme, bsp_dtype wdt, const void *w, const uint8_t *mask,
+                    void *values, int32_t *indices, int32_t *rowptr, void *dev_tiles,
+                    const bsp_conv_shape *conv_or_null, void *stream);
+
+/* Inverse of the canonical packing: w_masked_out (rows x cols, dtype) =
+ * W * mask, bit-exact.  Async.  For tests and checkpoints. */
+bsp_status bsp_unpack(const bsp_scheme *scheme, bsp_dtype wdt, const void *values,
+                      const int32_t *indices, const int32_t *rowptr, void *w_masked_out,
+                      void *stream);
+
+/* Forward of a pruned conv layer (the layer of Sec. 4.2 with pruned weights):
+ *   y[n,o,oh,ow] = bias[o] + sum_{kept (c,r,s)} W[o,c,r,s] * x[n,c,oh*sh-ph+r,ow*sw-pw+s]
+ * then ReLU if relu != 0.  x: NCHW of in_dt (must equal the packed dtype);
+ * y: NCHW [n][rows][Ho][Wo] of out_dt (fp32 accumulation, RNE to bf16).
+ * Only kept weights are multiplied; inputs must be finite (a removed weight
+ * is never multiplied, so Inf/NaN inputs do not propagate through it).
+ * bias may be NULL.  Async. */
+bsp_status bsp_conv2d(const bsp_scheme *scheme, const bsp_conv_shape *shape, bsp_dtype in_dt,
+                      bsp_dtype out_dt, const void *x, const void *dev_tiles,
+                      const float *bias_or_null, int32_t relu, void *y, void *stream);
+
+/* Forward of a pruned FC layer on feature-major activations:
+ *   y[o][b] = bias[o] + sum_{kept k} W[o][k] * x[k][b], then ReLU if relu.
+ * x: [cols][batch], y: [rows][batch].  dev_tiles packed with conv_or_null =
+ * NULL.  Async. */
+bsp_status bsp_linear(const bsp_scheme *scheme, int32_t batch, bsp_dtype in_dt, bsp_dtype out_dt,
+                      const void *x, const void *dev_tiles, const float *bias_or_null,
+                      int32_t relu, void *y, void *stream);
+
+/* 2x2 max pooling, stride 2 (floor), NCHW, same dtype in and out: the glue
+ * between VGG-16 stages.  y is [n][c][h/2][w/2].  Async. */
+bsp_status bsp_maxpool2x2(bsp_dtype dt, int32_t n, int32_t c, int32_t h, int32_t w,
+                          const void *x, void *y, void *stream);
+
+/* Static string for a status code. */
+const char *bsp_status_string(bsp_status status);
+
+/* Library version, e.g. 100 for 0.1.0. */
+int32_t bsp_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* BSP_H */

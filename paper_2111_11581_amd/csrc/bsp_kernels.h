@@ -1,0 +1,25 @@
+// Launchers of the device kernels (host side).  All take a validated plan.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include "bsp_common.h"
+
+namespace bsp {
+
+hipError_t launch_prune(const Plan &p, const void *w, uint8_t *mask, hipStream_t st);
+
+// Synchronous: returns BSP_OK, BSP_EMASK, BSP_EUNSUPPORTED or BSP_EDEVICE.
+bsp_status run_pack(const Plan &p, const void *w, const uint8_t *mask, void *values,
+                    int32_t *indices, int32_t *rowptr, uint8_t *tiles, hipStream_t st);
+
+hipError_t launch_unpack(const Plan &p, const void *values, const int32_t *indices,
+                         const int32_t *rowptr, void *w_out, hipStream_t st);
+
+hipError_t launch_conv(const Plan &p, int n, const void *x, const uint8_t *tiles,
+                       const float *bias, int relu, int out_bf16, void *y, hipStream_t st);
+
+hipError_t launch_maxpool2x2(int dt, int n, int c, int h, int w, const void *x, void *y,
+                             hipStream_t st);
+
+}  // namespace bsp

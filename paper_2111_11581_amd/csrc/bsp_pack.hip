@@ -1,0 +1,407 @@
+// Packing of pruned weights on the device.
+//
+// Canonical packing (checked bit-exact against the oracle): per block-row kept
+// column lists (column pruning) or per block kept row lists (row pruning) plus the
+// kept values - the same information as the paper's compact storage of Sec. 4.3
+// (kept weights and the column indices shared by the rows of a block), in this
+// library's own layout.  The private dev_tiles layout for the forward kernel adds
+// pre-decoded LDS gather offsets per kept column, MFMA-ordered weight tiles (8
+// consecutive kept columns per lane, zero padded to steps of 32), and the channel
+// windows ("chunks") the forward stages through LDS.
+#include <hip/hip_runtime.h>
+
+#include "bsp_kernels.h"
+
+namespace bsp {
+
+namespace {
+
+constexpr int kFlagOffset = 32;   // TileHeader::reserved[0]: error flag
+constexpr int kCountOffset = 36;  // TileHeader::reserved[1]: kept counter
+
+__device__ __forceinline__ int block_excl_scan_256(int v, int *wave_tot, int *total) {
+    // exclusive prefix of v (0/1) over a 256-thread workgroup, using ballots
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    const unsigned long long b = __ballot(v != 0);
+    const int pre = __builtin_amdgcn_mbcnt_hi((uint32_t)(b >> 32),
+                                              __builtin_amdgcn_mbcnt_lo((uint32_t)b, 0));
+    if (lane == 0) wave_tot[wv] = __popcll(b);
+    __syncthreads();
+    int off = 0, tot = 0;
+    for (int i = 0; i < 4; ++i) {
+        if (i < wv) off += wave_tot[i];
+        tot += wave_tot[i];
+    }
+    *total = tot;
+    __syncthreads();
+    return off + pre;
+}
+
+__global__ void k_validate_blocks(const uint8_t *__restrict__ mask, int R, int C, int bh, int bw,
+                                  int nbc, int col, int rate, int *flag) {
+    __shared__ int cnt;
+    if (threadIdx.x == 0) cnt = 0;
+    __syncthreads();
+    const int b = blockIdx.x;
+    const int bi = b / nbc, bj = b - bi * nbc;
+    const int r0 = bi * bh, r1 = min(R, r0 + bh), c0 = bj * bw, c1 = min(C, c0 + bw);
+    const int ng = col ? c1 - c0 : r1 - r0;
+    int bad = 0, local = 0;
+    for (int g = threadIdx.x; g < ng; g += blockDim.x) {
+        if (col) {
+            const uint8_t v0 = mask[(size_t)r0 * C + c0 + g];
+            bad |= v0 > 1;
+            for (int p = r0 + 1; p < r1; ++p) bad |= mask[(size_t)p * C + c0 + g] != v0;
+            local += v0 == 1;
+        } else {
+            const uint8_t *mr = mask + (size_t)(r0 + g) * C;
+            const uint8_t v0 = mr[c0];
+            bad |= v0 > 1;
+            for (int q = c0 + 1; q < c1; ++q) bad |= mr[q] != v0;
+            local += v0 == 1;
+        }
+    }
+    if (local) atomicAdd(&cnt, local);
+    if (bad) atomicOr(flag, 1);
+    __syncthreads();
+    if (threadIdx.x == 0 && cnt != (ng + rate - 1) / rate) atomicOr(flag, 1);
+}
+
+__global__ void k_validate_all(const uint8_t *__restrict__ mask, size_t n, int need_ones,
+                               int *flag, unsigned int *count) {
+    int bad = 0;
+    unsigned int c = 0;
+    for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n;
+         i += (size_t)gridDim.x * blockDim.x) {
+        const uint8_t v = mask[i];
+        bad |= v > 1;
+        if (need_ones) bad |= v != 1;
+        c += v == 1;
+    }
+    if (bad) atomicOr(flag, 1);
+    if (c) atomicAdd(count, c);
+}
+
+__global__ void k_check_count(const unsigned int *count, unsigned int k, int *flag) {
+    if (*count != k) atomicOr(flag, 1);
+}
+
+__global__ void k_col_lists(const uint8_t *__restrict__ mask, int R, int C, int bh, int nbr, int L,
+                            int32_t *__restrict__ indices, int32_t *__restrict__ rowptr,
+                            int *flag) {
+    __shared__ int wave_tot[4];
+    const int i = blockIdx.x;
+    const uint8_t *mr = mask + (size_t)i * bh * C;
+    int base = 0;
+    for (int q0 = 0; q0 < C; q0 += 256) {
+        const int q = q0 + threadIdx.x;
+        const int v = q < C ? mr[q] : 0;
+        int tot;
+        const int pos = base + block_excl_scan_256(v, wave_tot, &tot);
+        if (v) {
+            if (pos < L) indices[(size_t)i * L + pos] = q;
+            else atomicOr(flag, 1);
+        }
+        base += tot;
+    }
+    if (threadIdx.x == 0) {
+        if (base != L) atomicOr(flag, 1);
+        if (rowptr) {
+            rowptr[i] = i * L;
+            if (i == nbr - 1) rowptr[nbr] = nbr * L;
+        }
+    }
+}
+
+template <typename E>
+__global__ void k_col_values(const E *__restrict__ w, const int32_t *__restrict__ indices,
+                             E *__restrict__ values, int R, int C, int L, int bh) {
+    const size_t n = (size_t)R * L;
+    for (size_t e = blockIdx.x * (size_t)blockDim.x + threadIdx.x; e < n;
+         e += (size_t)gridDim.x * blockDim.x) {
+        const int row = (int)(e / L), t = (int)(e - (size_t)row * L);
+        const int i = row / bh;
+        values[e] = w[(size_t)row * C + indices[(size_t)i * L + t]];
+    }
+}
+
+__global__ void k_row_lists(const uint8_t *__restrict__ mask, int R, int C, int bh, int bw, int nbc,
+                            int rate, int32_t *__restrict__ indices, int32_t *__restrict__ rowptr,
+                            int *flag) {
+    __shared__ int wave_tot[4];
+    const int b = blockIdx.x;
+    const int bi = b / nbc, bj = b - bi * nbc;
+    const int r0 = bi * bh, r1 = min(R, r0 + bh), c0 = bj * bw;
+    const int kf = (bh + rate - 1) / rate, ki = (r1 - r0 + rate - 1) / rate;
+    const int off = bi * kf * nbc + bj * ki;
+    int base = 0;
+    for (int p0 = r0; p0 < r1; p0 += 256) {
+        const int p = p0 + threadIdx.x;
+        const int v = p < r1 ? mask[(size_t)p * C + c0] : 0;
+        int tot;
+        const int t = base + block_excl_scan_256(v, wave_tot, &tot);
+        if (v) {
+            if (t < ki) indices[off + t] = p;
+            else atomicOr(flag, 1);
+        }
+        base += tot;
+    }
+    if (threadIdx.x == 0) {
+        if (base != ki) atomicOr(flag, 1);
+        rowptr[b] = off;
+        if (b == (int)gridDim.x - 1) rowptr[b + 1] = off + ki;
+    }
+}
+
+template <typename E>
+__global__ void k_row_values(const E *__restrict__ w, const int32_t *__restrict__ indices,
+                             E *__restrict__ values, int R, int C, int bh, int bw, int nbc,
+                             int rate) {
+    const int b = blockIdx.x;
+    const int bi = b / nbc, bj = b - bi * nbc;
+    const int r0 = bi * bh, r1 = min(R, r0 + bh), c0 = bj * bw, c1 = min(C, c0 + bw);
+    const int wj = c1 - c0;
+    const int kf = (bh + rate - 1) / rate, ki = (r1 - r0 + rate - 1) / rate;
+    const int off = bi * kf * nbc + bj * ki;
+    const size_t voff = (size_t)bi * kf * C + (size_t)ki * bj * bw;
+    for (int e = threadIdx.x; e < ki * wj; e += blockDim.x) {
+        const int t = e / wj, q = e - t * wj;
+        values[voff + e] = w[(size_t)indices[off + t] * C + c0 + q];
+    }
+}
+
+template <typename E>
+__global__ void k_masked_copy(const E *__restrict__ w, const uint8_t *__restrict__ mask,
+                              E *__restrict__ out, size_t n) {
+    for (size_t e = blockIdx.x * (size_t)blockDim.x + threadIdx.x; e < n;
+         e += (size_t)gridDim.x * blockDim.x)
+        out[e] = mask[e] ? w[e] : (E)0;
+}
+
+struct DescArgs {
+    int shared, n_groups, L, LP, C, KH, KW, CH_STRIDE, RL, LEFT;
+};
+
+__global__ void k_desc(DescArgs a, const int32_t *__restrict__ indices, int32_t *__restrict__ desc) {
+    const int n = a.n_groups * a.LP;
+    const int khw = a.KH * a.KW;
+    for (int e = blockIdx.x * blockDim.x + threadIdx.x; e < n; e += gridDim.x * blockDim.x) {
+        const int g = e / a.LP, t = e - g * a.LP;
+        const int tt = t < a.L ? t : a.L - 1;  // padding repeats the last kept column
+        const int q = a.shared ? tt : indices[(size_t)g * a.L + tt];
+        const int c = q / khw, rs = q - c * khw;
+        const int r = rs / a.KW, s = rs - r * a.KW;
+        desc[e] = c * a.CH_STRIDE + r * a.RL + s + a.LEFT;
+    }
+}
+
+struct ATileArgs {
+    int shared, n_groups, mt_per_group, group_rows, S, L, R, C;
+};
+
+template <typename E>
+__global__ void k_atiles(ATileArgs a, const E *__restrict__ w, const uint8_t *__restrict__ mask,
+                         const int32_t *__restrict__ indices, E *__restrict__ A) {
+    const int64_t per_mt = (int64_t)a.S * 512;
+    const int64_t n = (int64_t)a.n_groups * a.mt_per_group * per_mt;
+    for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < n;
+         e += (int64_t)gridDim.x * blockDim.x) {
+        const int j = (int)(e & 7), lane = (int)((e >> 3) & 63);
+        const int64_t rest = e >> 9;
+        const int s = (int)(rest % a.S);
+        const int64_t gm = rest / a.S;
+        const int mt = (int)(gm % a.mt_per_group);
+        const int g = (int)(gm / a.mt_per_group);
+        const int rig = mt * 16 + (lane & 15);
+        const int row = g * a.group_rows + rig;
+        const int t = s * 32 + 8 * (lane >> 4) + j;
+        E v = (E)0;
+        if (rig < a.group_rows && row < a.R && t < a.L) {
+            const int q = a.shared ? t : indices[(size_t)g * a.L + t];
+            const size_t wi = (size_t)row * a.C + q;
+            if (mask[wi]) v = w[wi];
+        }
+        A[e] = v;
+    }
+}
+
+__global__ void k_step_spans(const int32_t *__restrict__ desc, int n_groups, int LP, int S,
+                             int CH_STRIDE, int4 *table) {
+    for (int s = blockIdx.x * blockDim.x + threadIdx.x; s < S; s += gridDim.x * blockDim.x) {
+        int lo = 0x7fffffff, hi = -1;
+        for (int g = 0; g < n_groups; ++g) {
+            const int a = desc[(size_t)g * LP + 32 * s] / CH_STRIDE;
+            const int b = desc[(size_t)g * LP + 32 * s + 31] / CH_STRIDE;
+            lo = min(lo, a);
+            hi = max(hi, b);
+        }
+        table[s] = make_int4(lo, hi, 0, 0);
+    }
+}
+
+__global__ void k_build_chunks(int4 *table, int S, int CC, int *n_chunks, int *flag) {
+    extern __shared__ int spans[];  // 2*S
+    for (int s = threadIdx.x; s < S; s += blockDim.x) {
+        spans[2 * s] = table[s].x;
+        spans[2 * s + 1] = table[s].y;
+    }
+    __syncthreads();
+    if (threadIdx.x != 0) return;
+    int nc = 0, s = 0;
+    while (s < S) {
+        const int lo = spans[2 * s];
+        int hi = spans[2 * s + 1];
+        if (hi - lo + 1 > CC) {
+            atomicOr(flag, 2);
+            break;
+        }
+        int e = s + 1;
+        while (e < S) {
+            const int h2 = max(hi, spans[2 * e + 1]);
+            if (spans[2 * e] < lo || h2 - lo + 1 > CC) break;
+            hi = h2;
+            ++e;
+        }
+        table[nc++] = make_int4(s, e, lo, hi - lo + 1);
+        s = e;
+    }
+    *n_chunks = nc;
+}
+
+template <typename E>
+__global__ void k_fill(E *p, size_t n, E v) {
+    for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n;
+         i += (size_t)gridDim.x * blockDim.x)
+        p[i] = v;
+}
+
+template <typename E>
+__global__ void k_col_unpack(const E *__restrict__ values, const int32_t *__restrict__ indices,
+                             E *__restrict__ out, int R, int C, int L, int bh) {
+    const size_t n = (size_t)R * L;
+    for (size_t e = blockIdx.x * (size_t)blockDim.x + threadIdx.x; e < n;
+         e += (size_t)gridDim.x * blockDim.x) {
+        const int row = (int)(e / L), t = (int)(e - (size_t)row * L);
+        out[(size_t)row * C + indices[(size_t)(row / bh) * L + t]] = values[e];
+    }
+}
+
+template <typename E>
+__global__ void k_row_unpack(const E *__restrict__ values, const int32_t *__restrict__ indices,
+                             E *__restrict__ out, int R, int C, int bh, int bw, int nbc, int rate) {
+    const int b = blockIdx.x;
+    const int bi = b / nbc, bj = b - bi * nbc;
+    const int r0 = bi * bh, r1 = min(R, r0 + bh), c0 = bj * bw, c1 = min(C, c0 + bw);
+    const int wj = c1 - c0;
+    const int kf = (bh + rate - 1) / rate, ki = (r1 - r0 + rate - 1) / rate;
+    const int off = bi * kf * nbc + bj * ki;
+    const size_t voff = (size_t)bi * kf * C + (size_t)ki * bj * bw;
+    for (int e = threadIdx.x; e < ki * wj; e += blockDim.x) {
+        const int t = e / wj, q = e - t * wj;
+        out[(size_t)indices[off + t] * C + c0 + q] = values[voff + e];
+    }
+}
+
+inline int grid_for(size_t n) { return (int)std::max<size_t>(1, std::min<size_t>(8192, (n + 255) / 256)); }
+
+template <typename E>
+bsp_status pack_t(const Plan &p, const E *w, const uint8_t *mask, E *values, int32_t *indices,
+                  int32_t *rowptr, uint8_t *tiles, hipStream_t st) {
+    int *flag = (int *)(tiles + kFlagOffset);
+    unsigned int *count = (unsigned int *)(tiles + kCountOffset);
+    TileHeader h;
+    memset(&h, 0, sizeof(h));
+    h.magic = kMagic;
+    h.fp_lo = (uint32_t)p.fingerprint;
+    h.fp_hi = (uint32_t)(p.fingerprint >> 32);
+    h.n_groups = p.n_groups;
+    h.mt_per_group = p.mt_per_group;
+    h.LP = p.LP;
+    h.S = p.S;
+    if (hipMemcpyAsync(tiles, &h, sizeof(h), hipMemcpyHostToDevice, st) != hipSuccess)
+        return BSP_EDEVICE;
+    const size_t n = (size_t)p.R * p.C;
+    // 1. validate the block structure
+    if (p.reg == BSP_COL || p.reg == BSP_ROW) {
+        const int ng = p.reg == BSP_COL ? p.bw_eff : p.bh_eff;
+        const int threads = std::min(256, ((ng + 63) / 64) * 64);
+        k_validate_blocks<<<p.nbr * p.nbc, threads, 0, st>>>(mask, p.R, p.C, p.bh_eff, p.bw_eff,
+                                                            p.nbc, p.reg == BSP_COL, p.rate, flag);
+    } else {
+        k_validate_all<<<grid_for(n), 256, 0, st>>>(mask, n, p.reg == BSP_DENSE, flag, count);
+        if (p.reg == BSP_UNSTRUCTURED)
+            k_check_count<<<1, 1, 0, st>>>(count, (unsigned int)((n + p.rate - 1) / p.rate), flag);
+    }
+    int hflag = 0;
+    if (hipMemcpyAsync(&hflag, flag, sizeof(int), hipMemcpyDeviceToHost, st) != hipSuccess ||
+        hipStreamSynchronize(st) != hipSuccess)
+        return BSP_EDEVICE;
+    if (hflag) return BSP_EMASK;
+    // 2. canonical packing
+    if (p.reg == BSP_COL) {
+        k_col_lists<<<p.nbr, 256, 0, st>>>(mask, p.R, p.C, p.bh_eff, p.nbr, p.L, indices, rowptr, flag);
+        k_col_values<E><<<grid_for((size_t)p.R * p.L), 256, 0, st>>>(w, indices, values, p.R, p.C,
+                                                                     p.L, p.bh_eff);
+    } else if (p.reg == BSP_ROW) {
+        k_row_lists<<<p.nbr * p.nbc, 256, 0, st>>>(mask, p.R, p.C, p.bh_eff, p.bw_eff, p.nbc,
+                                                    p.rate, indices, rowptr, flag);
+        k_row_values<E><<<p.nbr * p.nbc, 256, 0, st>>>(w, indices, values, p.R, p.C, p.bh_eff,
+                                                        p.bw_eff, p.nbc, p.rate);
+    } else {
+        k_masked_copy<E><<<grid_for(n), 256, 0, st>>>(w, mask, values, n);
+    }
+    // 3. forward layout
+    int32_t *desc = (int32_t *)(tiles + p.off_desc);
+    DescArgs da{p.shared, p.n_groups, p.L, p.LP, p.C, p.KH, p.KW, p.CH_STRIDE, p.RL, p.LEFT};
+    k_desc<<<grid_for((size_t)p.n_groups * p.LP), 256, 0, st>>>(da, indices, desc);
+    ATileArgs aa{p.shared, p.n_groups, p.mt_per_group, p.group_rows, p.S, p.L, p.R, p.C};
+    const size_t na = (size_t)p.n_groups * p.mt_per_group * p.S * 512;
+    k_atiles<E><<<grid_for(na), 256, 0, st>>>(aa, w, mask, indices, (E *)(tiles + p.off_a));
+    int4 *table = (int4 *)(tiles + p.off_chunks);
+    k_step_spans<<<grid_for(p.S), 256, 0, st>>>(desc, p.n_groups, p.LP, p.S, p.CH_STRIDE, table);
+    k_build_chunks<<<1, 256, sizeof(int) * 2 * p.S, st>>>(
+        table, p.S, p.CC, (int *)(tiles + offsetof(TileHeader, n_chunks)), flag);
+    if (hipGetLastError() != hipSuccess) return BSP_EDEVICE;
+    if (hipMemcpyAsync(&hflag, flag, sizeof(int), hipMemcpyDeviceToHost, st) != hipSuccess ||
+        hipStreamSynchronize(st) != hipSuccess)
+        return BSP_EDEVICE;
+    if (hflag & 2) return BSP_EUNSUPPORTED;
+    if (hflag) return BSP_EMASK;
+    return BSP_OK;
+}
+
+template <typename E>
+hipError_t unpack_t(const Plan &p, const E *values, const int32_t *indices, E *out, hipStream_t st) {
+    const size_t n = (size_t)p.R * p.C;
+    if (p.reg == BSP_DENSE || p.reg == BSP_UNSTRUCTURED) {
+        return hipMemcpyAsync(out, values, n * sizeof(E), hipMemcpyDeviceToDevice, st);
+    }
+    k_fill<E><<<grid_for(n), 256, 0, st>>>(out, n, (E)0);
+    if (p.reg == BSP_COL)
+        k_col_unpack<E><<<grid_for((size_t)p.R * p.L), 256, 0, st>>>(values, indices, out, p.R, p.C,
+                                                                     p.L, p.bh_eff);
+    else
+        k_row_unpack<E><<<p.nbr * p.nbc, 256, 0, st>>>(values, indices, out, p.R, p.C, p.bh_eff,
+                                                        p.bw_eff, p.nbc, p.rate);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+bsp_status run_pack(const Plan &p, const void *w, const uint8_t *mask, void *values,
+                    int32_t *indices, int32_t *rowptr, uint8_t *tiles, hipStream_t st) {
+    if (p.dt == BSP_F32)
+        return pack_t<float>(p, (const float *)w, mask, (float *)values, indices, rowptr, tiles, st);
+    return pack_t<uint16_t>(p, (const uint16_t *)w, mask, (uint16_t *)values, indices, rowptr,
+                            tiles, st);
+}
+
+hipError_t launch_unpack(const Plan &p, const void *values, const int32_t *indices,
+                         const int32_t *rowptr, void *w_out, hipStream_t st) {
+    (void)rowptr;
+    if (p.dt == BSP_F32)
+        return unpack_t<float>(p, (const float *)values, indices, (float *)w_out, st);
+    return unpack_t<uint16_t>(p, (const uint16_t *)values, indices, (uint16_t *)w_out, st);
+}
+
+}  // namespace bsp

@@ -1,0 +1,246 @@
+// Pruning masks on the device.
+//
+// Block row / column pruning (Sec. 4.1.1): one workgroup per block computes the
+// squared Frobenius norm of each of the block's columns (Eq. 3) or rows (Eq. 2) in
+// fp64, summed in ascending index order (the squares of fp32 / bf16 values are exact
+// in fp64, so fma(v, v, s) rounds exactly like s + v*v), then keeps the
+// ceil(extent / rate) largest (one-shot magnitude selection, Sec. 5.1) by counting,
+// for each group, the groups that beat it (larger score, or equal score and lower
+// index).  Unstructured pruning (Sec. 2.1.1) keeps the ceil(R*C/rate) largest |w| of
+// the layer: a most-significant-digit radix select over the bit patterns of |w|
+// (order preserving for non-negative floats) finds the threshold, and entries equal
+// to it are admitted in flat-index order.
+#include <hip/hip_runtime.h>
+
+#include "bsp_kernels.h"
+
+namespace bsp {
+
+__device__ __forceinline__ double ld_f64(const float *w, size_t i) { return (double)w[i]; }
+__device__ __forceinline__ double ld_f64(const uint16_t *w, size_t i) {
+    return (double)__uint_as_float((uint32_t)w[i] << 16);
+}
+__device__ __forceinline__ uint32_t abs_key(const float *w, size_t i) {
+    return __float_as_uint(w[i]) & 0x7fffffffu;
+}
+__device__ __forceinline__ uint32_t abs_key(const uint16_t *w, size_t i) {
+    return ((uint32_t)w[i] & 0x7fffu) << 16;
+}
+
+template <typename E>
+__global__ void k_prune_blocks(const E *__restrict__ w, uint8_t *__restrict__ mask, int R, int C,
+                               int bh, int bw, int nbc, int col, int rate) {
+    extern __shared__ double sc[];
+    const int b = blockIdx.x;
+    const int bi = b / nbc, bj = b - bi * nbc;
+    const int r0 = bi * bh, r1 = min(R, r0 + bh), c0 = bj * bw, c1 = min(C, c0 + bw);
+    const int ng = col ? c1 - c0 : r1 - r0;
+    const int k = (ng + rate - 1) / rate;
+    for (int g = threadIdx.x; g < ng; g += blockDim.x) {
+        double s = 0.0;
+        if (col) {
+            for (int p = r0; p < r1; ++p) {
+                const double v = ld_f64(w, (size_t)p * C + c0 + g);
+                s = fma(v, v, s);
+            }
+        } else {
+            const size_t row = (size_t)(r0 + g) * C;
+            for (int q = c0; q < c1; ++q) {
+                const double v = ld_f64(w, row + q);
+                s = fma(v, v, s);
+            }
+        }
+        sc[g] = s;
+    }
+    __syncthreads();
+    for (int g = threadIdx.x; g < ng; g += blockDim.x) {
+        const double s = sc[g];
+        int rank = 0;
+        for (int h = 0; h < ng; ++h) {
+            const double t = sc[h];
+            rank += (t > s) || (t == s && h < g);
+        }
+        const uint8_t keep = rank < k ? 1 : 0;
+        if (col) {
+            for (int p = r0; p < r1; ++p) mask[(size_t)p * C + c0 + g] = keep;
+        } else {
+            uint8_t *mr = mask + (size_t)(r0 + g) * C;
+            for (int q = c0; q < c1; ++q) mr[q] = keep;
+        }
+    }
+}
+
+__global__ void k_fill_u8(uint8_t *p, size_t n, uint8_t v) {
+    for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n;
+         i += (size_t)gridDim.x * blockDim.x)
+        p[i] = v;
+}
+
+// ---- unstructured: radix select ---------------------------------------------------
+struct SelState {
+    uint32_t prefix, pmask;
+    uint32_t remaining;   // how many keys still to take at or below the current prefix
+    uint32_t pad;
+    uint32_t hist[256];
+};
+
+__global__ void k_sel_init(SelState *st, uint32_t k) {
+    const int t = threadIdx.x;
+    st->hist[t] = 0;
+    if (t == 0) {
+        st->prefix = 0;
+        st->pmask = 0;
+        st->remaining = k;
+    }
+}
+
+template <typename E>
+__global__ void k_sel_hist(const E *__restrict__ w, size_t n, SelState *st, int shift) {
+    __shared__ uint32_t h[256];
+    h[threadIdx.x] = 0;
+    __syncthreads();
+    const uint32_t prefix = st->prefix, pmask = st->pmask;
+    for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n;
+         i += (size_t)gridDim.x * blockDim.x) {
+        const uint32_t key = abs_key(w, i);
+        if ((key & pmask) == prefix) atomicAdd(&h[(key >> shift) & 255u], 1u);
+    }
+    __syncthreads();
+    if (h[threadIdx.x]) atomicAdd(&st->hist[threadIdx.x], h[threadIdx.x]);
+}
+
+__global__ void k_sel_pick(SelState *st, int shift) {
+    // single thread: walk the digits from the largest down
+    uint32_t above = 0, rem = st->remaining;
+    int chosen = 0;
+    for (int b = 255; b >= 0; --b) {
+        const uint32_t c = st->hist[b];
+        if (above + c >= rem) {
+            chosen = b;
+            break;
+        }
+        above += c;
+    }
+    st->remaining = rem - above;
+    st->prefix |= (uint32_t)chosen << shift;
+    st->pmask |= 255u << shift;
+    for (int b = 0; b < 256; ++b) st->hist[b] = 0;
+}
+
+constexpr int kSelChunk = 4096;  // elements per workgroup in the final pass
+
+template <typename E>
+__global__ void k_sel_count_eq(const E *__restrict__ w, size_t n, const SelState *st,
+                               uint32_t *chunk_cnt) {
+    __shared__ uint32_t cnt;
+    if (threadIdx.x == 0) cnt = 0;
+    __syncthreads();
+    const uint32_t thr = st->prefix;
+    const size_t base = (size_t)blockIdx.x * kSelChunk;
+    uint32_t c = 0;
+    for (int j = threadIdx.x; j < kSelChunk; j += blockDim.x) {
+        const size_t i = base + j;
+        if (i < n && abs_key(w, i) == thr) ++c;
+    }
+    if (c) atomicAdd(&cnt, c);
+    __syncthreads();
+    if (threadIdx.x == 0) chunk_cnt[blockIdx.x] = cnt;
+}
+
+__global__ void k_sel_scan(uint32_t *chunk_cnt, int nchunks) {
+    uint32_t acc = 0;
+    for (int i = 0; i < nchunks; ++i) {
+        const uint32_t c = chunk_cnt[i];
+        chunk_cnt[i] = acc;
+        acc += c;
+    }
+}
+
+template <typename E>
+__global__ void k_sel_write(const E *__restrict__ w, size_t n, const SelState *st,
+                            const uint32_t *chunk_off, uint8_t *__restrict__ mask) {
+    // 256 threads x 16 consecutive elements each = one chunk
+    __shared__ uint32_t pre[256];
+    const uint32_t thr = st->prefix, need = st->remaining;
+    const size_t base = (size_t)blockIdx.x * kSelChunk + (size_t)threadIdx.x * 16;
+    uint32_t c = 0;
+    for (int j = 0; j < 16; ++j) {
+        const size_t i = base + j;
+        if (i < n && abs_key(w, i) == thr) ++c;
+    }
+    pre[threadIdx.x] = c;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        uint32_t acc = 0;
+        for (int t = 0; t < 256; ++t) {
+            const uint32_t v = pre[t];
+            pre[t] = acc;
+            acc += v;
+        }
+    }
+    __syncthreads();
+    uint32_t rank = chunk_off[blockIdx.x] + pre[threadIdx.x];
+    for (int j = 0; j < 16; ++j) {
+        const size_t i = base + j;
+        if (i >= n) break;
+        const uint32_t key = abs_key(w, i);
+        uint8_t keep = 0;
+        if (key > thr) keep = 1;
+        else if (key == thr) keep = (rank++ < need) ? 1 : 0;
+        mask[i] = keep;
+    }
+}
+
+template <typename E>
+static hipError_t prune_unstructured(const Plan &p, const E *w, uint8_t *mask, hipStream_t st) {
+    const size_t n = (size_t)p.R * p.C;
+    const uint32_t k = (uint32_t)((n + p.rate - 1) / p.rate);
+    const int nchunks = (int)((n + kSelChunk - 1) / kSelChunk);
+    void *scr = nullptr;
+    const size_t bytes = sizeof(SelState) + sizeof(uint32_t) * (size_t)nchunks;
+    hipError_t e = hipMallocAsync(&scr, bytes, st);
+    if (e != hipSuccess) return e;
+    SelState *s = (SelState *)scr;
+    uint32_t *cc = (uint32_t *)((char *)scr + sizeof(SelState));
+    const int hblocks = (int)std::min<size_t>(2048, (n + 255) / 256);
+    k_sel_init<<<1, 256, 0, st>>>(s, k);
+    for (int pass = 0; pass < 4; ++pass) {
+        const int shift = 24 - 8 * pass;
+        k_sel_hist<E><<<hblocks, 256, 0, st>>>(w, n, s, shift);
+        k_sel_pick<<<1, 1, 0, st>>>(s, shift);
+    }
+    k_sel_count_eq<E><<<nchunks, 256, 0, st>>>(w, n, s, cc);
+    k_sel_scan<<<1, 1, 0, st>>>(cc, nchunks);
+    k_sel_write<E><<<nchunks, 256, 0, st>>>(w, n, s, cc, mask);
+    e = hipGetLastError();
+    hipError_t e2 = hipFreeAsync(scr, st);
+    return e != hipSuccess ? e : e2;
+}
+
+hipError_t launch_prune(const Plan &p, const void *w, uint8_t *mask, hipStream_t st) {
+    const size_t n = (size_t)p.R * p.C;
+    if (p.reg == BSP_DENSE) {
+        const int blocks = (int)std::min<size_t>(4096, (n + 255) / 256);
+        k_fill_u8<<<blocks, 256, 0, st>>>(mask, n, 1);
+        return hipGetLastError();
+    }
+    if (p.reg == BSP_UNSTRUCTURED) {
+        return p.dt == BSP_F32 ? prune_unstructured(p, (const float *)w, mask, st)
+                               : prune_unstructured(p, (const uint16_t *)w, mask, st);
+    }
+    const int col = p.reg == BSP_COL;
+    const int ng_max = col ? p.bw_eff : p.bh_eff;
+    const int threads = std::min(256, ((ng_max + 63) / 64) * 64);
+    const size_t lds = sizeof(double) * (size_t)ng_max;
+    const int blocks = p.nbr * p.nbc;
+    if (p.dt == BSP_F32)
+        k_prune_blocks<float><<<blocks, threads, lds, st>>>((const float *)w, mask, p.R, p.C,
+                                                            p.bh_eff, p.bw_eff, p.nbc, col, p.rate);
+    else
+        k_prune_blocks<uint16_t><<<blocks, threads, lds, st>>>((const uint16_t *)w, mask, p.R, p.C,
+                                                               p.bh_eff, p.bw_eff, p.nbc, col,
+                                                               p.rate);
+    return hipGetLastError();
+}
+
+}  // namespace bsp

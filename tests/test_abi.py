@@ -1,0 +1,131 @@
+"""The C-ABI library loads and exports every declared symbol; host-only logic
+(sizes, argument validation, fast division, row staging) is right.  CPU only:
+no call here launches a kernel."""
+
+import ctypes
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "bsp.h")
+
+
+@pytest.fixture(scope="module")
+def bsp():
+    import paper_2111_11581_amd as B
+    if not os.path.exists(B.lib_path()):
+        from paper_2111_11581_amd import build
+        build.build()
+    B.lib()
+    return B
+
+
+def declared_symbols():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(bsp_[a-z0-9_]+)\s*\(", src)))
+
+
+def test_every_declared_symbol_is_exported(bsp):
+    syms = declared_symbols()
+    assert len(syms) >= 9
+    for s in syms:
+        assert hasattr(bsp.lib(), s), s
+
+
+def test_status_strings_and_version(bsp):
+    assert bsp.bsp_status_string(0) == "ok"
+    assert "block structure" in bsp.bsp_status_string(-4)
+    assert bsp.bsp_version() == 100
+
+
+def _sizes_from_oracle(R, C, bh, bw, reg, rate):
+    from oracle import prune as OP
+    w = np.random.default_rng(R + C).standard_normal((R, C))
+    m = OP.prune_mask(w, bh, bw, reg, rate)
+    pk = OP.pack(w.astype(np.float32), m, bh, bw, reg, rate)
+    return pk["values"].size, pk["indices"].size, pk["rowptr"].size
+
+
+@pytest.mark.parametrize("R,C,bh,bw,reg,rate", [
+    (64, 576, 16, 16, 1, 4), (64, 576, 8, 16, 1, 8), (256, 64, 32, 32, 0, 2), (37, 53, 8, 16, 1, 3),
+    (37, 53, 8, 16, 0, 3), (40, 40, 0, 0, 1, 4), (40, 40, 0, 0, 0, 4), (96, 100, 32, 32, 1, 10),
+    (64, 147, 0, 0, 3, 1), (30, 20, 1, 1, 2, 4)])
+def test_packed_sizes_match_oracle_packing(bsp, R, C, bh, bw, reg, rate):
+    s = bsp.Scheme(R, C, bh, bw, reg, rate)
+    nv, ni, nr, nb = bsp.bsp_packed_sizes(s, None, bsp.BF16)
+    assert (nv, ni, nr) == _sizes_from_oracle(R, C, bh, bw, reg, rate)
+    assert nb > 256
+
+
+def test_argument_errors_are_reported_before_any_launch(bsp):
+    L = bsp.lib()
+    s = bsp.Scheme(64, 576, 16, 16, 1, 4)
+    conv = bsp.ConvShape(1, 64, 32, 32, 3, 3, 1, 1, 1, 1)
+    EINVAL = -1
+    # null pointers
+    assert L.bsp_prune(ctypes.byref(s), 1, None, None, None) == EINVAL
+    assert L.bsp_conv2d(ctypes.byref(s), ctypes.byref(conv), 1, 1, None, None, None, 0, None, None) == EINVAL
+    # bad scheme: rate 0, negative block, bad regularity
+    for bad in (bsp.Scheme(64, 576, 16, 16, 1, 0), bsp.Scheme(64, 576, -1, 16, 1, 4),
+                bsp.Scheme(64, 576, 16, 16, 7, 4), bsp.Scheme(0, 576, 16, 16, 1, 4)):
+        out = [ctypes.c_int64() for _ in range(4)]
+        assert L.bsp_packed_sizes(ctypes.byref(bad), None, 1, *[ctypes.byref(o) for o in out]) == EINVAL
+    # conv geometry that does not match the GEMM form (cols != cin*kh*kw)
+    wrong = bsp.ConvShape(1, 32, 32, 32, 3, 3, 1, 1, 1, 1)
+    out = [ctypes.c_int64() for _ in range(4)]
+    assert L.bsp_packed_sizes(ctypes.byref(s), ctypes.byref(wrong), 1, *[ctypes.byref(o) for o in out]) == EINVAL
+    # bad dtype
+    assert L.bsp_packed_sizes(ctypes.byref(s), None, 5, *[ctypes.byref(o) for o in out]) == EINVAL
+    # bad maxpool sizes
+    assert L.bsp_maxpool2x2(1, -1, 1, 2, 2, ctypes.c_void_p(16), ctypes.c_void_p(16), None) == EINVAL
+
+
+HOST_TEST = r"""
+#include <cstdio>
+#include <cstdlib>
+#include "bsp_common.h"
+using namespace bsp;
+int main() {
+  // fast division against the hardware divide
+  unsigned ds[] = {1,2,3,5,7,9,10,13,49,56,64,100,196,3136,12544,65535,1000003};
+  for (unsigned d : ds) {
+    FastDiv f = make_fastdiv(d);
+    for (unsigned n = 0; n < 300000; n += 1) if (fdiv(n, f) != n / d) { printf("fdiv %u %u\n", n, d); return 1; }
+    for (unsigned n = 2147483647u; n > 2147000000u; n -= 97) if (fdiv(n, f) != n / d) { printf("fdiv hi %u %u\n", n, d); return 1; }
+  }
+  // slot staging: every (tile row, filter row) pair must name the input row it needs
+  int Hs[] = {7, 14, 28, 56, 3};
+  for (int Ho : Hs) for (int KH = 1; KH <= 7; KH += 2) for (int SH = 1; SH <= 2; ++SH)
+  for (int TRW : {1, 2, 4, 8, 16}) for (int g0 = 0; g0 < 3 * Ho; g0 += TRW) {
+    int rb[16], im[256], ih[256];
+    for (int i = 0; i < 256; ++i) { im[i] = -7; ih[i] = -7; }
+    int PH = KH / 2;
+    int ns = slot_layout(g0, TRW, Ho, 2 * Ho + 1, KH, SH, PH, rb, im, ih);
+    for (int tr = 0; tr < TRW; ++tr) {
+      int g = g0 + tr; if (g >= 2 * Ho + 1) { if (rb[tr] != 0) return 2; continue; }
+      int img = g / Ho, oh = g % Ho;
+      for (int r = 0; r < KH; ++r) {
+        int sl = rb[tr] + r;
+        if (sl >= ns || im[sl] != img || ih[sl] != oh * SH - PH + r) { printf("slot %d %d %d %d\n", Ho, KH, SH, g0); return 3; }
+      }
+    }
+  }
+  printf("ok\n");
+  return 0;
+}
+"""
+
+
+def test_fastdiv_and_slot_layout_host(tmp_path):
+    src = tmp_path / "t.cpp"
+    src.write_text(HOST_TEST)
+    exe = tmp_path / "t"
+    subprocess.run(["g++", "-O2", "-std=c++17", f"-I{ROOT}/include",
+                    f"-I{ROOT}/paper_2111_11581_amd/csrc", str(src), "-o", str(exe)], check=True)
+    r = subprocess.run([str(exe)], capture_output=True, text=True)
+    assert r.returncode == 0 and r.stdout.strip() == "ok", r.stdout

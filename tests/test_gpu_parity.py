@@ -1,0 +1,322 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle on the same
+seeded inputs.  Masks, indices, rowptr and packed values are compared bit-exact;
+outputs by relative L2 error: <= 1e-5 for fp32, <= 5e-3 for bf16 inputs with fp32
+accumulation (and bf16 output)."""
+
+import numpy as np
+import pytest
+
+from oracle import prune as OP
+from synthetic import workload, draw, draw_layer, seed_for, ConvLayer, LinearLayer, ROW, COL, UNSTRUCTURED, DENSE
+from tests.helpers import DT, to_dev, from_dev, as_f64, rel_l2, oracle_mask, oracle_conv, oracle_linear, out_to_f64
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"f32": 1e-5, "bf16": 5e-3}
+
+
+@pytest.fixture(scope="module")
+def B():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2111_11581_amd as B
+    B.lib()
+    return B
+
+
+def _layers():
+    from paper_2111_11581_amd import layers
+    return layers
+
+
+# ------------------------------------------------------------------ masks/pack ---
+MATS = [  # name, R, C, bh, bw, reg, rate, dtype, dist
+    ("c1 64x576 col16x16 r4 f32", 64, 576, 16, 16, COL, 4, "f32", ("normal", 0, 0.05)),
+    ("c2 256x1152 col8x16 r8", 256, 1152, 8, 16, COL, 8, "bf16", ("normal", 0, 0.04)),
+    ("c3 512x4608 col16x32 r4", 512, 4608, 16, 32, COL, 4, "bf16", ("normal", 0, 0.02)),
+    ("c3 2048x512 row32x32 r2", 2048, 512, 32, 32, ROW, 2, "bf16", ("normal", 0, 0.06)),
+    ("c4 4096x4096 col32x32 r10", 4096, 4096, 32, 32, COL, 10, "bf16", ("normal", 0, 0.02)),
+    ("c5 4x4 row r16", 256, 2304, 4, 4, ROW, 16, "bf16", ("normal", 0, 0.03)),
+    ("c5 64x64 col r2", 256, 2304, 64, 64, COL, 2, "bf16", ("normal", 0, 0.03)),
+    ("c5 whole col r8", 256, 2304, 0, 0, COL, 8, "bf16", ("normal", 0, 0.03)),
+    ("c5 whole row r4", 256, 2304, 0, 0, ROW, 4, "bf16", ("normal", 0, 0.03)),
+    ("c5 unstructured r4", 256, 2304, 1, 1, UNSTRUCTURED, 4, "bf16", ("normal", 0, 0.03)),
+    ("unstructured r3 f32", 100, 77, 1, 1, UNSTRUCTURED, 3, "f32", ("normal", 0, 1.0)),
+    ("dense", 64, 147, 0, 0, DENSE, 1, "bf16", ("normal", 0, 0.1)),
+    ("ragged col", 37, 53, 8, 16, COL, 3, "bf16", ("normal", 0, 1.0)),
+    ("ragged row", 37, 53, 8, 16, ROW, 3, "f32", ("normal", 0, 1.0)),
+    ("ties col", 48, 96, 16, 32, COL, 4, "bf16", ("ties",)),
+    ("ties row", 96, 48, 32, 16, ROW, 4, "f32", ("ties",)),
+    ("ties unstructured", 64, 64, 1, 1, UNSTRUCTURED, 5, "bf16", ("ties",)),
+]
+
+
+def _mat(i, R, C, dtype, dist):
+    if dist[0] == "ties":   # small integers: many exactly equal scores
+        a = np.random.default_rng(900 + i).integers(-2, 3, size=(R, C)).astype(np.float32)
+        return a if dtype == "f32" else (a.view(np.uint32) >> 16).astype(np.uint16)
+    return draw(seed_for(9, i, 1), (R, C), dist, dtype)
+
+
+@pytest.mark.parametrize("i", range(len(MATS)), ids=[m[0] for m in MATS])
+def test_prune_and_pack_bit_exact(B, i):
+    import torch
+    name, R, C, bh, bw, reg, rate, dtype, dist = MATS[i]
+    w = _mat(i, R, C, dtype, dist)
+    scheme = B.Scheme(R, C, bh, bw, reg, rate)
+    wd = to_dev(w, dtype)
+    layer = _layers().PackedLayer(scheme, DT[dtype], wd)
+    torch.cuda.synchronize()
+    m_ref = oracle_mask(w, dtype, scheme)
+    m_gpu = layer.mask.cpu().numpy().reshape(R, C)
+    assert np.array_equal(m_gpu, m_ref), f"{name}: {int((m_gpu != m_ref).sum())} mask entries differ"
+    pk = OP.pack(w, m_ref, bh, bw, reg, rate)
+    vals = from_dev(layer.values[:layer.n_values], dtype)
+    assert np.array_equal(vals.view(np.uint8), np.ascontiguousarray(pk["values"]).view(np.uint8))
+    if reg in (ROW, COL):
+        assert np.array_equal(layer.indices[:layer.n_indices].cpu().numpy(), pk["indices"])
+        assert np.array_equal(layer.rowptr[:layer.n_rowptr].cpu().numpy(), pk["rowptr"])
+    back = from_dev(layer.unpack(), dtype).reshape(R, C)
+    expect = np.where(m_ref == 1, w, np.zeros_like(w))
+    assert np.array_equal(back.view(np.uint8), expect.view(np.uint8))
+
+
+def test_pack_rejects_a_mask_without_block_structure(B):
+    import torch
+    R, C = 64, 256
+    w = draw(seed_for(9, 50, 1), (R, C), ("normal", 0, 1), "bf16")
+    m = oracle_mask(w, "bf16", B.Scheme(R, C, 16, 32, COL, 4))
+    m[5, np.nonzero(m[5])[0][0]] = 0         # one hole in a kept column
+    with pytest.raises(B.BspError) as e:
+        _layers().PackedLayer(B.Scheme(R, C, 16, 32, COL, 4), B.BF16, to_dev(w, "bf16"),
+                              mask=torch.from_numpy(m.reshape(-1)).cuda())
+    assert e.value.status == -4
+
+
+# ----------------------------------------------------------------------- conv ---
+def _conv_case(name, n, cin, h, w, cout, k, s, p, bh, bw, reg, rate, dtype="bf16", relu=False,
+               bias=False, out="same"):
+    return dict(name=name, layer=ConvLayer(name, n, cin, h, w, cout, k, k, s, s, p, p, bh, bw, reg, rate,
+                                           dtype, ("normal", 0, 1.0), ("normal", 0, (2.0 / (cin * k * k)) ** 0.5),
+                                           relu=relu), bias=bias, out=out)
+
+
+CONV_CASES = [
+    _conv_case("3x3 col16x32 r4 ragged-wo", 2, 64, 13, 11, 64, 3, 1, 1, 16, 32, COL, 4),
+    _conv_case("3x3 col16x32 r4 s2", 2, 64, 15, 15, 64, 3, 2, 1, 16, 32, COL, 4),
+    _conv_case("3x3 col8x16 r8 relu bias", 3, 64, 8, 8, 128, 3, 1, 1, 8, 16, COL, 8, relu=True, bias=True),
+    _conv_case("1x1 row32x32 r2", 2, 96, 14, 14, 160, 1, 1, 0, 32, 32, ROW, 2),
+    _conv_case("1x1 row32x32 r2 s2", 2, 64, 14, 14, 96, 1, 2, 0, 32, 32, ROW, 2),
+    _conv_case("7x7/2 dense", 1, 3, 40, 40, 64, 7, 2, 3, 0, 0, DENSE, 1),
+    _conv_case("5x5 pad2 col whole r4", 2, 20, 9, 9, 24, 5, 1, 2, 0, 0, COL, 4),
+    _conv_case("3x3 pad0 col4x4 r2 fp32out", 2, 8, 10, 12, 20, 3, 1, 0, 4, 4, COL, 2, out="f32"),
+    _conv_case("3x3 row whole r4 bias", 1, 16, 12, 12, 40, 3, 1, 1, 0, 0, ROW, 4, bias=True),
+    _conv_case("3x3 unstructured r4", 2, 32, 12, 12, 48, 3, 1, 1, 1, 1, UNSTRUCTURED, 4),
+    _conv_case("3x3 col r4 7x7 spans images", 5, 128, 7, 7, 96, 3, 1, 1, 16, 32, COL, 4),
+    _conv_case("3x3 s3 general stride", 2, 16, 17, 17, 32, 3, 3, 1, 16, 16, COL, 2),
+    _conv_case("f32 3x3 col16x16 r4", 1, 64, 32, 32, 64, 3, 1, 1, 16, 16, COL, 4, dtype="f32", out="f32"),
+    _conv_case("f32 3x3 s2 row", 2, 16, 11, 11, 48, 3, 2, 1, 16, 16, ROW, 2, dtype="f32", out="f32"),
+    _conv_case("3x3 col r16 many chunks", 1, 512, 6, 6, 64, 3, 1, 1, 16, 64, COL, 16),
+    _conv_case("1x1 col whole r2 4x4 image", 3, 256, 4, 4, 64, 1, 1, 0, 0, 0, COL, 2),
+]
+
+
+def run_conv(B, layer, x, w, dtype, out_dt, bias=None, relu=False, mask=None):
+    import torch
+    scheme = layer.scheme
+    conv = B.ConvShape(layer.n, layer.cin, layer.h, layer.w, layer.kh, layer.kw, layer.sh, layer.sw,
+                       layer.ph, layer.pw)
+    L = _layers().PackedLayer(scheme, DT[dtype], to_dev(w.reshape(layer.cout, -1), dtype), conv=conv,
+                              mask=mask)
+    xd = to_dev(x, dtype)
+    tdt = torch.float32 if out_dt == "f32" else torch.bfloat16
+    y = torch.full(layer.y_shape, float("nan"), dtype=tdt, device="cuda")
+    bd = None if bias is None else torch.from_numpy(bias.astype(np.float32)).cuda()
+    L.conv2d(xd, y, layer.n, DT[out_dt], bd, relu)
+    torch.cuda.synchronize()
+    return L, y
+
+
+@pytest.mark.parametrize("case", CONV_CASES, ids=[c["name"] for c in CONV_CASES])
+def test_conv_matches_oracle(B, case):
+    layer = case["layer"]
+    dtype = layer.dtype
+    out_dt = dtype if case["out"] == "same" else case["out"]
+    d = draw_layer(layer, 8, CONV_CASES.index(case), with_bias=case["bias"])
+    bias = d.get("bias")
+    L, y = run_conv(B, layer, d["x"], d["w"], dtype, out_dt, bias, layer.relu)
+    m = L.mask.cpu().numpy().reshape(layer.cout, -1)
+    assert np.array_equal(m, oracle_mask(d["w"], dtype, layer.scheme))
+    ref = oracle_conv(d["x"], d["w"], m, dtype, layer, bias=bias, relu=layer.relu)
+    got = out_to_f64(from_dev(y, out_dt), out_dt)
+    assert np.isfinite(got).all()
+    err = rel_l2(got, ref)
+    assert err <= TOL[dtype], f"{case['name']}: rel-L2 {err:.3e}"
+
+
+def test_conv_is_deterministic_and_empty_batch_is_a_noop(B):
+    import torch
+    case = CONV_CASES[0]
+    layer = case["layer"]
+    d = draw_layer(layer, 8, 0)
+    L, y1 = run_conv(B, layer, d["x"], d["w"], "bf16", "bf16")
+    y2 = torch.empty_like(y1)
+    L.conv2d(to_dev(d["x"], "bf16"), y2, layer.n, B.BF16)
+    torch.cuda.synchronize()
+    assert torch.equal(y1.view(torch.int16), y2.view(torch.int16))
+    y3 = torch.zeros(4, dtype=torch.bfloat16, device="cuda")
+    L.conv2d(to_dev(d["x"], "bf16"), y3, 0, B.BF16)
+    torch.cuda.synchronize()
+    assert torch.count_nonzero(y3.float()) == 0
+
+
+def test_tiles_packed_for_another_geometry_give_nan(B):
+    import torch
+    case = CONV_CASES[0]
+    layer = case["layer"]
+    d = draw_layer(layer, 8, 0)
+    other = B.ConvShape(1, layer.cin, layer.h, layer.w, 3, 3, 2, 2, 1, 1)   # stride 2: other layout
+    L = _layers().PackedLayer(layer.scheme, B.BF16, to_dev(d["w"].reshape(layer.cout, -1), "bf16"),
+                              conv=other)
+    shape = B.ConvShape(layer.n, layer.cin, layer.h, layer.w, 3, 3, 1, 1, 1, 1)
+    y = torch.zeros(layer.y_shape, dtype=torch.bfloat16, device="cuda")
+    nv, ni, nr, nb = B.bsp_packed_sizes(layer.scheme, shape, B.BF16)
+    if L.tiles.numel() >= nb:
+        B.bsp_conv2d(layer.scheme, shape, B.BF16, B.BF16, to_dev(d["x"], "bf16"), L.tiles, None, False, y)
+        torch.cuda.synchronize()
+        assert torch.isnan(y.float()).all()
+
+
+# ------------------------------------------------- full-size workloads, sampled ---
+def _c3_distinct():
+    seen, out = set(), []
+    for i, l in enumerate(workload(3)):
+        if l.kind != "conv":
+            continue
+        key = (l.cin, l.h, l.cout, l.kh, l.sh)
+        if key not in seen:
+            seen.add(key)
+            out.append((i, l))
+    return out
+
+
+C3 = _c3_distinct()
+
+
+@pytest.mark.parametrize("idx,layer", C3, ids=[l.name for _, l in C3])
+def test_resnet50_layer_full_batch_sampled_images(B, idx, layer):
+    """Batch-64 ResNet-50 layer in the launch configuration the benchmark times;
+    the oracle checks images 0 and 63 in full."""
+    d = draw_layer(layer, 3, idx)
+    L, y = run_conv(B, layer, d["x"], d["w"], "bf16", "bf16")
+    m = L.mask.cpu().numpy().reshape(layer.cout, -1)
+    assert np.array_equal(m, oracle_mask(d["w"], "bf16", layer.scheme))
+    ref = oracle_conv(d["x"], d["w"], m, "bf16", layer, images=[0, layer.n - 1])
+    got = out_to_f64(from_dev(y, "bf16"), "bf16")[[0, layer.n - 1]]
+    err = rel_l2(got, ref)
+    assert err <= TOL["bf16"], f"{layer.name}: rel-L2 {err:.3e}"
+
+
+def test_c1_full(B):
+    layer = workload(1)[0]
+    d = draw_layer(layer, 1, 0)
+    L, y = run_conv(B, layer, d["x"], d["w"], "f32", "f32")
+    m = L.mask.cpu().numpy().reshape(layer.cout, -1)
+    assert np.array_equal(m, oracle_mask(d["w"], "f32", layer.scheme))
+    ref = oracle_conv(d["x"], d["w"], m, "f32", layer)
+    err = rel_l2(from_dev(y, "f32"), ref)
+    assert err <= TOL["f32"], err
+
+
+# --------------------------------------------------------------------- linear ---
+def run_linear(B, layer, x, w, dtype, out_dt, bias=None, relu=False):
+    import torch
+    L = _layers().PackedLayer(layer.scheme, DT[dtype], to_dev(w, dtype))
+    tdt = torch.float32 if out_dt == "f32" else torch.bfloat16
+    y = torch.full(layer.y_shape, float("nan"), dtype=tdt, device="cuda")
+    bd = None if bias is None else torch.from_numpy(bias.astype(np.float32)).cuda()
+    L.linear(to_dev(x, dtype), y, layer.batch, DT[out_dt], bd, relu)
+    torch.cuda.synchronize()
+    return L, y
+
+
+def test_c4_fc_layer_sampled_columns(B):
+    layer = workload(4)[0]
+    d = draw_layer(layer, 4, 0)
+    L, y = run_linear(B, layer, d["x"], d["w"], "bf16", "bf16")
+    m = L.mask.cpu().numpy().reshape(layer.out_f, layer.in_f)
+    assert np.array_equal(m, oracle_mask(d["w"], "bf16", layer.scheme))
+    cols = [0, 1, 63, 64, 200, 300, 447, 511]
+    ref = oracle_linear(d["x"], d["w"], m, "bf16", cols=cols)
+    got = out_to_f64(from_dev(y, "bf16"), "bf16")[:, cols]
+    err = rel_l2(got, ref)
+    assert err <= TOL["bf16"], err
+
+
+@pytest.mark.parametrize("batch,reg,bh,bw,rate,out_dt,relu", [
+    (37, COL, 32, 32, 10, "bf16", False), (100, ROW, 32, 32, 2, "f32", True),
+    (64, DENSE, 0, 0, 1, "bf16", True), (130, COL, 16, 64, 4, "bf16", False)])
+def test_linear_small(B, batch, reg, bh, bw, rate, out_dt, relu):
+    layer = LinearLayer("fc", batch, 320, 200, bh, bw, reg, rate, "bf16", ("uniform", -1, 1),
+                        ("normal", 0, 0.05), relu=relu)
+    d = draw_layer(layer, 8, 90 + batch % 7, with_bias=True)
+    L, y = run_linear(B, layer, d["x"], d["w"], "bf16", out_dt, d["bias"], relu)
+    m = L.mask.cpu().numpy().reshape(200, 320)
+    ref = oracle_linear(d["x"], d["w"], m, "bf16", bias=d["bias"], relu=relu)
+    err = rel_l2(out_to_f64(from_dev(y, out_dt), out_dt), ref)
+    assert err <= TOL["bf16"], err
+
+
+# -------------------------------------------------------------- VGG-16 stack ---
+def test_maxpool_bit_exact(B):
+    import torch
+    from oracle import glue
+    x = draw(seed_for(8, 99, 0), (3, 5, 10, 14), ("normal", 0, 1), "bf16")
+    xd = to_dev(x, "bf16")
+    y = torch.empty((3, 5, 5, 7), dtype=torch.bfloat16, device="cuda")
+    B.bsp_maxpool2x2(B.BF16, 3, 5, 10, 14, xd, y)
+    torch.cuda.synchronize()
+    ref = glue.maxpool2x2(as_f64(x, "bf16"))
+    assert np.array_equal(out_to_f64(from_dev(y, "bf16"), "bf16"), ref)
+
+
+def test_vgg16_stack_per_layer_and_end_to_end(B):
+    """Each layer of the VGG-16 stack (batch reduced to 4 images) is gated on its
+    own seeded input; the chained stack is compared end to end against the oracle
+    run with bf16 storage between layers (reported, loosely gated)."""
+    import torch
+    from oracle import glue
+    from synthetic import f32_to_bf16_bits
+    layers = workload(2)
+    nimg = 4
+    x0 = draw(seed_for(2, 0, 0), (nimg, 3, 32, 32), ("normal", 0, 1), "bf16")
+    cur_gpu = to_dev(x0, "bf16")
+    cur_ref = as_f64(x0, "bf16")
+    for i, full in enumerate(layers):
+        layer = ConvLayer(full.name, nimg, full.cin, full.h, full.w, full.cout, 3, 3, 1, 1, 1, 1, full.bh,
+                          full.bw, full.regularity, full.rate, "bf16", full.x_dist, full.w_dist, relu=True)
+        d = draw_layer(layer, 2, i)
+        # per-layer gate on a seeded input
+        L, y = run_conv(B, layer, d["x"], d["w"], "bf16", "bf16", relu=True)
+        m = L.mask.cpu().numpy().reshape(layer.cout, -1)
+        ref = oracle_conv(d["x"], d["w"], m, "bf16", layer, relu=True)
+        err = rel_l2(out_to_f64(from_dev(y, "bf16"), "bf16"), ref)
+        assert err <= TOL["bf16"], f"{layer.name}: {err:.3e}"
+        # chained stack
+        yc = torch.empty(layer.y_shape, dtype=torch.bfloat16, device="cuda")
+        L.conv2d(cur_gpu, yc, nimg, B.BF16, None, True)
+        wm = as_f64(d["w"], "bf16") * m.reshape(layer.w_shape)
+        from oracle import direct
+        r = direct.conv2d(cur_ref, wm, None, (1, 1), (1, 1), relu=True)
+        r = as_f64(f32_to_bf16_bits(r.astype(np.float32)), "bf16")
+        if full.pool_after:
+            h = layer.h
+            yp = torch.empty((nimg, layer.cout, h // 2, h // 2), dtype=torch.bfloat16, device="cuda")
+            B.bsp_maxpool2x2(B.BF16, nimg, layer.cout, h, h, yc, yp)
+            yc, r = yp, glue.maxpool2x2(r)
+        cur_gpu, cur_ref = yc, r
+    torch.cuda.synchronize()
+    e2e = rel_l2(out_to_f64(from_dev(cur_gpu, "bf16"), "bf16"), cur_ref)
+    print(f"VGG-16 stack end-to-end rel-L2 {e2e:.3e}")
+    assert e2e <= 3e-2
