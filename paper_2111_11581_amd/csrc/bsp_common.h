@@ -43,6 +43,8 @@ constexpr int kLdsBudget = 63 * 1024;  // patch; the small tile tables stay unde
 constexpr int kMaxAccTiles = 8;  // G * T m-tiles per wave
 constexpr uint32_t kMagic = 0x31505342u;  // "BSP1"
 constexpr int kHeaderBytes = 256;
+constexpr int kZeroOffset = 128;  // 128 zero bytes inside the header: source of padding loads
+constexpr int kTargetWGs = 512;   // aim for at least two workgroups per CU
 
 // Unsigned division by a run-time constant with a multiply-high and a shift
 // (round-up method of Granlund and Montgomery, "Division by invariant integers
@@ -121,6 +123,7 @@ struct Plan {
     int Cin, H, W, KH, KW, SH, SW, PH, PW, Ho, Wo;
     int TW, TRW, Wop;             // tile width/rows, padded output width
     int VEC, LEFT, RL, NSLOT, CH_STRIDE, CC;
+    int gran;                     // patch fill: 16 / 4 = direct-to-LDS granule bytes, 0 = register path
     int gather;                   // 1: stride-1 8-byte reads, 2: stride-2 16-byte reads, 0: per element
     // work split
     int T, G;                     // m-tiles per group per wave, groups per wave
@@ -128,7 +131,7 @@ struct Plan {
     int mpg_blocks;               // split mode: m-blocks per group (4*T m-tiles each)
     int n_mb;                     // m-blocks (workgroups along the output rows)
     // dev_tiles layout (bytes)
-    int64_t off_chunks, off_desc, off_a, tile_bytes;
+    int64_t off_chunks, off_desc, off_desc16, off_a, tile_bytes;
     uint64_t fingerprint;
     // canonical sizes (elements)
     int64_t n_values, n_indices, n_rowptr;
@@ -137,6 +140,11 @@ struct Plan {
 // Computes the plan; the geometry part ignores conv->n.  Returns BSP_OK or an error.
 bsp_status make_plan(const bsp_scheme *s, const bsp_conv_shape *conv_or_null, bsp_dtype wdt,
                      int batch_for_linear, Plan *p);
+
+// Chooses how the waves of a workgroup share the m-tiles for n_pt pixel tiles
+// (fills p->T, G, split, mpg_blocks, n_mb).  T, G are powers of two with
+// G * T <= 4.
+void choose_split(Plan *p, int64_t n_pt);
 
 // Per-call launch arguments of the forward kernel.
 struct ConvArgs {
@@ -148,8 +156,8 @@ struct ConvArgs {
     int N, Cin, H, W, R, Ho, Wo, KH, KW, SH, SW, PH, PW;
     int TW, TRW, Wop, VEC, LEFT, RL, NSLOT, CH_STRIDE, CC;
     int n_groups, group_rows, mt_per_group, LP, S, T, G, split, mpg_blocks;
-    int n_ct, n_pt, n_mb, total, gather;
-    int64_t off_chunks, off_desc, off_a;
+    int n_ct, n_pt, n_mb, total, gather, gran;
+    int64_t off_chunks, off_desc16, off_a;
     uint32_t fp_lo, fp_hi;
     FastDiv div_nslot;   // row -> (channel, slot) in the patch loader
     FastDiv div_nv;      // vector index -> (row, vector in row) in the patch loader

@@ -6,20 +6,24 @@
 // list of W[o, q] * x[n, c, oh*sh - ph + r, ow*sw - pw + s], plus bias, then ReLU.
 //
 // How (one workgroup = 4 waves = one tile of 64 output pixels x a block of m-tiles):
-//  1. Thread 0 maps the tile's output rows to staged input rows ("slots").
+//  1. The tile's output rows are mapped to staged input rows ("slots"), one row per
+//     thread, in closed form.
 //  2. For each channel window of the kept lists ("chunk", built at pack time), the
 //     workgroup copies the input patch x[n, c_lo .. c_lo+cnt, slot rows, columns]
-//     into LDS with 2..16-byte coalesced loads; padding and out-of-image rows are 0.
+//     into LDS with asynchronous direct-to-LDS loads (global_load_lds, 16- or 4-byte
+//     granules, lane-linear destinations); padding and out-of-image rows are read from
+//     a zero block in the tile header.  Odd-width images fall back to batched
+//     register loads.
 //  3. Each wave walks its lists in steps of 32 kept columns.  Lane l owns kept
 //     positions 8*(l/16) .. +7 and the 4 horizontally adjacent pixels 4*(l%16) ..+3
 //     of the tile: per kept column it issues one 8-byte LDS read (stride 1; 16 bytes
-//     for stride 2) at the pre-decoded offset plus its pixel offset, and v_perm
-//     re-packs the 8 x 4 values into the B operands of 4 MFMAs (one per pixel of the
-//     group).  The A operand (weights) comes pre-tiled from dev_tiles, 16 bytes per
-//     lane, and is reused across the 4 pixel n-tiles; when a list is shared by
-//     several m-tiles (row pruning, dense) the gathered B operands are reused across
-//     them too.
-//  4. Epilogue: bias + ReLU + round-to-nearest-even bf16 (or fp32), each lane writes
+//     for stride 2) at the pre-decoded 16-bit offset plus its pixel offset, and
+//     v_perm re-packs the 8 x 4 values into the B operands of 4 MFMAs (one per pixel
+//     of the group).  The weights (A operand) come pre-tiled, 16 bytes per lane, and
+//     are reused across the 4 pixel n-tiles; a list shared by several m-tiles (row
+//     pruning, dense) also reuses the gathered B operands across them.  Offsets and
+//     weights of step s+1 are loaded while step s computes.
+//  4. Epilogue: bias + ReLU + round-to-nearest-even bf16 (or fp32); each lane writes
 //     4 adjacent pixels of 4 output rows with 8-byte stores.
 // Workgroup ids are remapped so that consecutive logical tiles (which share input
 // rows and weights) run on the same XCD and its L2.
@@ -31,6 +35,7 @@ namespace bsp {
 
 typedef short s16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void lds_void_t;
 
 namespace {
 
@@ -43,112 +48,98 @@ __device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
     return __builtin_bit_cast(uint16_t, h);
 }
 
-template <int VB>
-struct VecT;
-template <> struct VecT<2> { typedef uint16_t type; };
-template <> struct VecT<4> { typedef uint32_t type; };
-template <> struct VecT<8> { typedef uint2 type; };
-template <> struct VecT<16> { typedef uint4 type; };
+__device__ __forceinline__ void wait_vm_all() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
-template <typename E, int VB>
-__device__ __forceinline__ void load_patch_vec(const ConvArgs &a, E *patch, const int *s_img,
-                                               const int *s_ih, int c_lo, int c_cnt, int a0) {
-    typedef typename VecT<VB>::type V;
-    constexpr int VEC = VB / (int)sizeof(E);
-    const int NV = a.RL / VEC;
+// Direct-to-LDS patch fill.  Granule g (GB bytes) of the patch lands at byte g*GB;
+// with LDS destinations lane-linear per instruction, 64 consecutive granules per
+// wave instruction.
+template <typename E, int GB>
+__device__ __forceinline__ void fill_patch_direct(const ConvArgs &a, unsigned char *patch,
+                                                  const int *s_img, const int *s_ih, int c_lo,
+                                                  int c_cnt, int a0) {
+    constexpr int GE = GB / (int)sizeof(E);
+    const int NV = a.RL / GE;
     const int total = c_cnt * a.NSLOT * NV;
-    const E *x = (const E *)a.x;
-    for (int v = threadIdx.x; v < total; v += kThreads) {
-        const int row = (int)fdiv((uint32_t)v, a.div_nv);
-        const int vi = v - row * NV;
-        const int c = (int)fdiv((uint32_t)row, a.div_nslot);
-        const int sl = row - c * a.NSLOT;
-        const int ih = s_ih[sl];
-        const int iw = a0 + vi * VEC;
-        V val;
-        if (ih >= 0 && ih < a.H && iw >= 0 && iw < a.W) {
-            const size_t off = ((size_t)(s_img[sl] * a.Cin + c_lo + c) * a.H + ih) * a.W + iw;
-            val = *(const V *)(x + off);
-        } else {
-            val = V{};
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const unsigned char *x = (const unsigned char *)a.x;
+    const unsigned char *zero = a.tiles + kZeroOffset;
+    for (int v0 = wave * 64; v0 < total; v0 += kThreads) {
+        const int v = v0 + lane;
+        if (v < total) {
+            const int row = (int)fdiv((uint32_t)v, a.div_nv);
+            const int vi = v - row * NV;
+            const int c = (int)fdiv((uint32_t)row, a.div_nslot);
+            const int sl = row - c * a.NSLOT;
+            const int ih = s_ih[sl];
+            const int iw = a0 + vi * GE;
+            const unsigned char *src = zero;
+            if (ih >= 0 && ih < a.H && iw >= 0 && iw < a.W)
+                src = x + (((size_t)(s_img[sl] * a.Cin + c_lo + c) * a.H + ih) * a.W + iw) * sizeof(E);
+            lds_void_t *dst = (lds_void_t *)(patch + (size_t)v0 * GB);
+            if constexpr (GB == 16) __builtin_amdgcn_global_load_lds((const void *)src, dst, 16, 0, 0);
+            else __builtin_amdgcn_global_load_lds((const void *)src, dst, 4, 0, 0);
         }
-        *(V *)(patch + c * a.CH_STRIDE + sl * a.RL + vi * VEC) = val;
+    }
+}
+
+// Register-path patch fill (2-byte elements of odd-width rows): 8 loads in flight
+// per thread before the LDS stores.
+__device__ __forceinline__ void fill_patch_regs(const ConvArgs &a, uint16_t *patch, const int *s_img,
+                                                const int *s_ih, int c_lo, int c_cnt, int a0) {
+    const int NV = a.RL;
+    const int total = c_cnt * a.NSLOT * NV;
+    const uint16_t *x = (const uint16_t *)a.x;
+    for (int v0 = threadIdx.x; v0 < total; v0 += kThreads * 8) {
+        uint16_t val[8];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+            const int v = v0 + k * kThreads;
+            val[k] = 0;
+            if (v < total) {
+                const int row = (int)fdiv((uint32_t)v, a.div_nv);
+                const int iw = a0 + (v - row * NV);
+                const int c = (int)fdiv((uint32_t)row, a.div_nslot);
+                const int sl = row - c * a.NSLOT;
+                const int ih = s_ih[sl];
+                if (ih >= 0 && ih < a.H && iw >= 0 && iw < a.W)
+                    val[k] = x[((size_t)(s_img[sl] * a.Cin + c_lo + c) * a.H + ih) * a.W + iw];
+            }
+        }
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+            const int v = v0 + k * kThreads;
+            if (v < total) patch[v] = val[k];
+        }
     }
 }
 
 template <typename E>
-__device__ __forceinline__ void load_patch(const ConvArgs &a, E *patch, const int *s_img,
+__device__ __forceinline__ void fill_patch(const ConvArgs &a, unsigned char *patch, const int *s_img,
                                            const int *s_ih, int c_lo, int c_cnt, int a0) {
-    switch (a.VEC * (int)sizeof(E)) {
-        case 16: load_patch_vec<E, 16>(a, patch, s_img, s_ih, c_lo, c_cnt, a0); break;
-        case 8: load_patch_vec<E, 8>(a, patch, s_img, s_ih, c_lo, c_cnt, a0); break;
-        case 4: load_patch_vec<E, 4>(a, patch, s_img, s_ih, c_lo, c_cnt, a0); break;
-        default: load_patch_vec<E, 2>(a, patch, s_img, s_ih, c_lo, c_cnt, a0); break;
-    }
+    if (a.gran == 16) fill_patch_direct<E, 16>(a, patch, s_img, s_ih, c_lo, c_cnt, a0);
+    else if (a.gran == 4) fill_patch_direct<E, 4>(a, patch, s_img, s_ih, c_lo, c_cnt, a0);
+    else fill_patch_regs(a, (uint16_t *)patch, s_img, s_ih, c_lo, c_cnt, a0);
 }
 
-// ---- bf16 operand gathers -----------------------------------------------------------
+// ---- operand gathers -------------------------------------------------------------
 // v[j] holds pixels 0..3 (16 bits each) of kept column j of this lane; B[nt] is the
 // 8-wide k-vector of pixel nt.
 __device__ __forceinline__ void repack_bf16(const uint2 *v, s16x8 *B) {
 #pragma unroll
     for (int d = 0; d < 4; ++d) {
         const uint2 lo = v[2 * d], hi = v[2 * d + 1];
-        uint32_t w0 = perm(hi.x, lo.x, 0x05040100u);
-        uint32_t w1 = perm(hi.x, lo.x, 0x07060302u);
-        uint32_t w2 = perm(hi.y, lo.y, 0x05040100u);
-        uint32_t w3 = perm(hi.y, lo.y, 0x07060302u);
-        ((uint32_t *)&B[0])[d] = w0;
-        ((uint32_t *)&B[1])[d] = w1;
-        ((uint32_t *)&B[2])[d] = w2;
-        ((uint32_t *)&B[3])[d] = w3;
+        ((uint32_t *)&B[0])[d] = perm(hi.x, lo.x, 0x05040100u);
+        ((uint32_t *)&B[1])[d] = perm(hi.x, lo.x, 0x07060302u);
+        ((uint32_t *)&B[2])[d] = perm(hi.y, lo.y, 0x05040100u);
+        ((uint32_t *)&B[3])[d] = perm(hi.y, lo.y, 0x07060302u);
     }
 }
 
-__device__ __forceinline__ void gather_bf16(const uint16_t *patch, const int *ad, int mode, int SW,
-                                            s16x8 *B) {
-    uint2 v[8];
-    if (mode == 1) {
-#pragma unroll
-        for (int j = 0; j < 8; ++j) __builtin_memcpy(&v[j], patch + ad[j], 8);
-    } else if (mode == 2) {
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            uint4 u;
-            __builtin_memcpy(&u, patch + ad[j], 16);
-            v[j].x = perm(u.y, u.x, 0x05040100u);
-            v[j].y = perm(u.w, u.z, 0x05040100u);
-        }
-    } else {
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            const uint16_t *p = patch + ad[j];
-            v[j].x = (uint32_t)p[0] | ((uint32_t)p[SW] << 16);
-            v[j].y = (uint32_t)p[2 * SW] | ((uint32_t)p[3 * SW] << 16);
-        }
-    }
-    repack_bf16(v, B);
-}
-
-__device__ __forceinline__ void gather_f32(const float *patch, const int *ad, int mode, int SW,
-                                           float (*B)[8]) {
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-        if (mode == 1) {
-            float4 f;
-            __builtin_memcpy(&f, patch + ad[j], 16);
-            B[0][j] = f.x;
-            B[1][j] = f.y;
-            B[2][j] = f.z;
-            B[3][j] = f.w;
-        } else {
-            const float *p = patch + ad[j];
-            B[0][j] = p[0];
-            B[1][j] = p[SW];
-            B[2][j] = p[2 * SW];
-            B[3][j] = p[3 * SW];
-        }
-    }
+__device__ __forceinline__ void offsets(uint4 d, int pixoff, int *ad) {
+    ad[0] = (int)(d.x & 0xffffu) + pixoff; ad[1] = (int)(d.x >> 16) + pixoff;
+    ad[2] = (int)(d.y & 0xffffu) + pixoff; ad[3] = (int)(d.y >> 16) + pixoff;
+    ad[4] = (int)(d.z & 0xffffu) + pixoff; ad[5] = (int)(d.z >> 16) + pixoff;
+    ad[6] = (int)(d.w & 0xffffu) + pixoff; ad[7] = (int)(d.w >> 16) + pixoff;
 }
 
 template <typename E>
@@ -156,28 +147,79 @@ struct Frag;
 
 template <>
 struct Frag<uint16_t> {
+    typedef uint4 AReg;   // 8 bf16 weights of this lane
     s16x8 b[4];
-    __device__ __forceinline__ void gather(const uint16_t *patch, const int *ad, int mode, int SW) {
-        gather_bf16(patch, ad, mode, SW, b);
+    __device__ __forceinline__ void gather(const unsigned char *patch_b, uint4 d, int pixoff, int mode,
+                                           int SW) {
+        const uint16_t *patch = (const uint16_t *)patch_b;
+        int ad[8];
+        offsets(d, pixoff, ad);
+        uint2 v[8];
+        if (mode == 1) {
+#pragma unroll
+            for (int j = 0; j < 8; ++j) __builtin_memcpy(&v[j], patch + ad[j], 8);
+        } else if (mode == 2) {
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                uint4 u;
+                __builtin_memcpy(&u, patch + ad[j], 16);
+                v[j].x = perm(u.y, u.x, 0x05040100u);
+                v[j].y = perm(u.w, u.z, 0x05040100u);
+            }
+        } else {
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const uint16_t *p = patch + ad[j];
+                v[j].x = (uint32_t)p[0] | ((uint32_t)p[SW] << 16);
+                v[j].y = (uint32_t)p[2 * SW] | ((uint32_t)p[3 * SW] << 16);
+            }
+        }
+        repack_bf16(v, b);
     }
-    __device__ __forceinline__ void mma(const uint16_t *ap, f32x4 *acc) const {
-        const s16x8 A = *(const s16x8 *)ap;
+    static __device__ __forceinline__ AReg load_a(const unsigned char *ap) {
+        return *(const uint4 *)ap;
+    }
+    __device__ __forceinline__ void mma(const AReg &ar, f32x4 *acc) const {
+        const s16x8 A = __builtin_bit_cast(s16x8, ar);
 #pragma unroll
         for (int nt = 0; nt < 4; ++nt)
             acc[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, b[nt], acc[nt], 0, 0, 0);
     }
 };
 
+struct F32x8 {
+    float4 lo, hi;
+};
+
 template <>
 struct Frag<float> {
+    typedef F32x8 AReg;
     float b[4][8];
-    __device__ __forceinline__ void gather(const float *patch, const int *ad, int mode, int SW) {
-        gather_f32(patch, ad, mode, SW, b);
+    __device__ __forceinline__ void gather(const unsigned char *patch_b, uint4 d, int pixoff, int mode,
+                                           int SW) {
+        const float *patch = (const float *)patch_b;
+        int ad[8];
+        offsets(d, pixoff, ad);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            if (mode == 1) {
+                float4 f;
+                __builtin_memcpy(&f, patch + ad[j], 16);
+                b[0][j] = f.x; b[1][j] = f.y; b[2][j] = f.z; b[3][j] = f.w;
+            } else {
+                const float *p = patch + ad[j];
+                b[0][j] = p[0]; b[1][j] = p[SW]; b[2][j] = p[2 * SW]; b[3][j] = p[3 * SW];
+            }
+        }
     }
-    __device__ __forceinline__ void mma(const float *ap, f32x4 *acc) const {
-        const float4 a0 = *(const float4 *)ap;
-        const float4 a1 = *(const float4 *)(ap + 4);
-        const float A[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
+    static __device__ __forceinline__ AReg load_a(const unsigned char *ap) {
+        AReg r;
+        r.lo = *(const float4 *)ap;
+        r.hi = *(const float4 *)(ap + 16);
+        return r;
+    }
+    __device__ __forceinline__ void mma(const AReg &ar, f32x4 *acc) const {
+        const float A[8] = {ar.lo.x, ar.lo.y, ar.lo.z, ar.lo.w, ar.hi.x, ar.hi.y, ar.hi.z, ar.hi.w};
 #pragma unroll
         for (int nt = 0; nt < 4; ++nt)
 #pragma unroll
@@ -193,13 +235,14 @@ __device__ __forceinline__ float epi(float v, float b, int relu) {
 
 template <typename E, int T, int G>
 __global__ __launch_bounds__(kThreads, 2) void k_conv(ConvArgs a) {
-    extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+    extern __shared__ __attribute__((aligned(16))) unsigned char patch[];
     __shared__ int s_rowbase[kMaxTileRows];
     __shared__ int s_img[kMaxSlots];
     __shared__ int s_ih[kMaxSlots];
-    E *patch = (E *)smem;
+    typedef typename Frag<E>::AReg AReg;
+    constexpr int ABYTES = 8 * (int)sizeof(E);   // weight bytes per lane per m-tile and step
 
-    // XCD-aware remap: hardware places workgroup id on XCD id % 8; give each XCD a
+    // XCD-aware remap: hardware places workgroup id on XCD (id % 8); give each XCD a
     // contiguous range of logical tiles.
     const int per = gridDim.x >> 3;
     const int lid = (int)(blockIdx.x & 7) * per + (int)(blockIdx.x >> 3);
@@ -209,12 +252,25 @@ __global__ __launch_bounds__(kThreads, 2) void k_conv(ConvArgs a) {
     const int g0 = rt * a.TRW, ow0 = ct * a.TW;
     const int n_rows = a.N * a.Ho;
 
-    if (threadIdx.x == 0) {
-        for (int i = 0; i < a.NSLOT; ++i) {
-            s_img[i] = 0;
-            s_ih[i] = -1;
+    // staged input rows: row tr of the tile uses slots rowbase[tr] + r (r < KH)
+    if ((int)threadIdx.x < a.NSLOT) {
+        s_img[threadIdx.x] = 0;
+        s_ih[threadIdx.x] = -1;
+    }
+    __syncthreads();
+    if ((int)threadIdx.x < a.TRW) {
+        const int tr = threadIdx.x, g = g0 + tr;
+        int base = 0;
+        if (g < n_rows) {
+            const int img = (int)fdiv((uint32_t)g, a.div_Ho), oh = g - img * a.Ho;
+            const int k = img - (int)fdiv((uint32_t)g0, a.div_Ho);   // image boundaries crossed
+            base = (tr - k) * min(a.SH, a.KH) + k * a.KH;
+            for (int r = 0; r < a.KH; ++r) {
+                s_img[base + r] = img;
+                s_ih[base + r] = oh * a.SH - a.PH + r;
+            }
         }
-        slot_layout(g0, a.TRW, a.Ho, n_rows, a.KH, a.SH, a.PH, s_rowbase, s_img, s_ih);
+        s_rowbase[tr] = base;
     }
     __syncthreads();
 
@@ -235,14 +291,17 @@ __global__ __launch_bounds__(kThreads, 2) void k_conv(ConvArgs a) {
         tcount = min(T, a.mt_per_group - t0);
         gcount = 1;
     }
+    const bool active = gcount > 0 && tcount > 0;
 
     const TileHeader *hdr = (const TileHeader *)a.tiles;
     const bool ok = hdr->magic == kMagic && hdr->fp_lo == a.fp_lo && hdr->fp_hi == a.fp_hi;
     const int n_chunks = ok ? hdr->n_chunks : 0;
     const int4 *table = (const int4 *)(a.tiles + a.off_chunks);
-    const int32_t *desc = (const int32_t *)(a.tiles + a.off_desc);
-    const E *At = (const E *)(a.tiles + a.off_a);
+    const uint16_t *desc = (const uint16_t *)(a.tiles + a.off_desc16);
+    const unsigned char *At = a.tiles + a.off_a;
     const int a0 = ow0 * a.SW - a.PW - a.LEFT;
+    const size_t a_step = (size_t)64 * ABYTES;               // one m-tile, one step
+    const size_t a_mt = (size_t)a.S * a_step;                // one m-tile, all steps
 
     f32x4 acc[G][T][4];
 #pragma unroll
@@ -252,27 +311,48 @@ __global__ __launch_bounds__(kThreads, 2) void k_conv(ConvArgs a) {
 #pragma unroll
             for (int nt = 0; nt < 4; ++nt) acc[gi][ti][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+    uint4 dn[G];
+    AReg an[G][T];
+    auto fetch = [&](int s) {
+#pragma unroll
+        for (int gi = 0; gi < G; ++gi) {
+            if (gi < gcount && active) {
+                const int g = gbase + gi;
+                dn[gi] = *(const uint4 *)(desc + (size_t)g * a.LP + s * kKS + kg * 8);
+                const unsigned char *ap = At + ((size_t)g * a.mt_per_group + t0) * a_mt +
+                                          (size_t)s * a_step + (size_t)lane * ABYTES;
+#pragma unroll
+                for (int ti = 0; ti < T; ++ti)
+                    if (ti < tcount) an[gi][ti] = Frag<E>::load_a(ap + ti * a_mt);
+            }
+        }
+    };
+
     for (int ch = 0; ch < n_chunks; ++ch) {
         const int4 cd = table[ch];  // first step, end step, first channel, channel count
+        __syncthreads();            // previous chunk's gathers are done
+        fill_patch<E>(a, patch, s_img, s_ih, cd.z, cd.w, a0);
+        fetch(cd.x);
+        wait_vm_all();
         __syncthreads();
-        load_patch<E>(a, patch, s_img, s_ih, cd.z, cd.w, a0);
-        __syncthreads();
-        const int cbase = cd.z * a.CH_STRIDE - pixoff;
         for (int s = cd.x; s < cd.y; ++s) {
+            uint4 dc[G];
+            AReg ac[G][T];
 #pragma unroll
             for (int gi = 0; gi < G; ++gi) {
-                if (gi < gcount && tcount > 0) {
-                    const int g = gbase + gi;
-                    const int32_t *dp = desc + (size_t)g * a.LP + s * kKS + kg * 8;
-                    const int4 d0 = *(const int4 *)dp, d1 = *(const int4 *)(dp + 4);
-                    const int ad[8] = {d0.x - cbase, d0.y - cbase, d0.z - cbase, d0.w - cbase,
-                                       d1.x - cbase, d1.y - cbase, d1.z - cbase, d1.w - cbase};
+                dc[gi] = dn[gi];
+#pragma unroll
+                for (int ti = 0; ti < T; ++ti) ac[gi][ti] = an[gi][ti];
+            }
+            if (s + 1 < cd.y) fetch(s + 1);
+#pragma unroll
+            for (int gi = 0; gi < G; ++gi) {
+                if (gi < gcount && active) {
                     Frag<E> f;
-                    f.gather(patch, ad, a.gather, a.SW);
-                    const E *ap = At + (((size_t)g * a.mt_per_group + t0) * a.S + s) * 512 + lane * 8;
+                    f.gather(patch, dc[gi], pixoff, a.gather, a.SW);
 #pragma unroll
                     for (int ti = 0; ti < T; ++ti)
-                        if (ti < tcount) f.mma(ap + (size_t)ti * a.S * 512, acc[gi][ti]);
+                        if (ti < tcount) f.mma(ac[gi][ti], acc[gi][ti]);
                 }
             }
         }
@@ -336,23 +416,25 @@ conv_fn pick(int T, int G) {
         case 0x11: return k_conv<E, 1, 1>;
         case 0x12: return k_conv<E, 1, 2>;
         case 0x14: return k_conv<E, 1, 4>;
-        case 0x18: return k_conv<E, 1, 8>;
         case 0x21: return k_conv<E, 2, 1>;
         case 0x22: return k_conv<E, 2, 2>;
-        case 0x24: return k_conv<E, 2, 4>;
         case 0x41: return k_conv<E, 4, 1>;
-        case 0x42: return k_conv<E, 4, 2>;
-        case 0x81: return k_conv<E, 8, 1>;
         default: return nullptr;
     }
 }
 
 }  // namespace
 
-hipError_t launch_conv(const Plan &p, int n, const void *x, const uint8_t *tiles, const float *bias,
+hipError_t launch_conv(const Plan &plan, int n, const void *x, const uint8_t *tiles, const float *bias,
                        int relu, int out_bf16, void *y, hipStream_t st) {
+    Plan p = plan;
     ConvArgs a;
     memset(&a, 0, sizeof(a));
+    a.n_ct = p.Wop / p.TW;
+    const int64_t n_rt = div_up64((int64_t)n * p.Ho, p.TRW);
+    const int64_t n_pt = n_rt * a.n_ct;
+    if (n_pt <= 0) return hipSuccess;
+    choose_split(&p, n_pt);
     a.x = x;
     a.y = y;
     a.tiles = tiles;
@@ -367,21 +449,20 @@ hipError_t launch_conv(const Plan &p, int n, const void *x, const uint8_t *tiles
     a.n_groups = p.n_groups; a.group_rows = p.group_rows; a.mt_per_group = p.mt_per_group;
     a.LP = p.LP; a.S = p.S; a.T = p.T; a.G = p.G; a.split = p.split; a.mpg_blocks = p.mpg_blocks;
     a.gather = p.gather;
-    a.n_ct = p.Wop / p.TW;
-    const int n_rt = div_up(n * p.Ho, p.TRW);
-    a.n_pt = n_rt * a.n_ct;
+    a.gran = p.gran;
+    a.n_pt = (int)n_pt;
     a.n_mb = p.n_mb;
-    const int64_t total = (int64_t)a.n_pt * a.n_mb;
-    if (total <= 0) return hipSuccess;
+    const int64_t total = n_pt * a.n_mb;
     if (total > (int64_t)INT32_MAX - 8) return hipErrorInvalidValue;
     a.total = (int)total;
     a.off_chunks = p.off_chunks;
-    a.off_desc = p.off_desc;
+    a.off_desc16 = p.off_desc16;
     a.off_a = p.off_a;
     a.fp_lo = (uint32_t)p.fingerprint;
     a.fp_hi = (uint32_t)(p.fingerprint >> 32);
+    const int ge = p.gran ? p.gran / p.esize : 1;   // elements per fill granule
     a.div_nslot = make_fastdiv((uint32_t)p.NSLOT);
-    a.div_nv = make_fastdiv((uint32_t)(p.RL / p.VEC));
+    a.div_nv = make_fastdiv((uint32_t)(p.RL / ge));
     a.div_Ho = make_fastdiv((uint32_t)p.Ho);
     conv_fn fn = p.dt == BSP_F32 ? pick<float>(p.T, p.G) : pick<uint16_t>(p.T, p.G);
     if (!fn) return hipErrorInvalidValue;

@@ -268,6 +268,31 @@ __global__ void k_build_chunks(int4 *table, int S, int CC, int *n_chunks, int *f
     *n_chunks = nc;
 }
 
+// 16-bit chunk-relative gather offsets: each step belongs to one chunk (a range of
+// steps); the offset of a kept column relative to the chunk's first channel is
+// below CC * CH_STRIDE, which fits 16 bits by the LDS budget.
+__global__ void k_desc16(const int32_t *__restrict__ desc, const int4 *__restrict__ table,
+                         const int *n_chunks_p, int n_groups, int LP, int CH_STRIDE,
+                         uint16_t *__restrict__ desc16, int *flag) {
+    const int n = n_groups * LP;
+    const int nch = *n_chunks_p;
+    for (int e = blockIdx.x * blockDim.x + threadIdx.x; e < n; e += gridDim.x * blockDim.x) {
+        const int s = (e % LP) / 32;
+        int lo = -1;
+        for (int c = 0; c < nch; ++c) {
+            const int4 t = table[c];
+            if (s >= t.x && s < t.y) { lo = t.z; break; }
+        }
+        const int off = desc[e] - lo * CH_STRIDE;
+        if (lo < 0 || off < 0 || off > 0xffff) {
+            atomicOr(flag, 2);
+            desc16[e] = 0;
+        } else {
+            desc16[e] = (uint16_t)off;
+        }
+    }
+}
+
 template <typename E>
 __global__ void k_fill(E *p, size_t n, E v) {
     for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n;
@@ -361,6 +386,9 @@ bsp_status pack_t(const Plan &p, const E *w, const uint8_t *mask, E *values, int
     k_step_spans<<<grid_for(p.S), 256, 0, st>>>(desc, p.n_groups, p.LP, p.S, p.CH_STRIDE, table);
     k_build_chunks<<<1, 256, sizeof(int) * 2 * p.S, st>>>(
         table, p.S, p.CC, (int *)(tiles + offsetof(TileHeader, n_chunks)), flag);
+    k_desc16<<<grid_for((size_t)p.n_groups * p.LP), 256, 0, st>>>(
+        desc, table, (const int *)(tiles + offsetof(TileHeader, n_chunks)), p.n_groups, p.LP,
+        p.CH_STRIDE, (uint16_t *)(tiles + p.off_desc16), flag);
     if (hipGetLastError() != hipSuccess) return BSP_EDEVICE;
     if (hipMemcpyAsync(&hflag, flag, sizeof(int), hipMemcpyDeviceToHost, st) != hipSuccess ||
         hipStreamSynchronize(st) != hipSuccess)

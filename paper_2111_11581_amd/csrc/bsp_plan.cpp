@@ -99,14 +99,40 @@ bsp_status make_plan(const bsp_scheme *s, const bsp_conv_shape *conv, bsp_dtype 
         p->Wo = (c.w + 2 * c.pad_w - c.kw) / c.stride_w + 1;
         if (c.h + 2 * c.pad_h < c.kh || c.w + 2 * c.pad_w < c.kw || p->Ho <= 0 || p->Wo <= 0)
             return BSP_EINVAL;
-        const int wo4 = div_up(p->Wo, 4) * 4;
-        p->TW = 4;
-        for (int t = 64; t >= 4; t >>= 1)
-            if (wo4 % t == 0) { p->TW = t; break; }
-        p->Wop = wo4;
+        p->gather = p->SW == 1 ? 1 : ((p->SW == 2 && wdt == BSP_BF16) ? 2 : 0);
+        // pick the tile width: padded-pixel waste against LDS patch overhead
         int vw = 1;
         while (vw < vmax && p->W % (2 * vw) == 0) vw *= 2;
-        p->VEC = vw < p->TW * p->SW ? vw : p->TW * p->SW;
+        double best = 1e30;
+        for (int tw = 4; tw <= 64; tw *= 2) {
+            const int wop = div_up(p->Wo, tw) * tw;
+            if (tw > 4 && div_up(p->Wo, 4) * 4 <= tw / 2) break;   // wider than needed
+            // alignment unit of the staged rows: the widest vector whose left pad stays <= 1
+            int vec = 1;
+            for (int v = vw; v >= 1; v >>= 1) {
+                if (v > tw * p->SW) continue;
+                const int left = (v - p->PW % v) % v;
+                if (left <= 1 || p->PW % v == 0) { vec = v; break; }
+            }
+            const int left = (vec - p->PW % vec) % vec;
+            const int need = left + (tw - 1) * p->SW + p->KW + (p->gather == 2 ? 1 : 0);
+            const int rl = div_up(need, vec) * vec;
+            const int trw = kNPIX / tw;
+            const int period = p->Ho / gcd_int(p->Ho, trw);
+            int nsl = 0;
+            for (int t = 0; t < period; ++t) {
+                const int v = slot_layout(t * trw, trw, p->Ho, INT_MAX, p->KH, p->SH, p->PH,
+                                          nullptr, nullptr, nullptr);
+                if (v > nsl) nsl = v;
+            }
+            if (nsl > kMaxSlots) continue;
+            const double cost = (double)wop / p->Wo * (1.0 + 0.25 * rl * nsl / (double)kNPIX);
+            if (cost < best - 1e-9) {
+                best = cost;
+                p->TW = tw; p->Wop = wop; p->VEC = vec; p->LEFT = left; p->RL = rl; p->NSLOT = nsl;
+            }
+        }
+        if (best >= 1e30) return BSP_EUNSUPPORTED;
     } else {
         p->is_linear = 1;
         p->Cin = p->C; p->H = 1; p->W = batch_for_linear > 0 ? batch_for_linear : 64;
@@ -114,33 +140,22 @@ bsp_status make_plan(const bsp_scheme *s, const bsp_conv_shape *conv, bsp_dtype 
         p->PH = p->PW = 0;
         p->Ho = 1;
         p->Wo = p->W;
+        p->gather = 1;
         p->TW = 64;
         p->Wop = div_up(p->Wo, 64) * 64;
         int vw = 1;
         while (vw < vmax && p->W % (2 * vw) == 0) vw *= 2;
+        // the layout constants below do not depend on the batch size
         p->VEC = vw;
+        p->LEFT = 0;
+        p->RL = 64;
+        p->NSLOT = 1;
     }
     p->TRW = kNPIX / p->TW;
-    p->gather = p->SW == 1 ? 1 : ((p->SW == 2 && wdt == BSP_BF16) ? 2 : 0);
-    // The layout constants below must not depend on the linear batch size:
-    // linear layers use LEFT = 0 and RL = 64 for every VEC.
-    p->LEFT = (p->VEC - p->PW % p->VEC) % p->VEC;
+    // patch fill: direct-to-LDS granules of 16 or 4 bytes, else per-element register loads
     {
-        const int need = p->LEFT + (p->TW - 1) * p->SW + p->KW + (p->gather == 2 ? 1 : 0);
-        const int al = p->is_linear ? 8 : p->VEC;
-        p->RL = div_up(need, al) * al;
-    }
-    // slots: worst case over every phase of the row tiling
-    {
-        const int period = p->Ho / gcd_int(p->Ho, p->TRW);
-        int mx = 0;
-        for (int t = 0; t < period; ++t) {
-            int nsl = slot_layout(t * p->TRW, p->TRW, p->Ho, INT_MAX, p->KH, p->SH, p->PH,
-                                  nullptr, nullptr, nullptr);
-            if (nsl > mx) mx = nsl;
-        }
-        p->NSLOT = mx;
-        if (p->NSLOT > kMaxSlots) return BSP_EUNSUPPORTED;
+        const int vb = p->VEC * p->esize;
+        p->gran = vb >= 16 ? 16 : (vb >= 4 ? 4 : 0);
     }
     p->CH_STRIDE = p->NSLOT * p->RL;
     {
@@ -149,30 +164,13 @@ bsp_status make_plan(const bsp_scheme *s, const bsp_conv_shape *conv, bsp_dtype 
         p->CC = (int)(cc < p->Cin ? cc : p->Cin);
     }
 
-    // work split over waves
-    // T and G are powers of two (kernel instantiations); T * G <= kMaxAccTiles.
-    if (p->n_groups >= kWaves && p->mt_per_group <= kMaxAccTiles) {
-        p->T = pow2_ceil(p->mt_per_group);
-        const int gneed = div_up(p->n_groups, kWaves);
-        int g = 1;
-        while (g * 2 * p->T <= kMaxAccTiles && g < gneed) g *= 2;
-        p->G = g;
-        p->split = 0;
-        p->mpg_blocks = 1;
-        p->n_mb = div_up(p->n_groups, kWaves * p->G);
-    } else {
-        p->G = 1;
-        const int t = pow2_ceil(div_up(p->mt_per_group, kWaves));
-        p->T = t < kMaxAccTiles ? t : kMaxAccTiles;
-        p->split = 1;
-        p->mpg_blocks = div_up(p->mt_per_group, kWaves * p->T);
-        p->n_mb = p->n_groups * p->mpg_blocks;
-    }
+    choose_split(p, kTargetWGs);
 
     // dev_tiles layout
     p->off_chunks = kHeaderBytes;
     p->off_desc = align256(p->off_chunks + (int64_t)16 * p->S);
-    p->off_a = align256(p->off_desc + (int64_t)4 * p->n_groups * p->LP);
+    p->off_desc16 = align256(p->off_desc + (int64_t)4 * p->n_groups * p->LP);
+    p->off_a = align256(p->off_desc16 + (int64_t)2 * p->n_groups * p->LP);
     p->tile_bytes = p->off_a + (int64_t)p->n_groups * p->mt_per_group * p->S * 64 * 8 * p->esize;
 
     const int fpv[] = {p->R, p->C, p->bh_eff, p->bw_eff, p->reg, p->rate, p->dt, p->n_groups,
@@ -181,6 +179,28 @@ bsp_status make_plan(const bsp_scheme *s, const bsp_conv_shape *conv, bsp_dtype 
                        p->is_linear ? 0 : p->TW};
     p->fingerprint = fnv1a(fpv, (int)(sizeof(fpv) / sizeof(fpv[0])));
     return BSP_OK;
+}
+
+void choose_split(Plan *p, int64_t n_pt) {
+    if (n_pt < 1) n_pt = 1;
+    if (p->n_groups >= kWaves && p->mt_per_group <= 4) {
+        p->T = pow2_ceil(p->mt_per_group);
+        p->split = 0;
+        p->mpg_blocks = 1;
+        int g = 4;
+        while (g > 1 && (g * p->T > 4 || n_pt * div_up(p->n_groups, kWaves * g) < kTargetWGs)) g >>= 1;
+        p->G = g;
+        p->n_mb = div_up(p->n_groups, kWaves * p->G);
+    } else {
+        p->G = 1;
+        p->split = 1;
+        int t = pow2_ceil(div_up(p->mt_per_group, kWaves));
+        if (t > 4) t = 4;
+        while (t > 1 && n_pt * p->n_groups * div_up(p->mt_per_group, kWaves * t) < kTargetWGs) t >>= 1;
+        p->T = t;
+        p->mpg_blocks = div_up(p->mt_per_group, kWaves * p->T);
+        p->n_mb = p->n_groups * p->mpg_blocks;
+    }
 }
 
 }  // namespace bsp

@@ -8,7 +8,7 @@ the exact same host bits produced here.
 
 from .gen import (  # noqa: F401
     SEED_X, SEED_W, SEED_B, seed_for, f32_to_bf16_bits, bf16_bits_to_f32,
-    draw, draw_layer,
+    draw, draw_layer, draw_device,
 )
 from .workloads import (  # noqa: F401
     Scheme, ConvLayer, LinearLayer, workload, WORKLOADS,

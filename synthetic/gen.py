@@ -20,9 +20,13 @@ def seed_for(config: int, layer: int, which: int) -> int:
 
 def f32_to_bf16_bits(a: np.ndarray) -> np.ndarray:
     """fp32 -> bf16 bit patterns, round to nearest even (finite inputs)."""
-    u = np.ascontiguousarray(a, dtype=np.float32).view(np.uint32).astype(np.uint64)
-    bias = np.uint64(0x7FFF) + ((u >> np.uint64(16)) & np.uint64(1))
-    return ((u + bias) >> np.uint64(16)).astype(np.uint16)
+    u = np.ascontiguousarray(a, dtype=np.float32).view(np.uint32)
+    # finite values never overflow 32 bits here (largest: 0xFF7FFFFF + 0x8000)
+    r = (u >> np.uint32(16)) & np.uint32(1)
+    r += np.uint32(0x7FFF)
+    r += u
+    r >>= np.uint32(16)
+    return r.astype(np.uint16)
 
 
 def bf16_bits_to_f32(b: np.ndarray) -> np.ndarray:
@@ -35,11 +39,15 @@ def _draw_f32(seed: int, shape, dist) -> np.ndarray:
     if kind == "uniform":
         lo, hi = float(dist[1]), float(dist[2])
         v = rng.random(size=shape, dtype=np.float32)
-        return (np.float32(lo) + v * np.float32(hi - lo)).astype(np.float32)
+        v *= np.float32(hi - lo)          # same fp32 operations, in place
+        v += np.float32(lo)
+        return v
     if kind == "normal":
         mean, std = float(dist[1]), float(dist[2])
         v = rng.standard_normal(size=shape, dtype=np.float32)
-        return (np.float32(mean) + v * np.float32(std)).astype(np.float32)
+        v *= np.float32(std)
+        v += np.float32(mean)
+        return v
     raise ValueError(f"unknown distribution {dist!r}")
 
 
@@ -62,3 +70,23 @@ def draw_layer(layer, config: int, index: int, with_bias: bool = False) -> dict:
     if with_bias:
         out["bias"] = _draw_f32(seed_for(config, index, SEED_B), (layer.cout,), ("normal", 0.0, 0.1))
     return out
+
+
+def draw_device(seed: int, shape, dist, dtype: str, device="cuda"):
+    """Seeded draw on the GPU with torch's generator (same distributions as
+    ``draw``, different stream of numbers).  Used where the host generator is
+    too slow for the data volume (benchmark activations); values are fp32,
+    then rounded to nearest even bf16 when dtype is 'bf16'."""
+    import torch
+    g = torch.Generator(device=device)
+    g.manual_seed(int(seed))
+    kind = dist[0]
+    if kind == "normal":
+        t = torch.randn(shape, generator=g, device=device, dtype=torch.float32)
+        t = t * float(dist[2]) + float(dist[1])
+    elif kind == "uniform":
+        t = torch.rand(shape, generator=g, device=device, dtype=torch.float32)
+        t = t * float(dist[2] - dist[1]) + float(dist[1])
+    else:
+        raise ValueError(dist)
+    return t if dtype == "f32" else t.to(torch.bfloat16)

@@ -108,6 +108,10 @@ int main() {
     int ns = slot_layout(g0, TRW, Ho, 2 * Ho + 1, KH, SH, PH, rb, im, ih);
     for (int tr = 0; tr < TRW; ++tr) {
       int g = g0 + tr; if (g >= 2 * Ho + 1) { if (rb[tr] != 0) return 2; continue; }
+      // the forward kernel computes each row's base in closed form
+      int k = g / Ho - g0 / Ho;
+      int closed = (tr - k) * (SH < KH ? SH : KH) + k * KH;
+      if (closed != rb[tr]) { printf("closed form %d %d %d %d %d\n", Ho, KH, SH, g0, tr); return 4; }
       int img = g / Ho, oh = g % Ho;
       for (int r = 0; r < KH; ++r) {
         int sl = rb[tr] + r;
