@@ -58,7 +58,7 @@ bsp_status bsp_prune(const bsp_scheme *scheme, bsp_dtype wdt, const void *w, uin
                      void *stream) {
     if (!scheme || !w || !mask) return BSP_EINVAL;
     Plan p;
-    bsp_status st = make_plan(scheme, nullptr, wdt, 0, &p);
+    bsp_status st = make_plan(scheme, nullptr, wdt, -1, &p);
     if (st != BSP_OK) return st;
     if ((st = check_scheme_for_prune(p)) != BSP_OK) return st;
     return launch_prune(p, w, mask, S(stream)) == hipSuccess ? BSP_OK : BSP_EDEVICE;
@@ -81,7 +81,7 @@ bsp_status bsp_unpack(const bsp_scheme *scheme, bsp_dtype wdt, const void *value
                       const int32_t *indices, const int32_t *rowptr, void *w_out, void *stream) {
     if (!scheme || !values || !w_out) return BSP_EINVAL;
     Plan p;
-    bsp_status st = make_plan(scheme, nullptr, wdt, 0, &p);
+    bsp_status st = make_plan(scheme, nullptr, wdt, -1, &p);
     if (st != BSP_OK) return st;
     if ((p.reg == BSP_COL || p.reg == BSP_ROW) && (!indices || !rowptr)) return BSP_EINVAL;
     return launch_unpack(p, values, indices, rowptr, w_out, S(stream)) == hipSuccess ? BSP_OK

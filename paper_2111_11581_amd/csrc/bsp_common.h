@@ -6,14 +6,16 @@
 //    GEMM columns.  Column pruning (Sec. 4.1.1 / Eq. 3) gives one list per block-row;
 //    row pruning, dense and unstructured layers use one identity list (all columns)
 //    shared by every m-tile, with pruned weights zero in the weight tiles.
-//  * A workgroup owns a tile of 64 output pixels (TRW output rows x TW columns,
-//    rows flattened over images) and a block of m-tiles.  It stages an input patch
-//    for a window of input channels in LDS, then each wave walks its lists in
-//    steps of 32 kept columns: per lane, 8 kept columns x 4 neighbouring pixels are
-//    gathered from LDS with one 8-byte read each, re-packed, and fed to
-//    v_mfma_f32_16x16x32_bf16 (or 8 x v_mfma_f32_16x16x4_f32 for fp32).
-//  * The channel windows ("chunks") are ranges of 32-wide steps whose kept columns
-//    fall in at most CC consecutive input channels; they are built at pack time.
+//  * Pixels are cut into sub-tiles of 64 outputs (TRW output rows x TW columns, rows
+//    flattened over images).  A workgroup (4 waves) owns NSUB vertically stacked
+//    sub-tiles and one "m-block" of m-tiles; wave w works on sub-tile w % NSUB for the
+//    m-set w / NSUB of the m-block.  Workgroups are persistent: each walks a
+//    contiguous range of pixel tiles for its m-block.
+//  * Work items are (tile, chunk): a chunk is a range of 32-wide steps of the kept
+//    lists whose columns fall in at most CC consecutive input channels (and, when
+//    weights are streamed, at most SMAX steps).  Items are double buffered in LDS:
+//    the input patch (and streamed weight / offset slices) of item i+1 load with
+//    asynchronous direct-to-LDS copies while item i computes.
 #pragma once
 
 #include <stddef.h>
@@ -32,19 +34,20 @@
 
 namespace bsp {
 
-constexpr int kMT = 16;          // MFMA tile rows (M) and pixels per n-tile (N)
-constexpr int kKS = 32;          // kept columns per step
-constexpr int kNPIX = 64;        // output pixels per workgroup tile
+constexpr int kMT = 16;            // MFMA tile rows (M) and pixels per n-tile (N)
+constexpr int kKS = 32;            // kept columns per step
+constexpr int kNPIX = 64;          // output pixels per sub-tile
 constexpr int kWaves = 4;
 constexpr int kThreads = 256;
-constexpr int kMaxTileRows = 16; // TRW <= 64 / 4
-constexpr int kMaxSlots = 64;    // input rows staged per tile (<= TRW * KH)
-constexpr int kLdsBudget = 63 * 1024;  // patch; the small tile tables stay under 64 KiB
-constexpr int kMaxAccTiles = 8;  // G * T m-tiles per wave
-constexpr uint32_t kMagic = 0x31505342u;  // "BSP1"
+constexpr int kMaxTileRows = 64;   // NSUB * TRW
+constexpr int kMaxSlots = 160;     // staged input rows per workgroup tile
+constexpr int kLdsPerWG = 76 * 1024;  // dynamic LDS per workgroup (two per CU with the static tables)
+constexpr int kLdsOneWG = 152 * 1024; // dynamic LDS when one workgroup per CU is needed
+constexpr int kSmaxStreamed = 4;   // steps per item when weights are streamed
+constexpr uint32_t kMagic = 0x32505342u;  // "BSP2"
 constexpr int kHeaderBytes = 256;
-constexpr int kZeroOffset = 128;  // 128 zero bytes inside the header: source of padding loads
-constexpr int kTargetWGs = 512;   // aim for at least two workgroups per CU
+constexpr int kZeroOffset = 128;   // 128 zero bytes inside the header: source of padding loads
+constexpr int kTargetWGs = 512;    // two resident workgroups per CU
 
 // Unsigned division by a run-time constant with a multiply-high and a shift
 // (round-up method of Granlund and Montgomery, "Division by invariant integers
@@ -99,8 +102,8 @@ BSP_HD inline int slot_layout(int g0, int TRW, int Ho, int n_rows_total, int KH,
     return nslot;
 }
 
-// Header at the start of dev_tiles.  Written by the host (fields up to
-// n_steps) and by the device chunk builder (n_chunks).
+// Header at the start of dev_tiles.  Written by the host, except n_chunks
+// (device chunk builder).  Bytes [kZeroOffset, kHeaderBytes) stay zero.
 struct TileHeader {
     uint32_t magic;
     uint32_t fp_lo, fp_hi;       // plan fingerprint
@@ -121,15 +124,18 @@ struct Plan {
     // geometry (linear: Cin = C, H = 1, W = batch, KH = KW = 1)
     int is_linear;
     int Cin, H, W, KH, KW, SH, SW, PH, PW, Ho, Wo;
-    int TW, TRW, Wop;             // tile width/rows, padded output width
+    int TW, TRW, Wop;             // sub-tile width/rows, padded output width
+    int NSUB;                     // sub-tiles per workgroup tile (stacked rows)
     int VEC, LEFT, RL, NSLOT, CH_STRIDE, CC;
     int gran;                     // patch fill: 16 / 4 = direct-to-LDS granule bytes, 0 = register path
     int gather;                   // 1: stride-1 8-byte reads, 2: stride-2 16-byte reads, 0: per element
-    // work split
-    int T, G;                     // m-tiles per group per wave, groups per wave
-    int split;                    // 0: waves own whole groups, 1: waves split one group's m-tiles
-    int mpg_blocks;               // split mode: m-blocks per group (4*T m-tiles each)
-    int n_mb;                     // m-blocks (workgroups along the output rows)
+    // m-blocks: wave w of a workgroup handles m-set w / NSUB (4 / NSUB m-sets)
+    int split;                    // 0: m-sets own G whole groups; 1: m-sets own T m-tiles of one group
+    int T, G;                     // m-tiles per group per wave, groups per wave (powers of two)
+    int msets, mb_tiles, mb_groups, mpg_blocks, n_mb;
+    int resident;                 // 1: the m-block's weights stay in LDS; 0: streamed per item
+    int SMAX;                     // steps per item (0 = unlimited)
+    int lds_a, lds_d, lds_patch, lds_buf, lds_total;   // LDS bytes
     // dev_tiles layout (bytes)
     int64_t off_chunks, off_desc, off_desc16, off_a, tile_bytes;
     uint64_t fingerprint;
@@ -137,14 +143,11 @@ struct Plan {
     int64_t n_values, n_indices, n_rowptr;
 };
 
-// Computes the plan; the geometry part ignores conv->n.  Returns BSP_OK or an error.
+// Computes the plan; the geometry part ignores conv->n.  With conv_or_null == NULL
+// and batch_for_linear < 0 only the scheme and list structure are resolved.
+// Returns BSP_OK or an error.
 bsp_status make_plan(const bsp_scheme *s, const bsp_conv_shape *conv_or_null, bsp_dtype wdt,
                      int batch_for_linear, Plan *p);
-
-// Chooses how the waves of a workgroup share the m-tiles for n_pt pixel tiles
-// (fills p->T, G, split, mpg_blocks, n_mb).  T, G are powers of two with
-// G * T <= 4.
-void choose_split(Plan *p, int64_t n_pt);
 
 // Per-call launch arguments of the forward kernel.
 struct ConvArgs {
@@ -154,14 +157,19 @@ struct ConvArgs {
     const float *bias;
     int relu, out_bf16;
     int N, Cin, H, W, R, Ho, Wo, KH, KW, SH, SW, PH, PW;
-    int TW, TRW, Wop, VEC, LEFT, RL, NSLOT, CH_STRIDE, CC;
-    int n_groups, group_rows, mt_per_group, LP, S, T, G, split, mpg_blocks;
-    int n_ct, n_pt, n_mb, total, gather, gran;
+    int TW, TRW, NSUB, RL, NSLOT, CH_STRIDE, LEFT;
+    int n_groups, group_rows, mt_per_group, LP, S;
+    int split, msets, mb_tiles, mb_groups, mpg_blocks, n_mb;
+    int resident, gran, gather;
+    int lds_a, lds_d, lds_patch, lds_buf;
+    int n_ct, n_wt;               // column tiles, workgroup tiles
+    int wg_per_mb, tiles_per_wg;  // persistent split of the tiles of one m-block
+    int grid_valid;               // number of real workgroups (grid is padded to 8)
     int64_t off_chunks, off_desc16, off_a;
     uint32_t fp_lo, fp_hi;
-    FastDiv div_nslot;   // row -> (channel, slot) in the patch loader
-    FastDiv div_nv;      // vector index -> (row, vector in row) in the patch loader
-    FastDiv div_Ho;      // flattened output row -> (image, oh)
+    FastDiv div_nslot;            // row -> (channel, slot) in the patch loader
+    FastDiv div_nv;               // granule index -> (row, granule in row)
+    FastDiv div_Ho;               // flattened output row -> (image, oh)
 };
 
 inline int div_up(int a, int b) { return (a + b - 1) / b; }

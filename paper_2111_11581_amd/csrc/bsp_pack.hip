@@ -239,7 +239,7 @@ __global__ void k_step_spans(const int32_t *__restrict__ desc, int n_groups, int
     }
 }
 
-__global__ void k_build_chunks(int4 *table, int S, int CC, int *n_chunks, int *flag) {
+__global__ void k_build_chunks(int4 *table, int S, int CC, int smax, int *n_chunks, int *flag) {
     extern __shared__ int spans[];  // 2*S
     for (int s = threadIdx.x; s < S; s += blockDim.x) {
         spans[2 * s] = table[s].x;
@@ -256,7 +256,7 @@ __global__ void k_build_chunks(int4 *table, int S, int CC, int *n_chunks, int *f
             break;
         }
         int e = s + 1;
-        while (e < S) {
+        while (e < S && (smax == 0 || e - s < smax)) {
             const int h2 = max(hi, spans[2 * e + 1]);
             if (spans[2 * e] < lo || h2 - lo + 1 > CC) break;
             hi = h2;
@@ -385,7 +385,7 @@ bsp_status pack_t(const Plan &p, const E *w, const uint8_t *mask, E *values, int
     int4 *table = (int4 *)(tiles + p.off_chunks);
     k_step_spans<<<grid_for(p.S), 256, 0, st>>>(desc, p.n_groups, p.LP, p.S, p.CH_STRIDE, table);
     k_build_chunks<<<1, 256, sizeof(int) * 2 * p.S, st>>>(
-        table, p.S, p.CC, (int *)(tiles + offsetof(TileHeader, n_chunks)), flag);
+        table, p.S, p.CC, p.SMAX, (int *)(tiles + offsetof(TileHeader, n_chunks)), flag);
     k_desc16<<<grid_for((size_t)p.n_groups * p.LP), 256, 0, st>>>(
         desc, table, (const int *)(tiles + offsetof(TileHeader, n_chunks)), p.n_groups, p.LP,
         p.CH_STRIDE, (uint16_t *)(tiles + p.off_desc16), flag);

@@ -1,6 +1,8 @@
 // Host planner: resolves a pruning scheme and a layer geometry into the list
-// structure, the pixel tiling, the LDS patch layout and the dev_tiles layout.
-// Everything here is a pure function of its arguments.
+// structure, the pixel tiling, the LDS layout of the forward, the work split and the
+// dev_tiles layout.  Everything here is a pure function of its arguments (the batch
+// size of a conv does not enter; the batch of a linear layer only picks its vector
+// width).
 #include <climits>
 #include <cstring>
 
@@ -32,6 +34,58 @@ static uint64_t fnv1a(const int *v, int n) {
     }
     return h;
 }
+
+// Worst case number of staged input rows over every phase of a row tiling.
+static int max_slots(int rows, int Ho, int KH, int SH, int PH) {
+    const int period = Ho / gcd_int(Ho, rows);
+    int mx = 0;
+    for (int t = 0; t < period; ++t) {
+        const int v = slot_layout(t * rows, rows, Ho, INT_MAX, KH, SH, PH, nullptr, nullptr, nullptr);
+        if (v > mx) mx = v;
+    }
+    return mx;
+}
+
+namespace {
+
+struct MBlock {
+    int split, T, G, msets, mb_tiles, mb_groups, mpg_blocks, n_mb;
+};
+
+// m-block candidates for m-sets of msets waves
+int mblock_candidates(const Plan &p, int msets, MBlock *out) {
+    int n = 0;
+    // accumulator tiles per wave: fp32 and stride-2 gathers hold more registers
+    const int max_tg = (p.esize == 4 || p.gather == 2) ? 2 : 4;
+    if (p.n_groups == 1 || p.mt_per_group > 2) {
+        for (int T = max_tg; T >= 1; T >>= 1) {
+            MBlock m;
+            m.split = 1; m.T = T; m.G = 1; m.msets = msets;
+            m.mb_tiles = msets * T;
+            if (m.mb_tiles > 2 * pow2_ceil(p.mt_per_group) && T > 1) continue;  // mostly idle waves
+            m.mb_groups = 1;
+            m.mpg_blocks = div_up(p.mt_per_group, m.mb_tiles);
+            m.n_mb = p.n_groups * m.mpg_blocks;
+            out[n++] = m;
+        }
+    } else {
+        // per-group lists: at most two accumulator tiles per wave (more spill registers)
+        const int T = pow2_ceil(p.mt_per_group);
+        for (int G = 2 / T; G >= 1; G >>= 1) {
+            MBlock m;
+            m.split = 0; m.T = T; m.G = G; m.msets = msets;
+            m.mb_groups = msets * G;
+            if (m.mb_groups > 2 * pow2_ceil(p.n_groups) && G > 1) continue;
+            m.mb_tiles = m.mb_groups * p.mt_per_group;
+            m.mpg_blocks = 1;
+            m.n_mb = div_up(p.n_groups, m.mb_groups);
+            out[n++] = m;
+        }
+    }
+    return n;
+}
+
+}  // namespace
 
 bsp_status make_plan(const bsp_scheme *s, const bsp_conv_shape *conv, bsp_dtype wdt,
                      int batch_for_linear, Plan *p) {
@@ -83,6 +137,7 @@ bsp_status make_plan(const bsp_scheme *s, const bsp_conv_shape *conv, bsp_dtype 
     p->mt_per_group = div_up(p->group_rows, kMT);
     p->LP = div_up(p->L, kKS) * kKS;
     p->S = p->LP / kKS;
+    if (!conv && batch_for_linear < 0) return BSP_OK;   // list structure only (prune, unpack)
 
     // geometry
     const int vmax = wdt == BSP_F32 ? 4 : 8;  // elements per 16-byte vector
@@ -100,39 +155,6 @@ bsp_status make_plan(const bsp_scheme *s, const bsp_conv_shape *conv, bsp_dtype 
         if (c.h + 2 * c.pad_h < c.kh || c.w + 2 * c.pad_w < c.kw || p->Ho <= 0 || p->Wo <= 0)
             return BSP_EINVAL;
         p->gather = p->SW == 1 ? 1 : ((p->SW == 2 && wdt == BSP_BF16) ? 2 : 0);
-        // pick the tile width: padded-pixel waste against LDS patch overhead
-        int vw = 1;
-        while (vw < vmax && p->W % (2 * vw) == 0) vw *= 2;
-        double best = 1e30;
-        for (int tw = 4; tw <= 64; tw *= 2) {
-            const int wop = div_up(p->Wo, tw) * tw;
-            if (tw > 4 && div_up(p->Wo, 4) * 4 <= tw / 2) break;   // wider than needed
-            // alignment unit of the staged rows: the widest vector whose left pad stays <= 1
-            int vec = 1;
-            for (int v = vw; v >= 1; v >>= 1) {
-                if (v > tw * p->SW) continue;
-                const int left = (v - p->PW % v) % v;
-                if (left <= 1 || p->PW % v == 0) { vec = v; break; }
-            }
-            const int left = (vec - p->PW % vec) % vec;
-            const int need = left + (tw - 1) * p->SW + p->KW + (p->gather == 2 ? 1 : 0);
-            const int rl = div_up(need, vec) * vec;
-            const int trw = kNPIX / tw;
-            const int period = p->Ho / gcd_int(p->Ho, trw);
-            int nsl = 0;
-            for (int t = 0; t < period; ++t) {
-                const int v = slot_layout(t * trw, trw, p->Ho, INT_MAX, p->KH, p->SH, p->PH,
-                                          nullptr, nullptr, nullptr);
-                if (v > nsl) nsl = v;
-            }
-            if (nsl > kMaxSlots) continue;
-            const double cost = (double)wop / p->Wo * (1.0 + 0.25 * rl * nsl / (double)kNPIX);
-            if (cost < best - 1e-9) {
-                best = cost;
-                p->TW = tw; p->Wop = wop; p->VEC = vec; p->LEFT = left; p->RL = rl; p->NSLOT = nsl;
-            }
-        }
-        if (best >= 1e30) return BSP_EUNSUPPORTED;
     } else {
         p->is_linear = 1;
         p->Cin = p->C; p->H = 1; p->W = batch_for_linear > 0 ? batch_for_linear : 64;
@@ -141,66 +163,141 @@ bsp_status make_plan(const bsp_scheme *s, const bsp_conv_shape *conv, bsp_dtype 
         p->Ho = 1;
         p->Wo = p->W;
         p->gather = 1;
-        p->TW = 64;
-        p->Wop = div_up(p->Wo, 64) * 64;
-        int vw = 1;
-        while (vw < vmax && p->W % (2 * vw) == 0) vw *= 2;
-        // the layout constants below do not depend on the batch size
-        p->VEC = vw;
-        p->LEFT = 0;
-        p->RL = 64;
-        p->NSLOT = 1;
     }
-    p->TRW = kNPIX / p->TW;
-    // patch fill: direct-to-LDS granules of 16 or 4 bytes, else per-element register loads
+    int vw = 1;
+    while (vw < vmax && p->W % (2 * vw) == 0) vw *= 2;
+
+    // Channels one 32-wide step of a kept list can span: the LDS window of a chunk
+    // must hold at least that many.  Identity lists: 32 consecutive columns.  Column
+    // blocks keep the same count in every block, so a step covers a known number of
+    // blocks; whole-width blocks are data dependent (twice the mean spacing is used).
+    int span_req;
+    {
+        const int khw = p->KH * p->KW;
+        int64_t cols;
+        if (p->shared) cols = kKS;
+        else if (p->nbc > 1) cols = (int64_t)(div_up(kKS, kept_count(p->bw_eff, p->rate)) + 1) * p->bw_eff;
+        else cols = (int64_t)2 * kKS * p->rate;
+        span_req = (int)std::min<int64_t>(p->Cin, cols / khw + 2);
+    }
+
+    // search: sub-tile width x sub-tiles per workgroup x m-block x weight residency
+    const int a_step = 64 * 8 * p->esize;   // one m-tile, one step
+    const int64_t a_total = (int64_t)p->n_groups * p->mt_per_group * p->S * a_step;
+    double best = 1e300;
+    Plan bestp = *p;
+    for (int tw = 4; tw <= 64; tw *= 2) {
+        if (p->is_linear && tw != 64) continue;
+        if (!p->is_linear && tw > 4 && div_up(p->Wo, 4) * 4 <= tw / 2) break;   // wider than needed
+        const int wop = div_up(p->Wo, tw) * tw;
+        // alignment unit of staged rows: the widest vector whose left pad stays <= 1
+        int vec = 1;
+        for (int v = vw; v >= 1; v >>= 1) {
+            if (!p->is_linear && v > tw * p->SW) continue;
+            const int left = (v - p->PW % v) % v;
+            if (left <= 1 || p->PW % v == 0) { vec = v; break; }
+        }
+        const int left = (vec - p->PW % vec) % vec;
+        const int need = left + (tw - 1) * p->SW + p->KW + (p->gather == 2 ? 1 : 0);
+        // linear layers keep RL = 64 for every batch (their vector width varies)
+        const int rl = p->is_linear ? 64 : div_up(need, vec) * vec;
+        const int trw = kNPIX / tw;
+        for (int nsub = 1; nsub <= 4; nsub *= 2) {
+            if (trw * nsub > kMaxTileRows || (p->is_linear && nsub > 1)) continue;
+            const int nslot = max_slots(trw * nsub, p->Ho, p->KH, p->SH, p->PH);
+            if (nslot > kMaxSlots) continue;
+            const int chs = nslot * rl;
+            const int64_t pch = (int64_t)chs * p->esize;   // patch bytes per channel
+            MBlock cand[8];
+            const int nc = mblock_candidates(*p, 4 / nsub, cand);
+            for (int ci = 0; ci < nc; ++ci) {
+                const MBlock &m = cand[ci];
+                const int64_t lds_a = (int64_t)m.mb_tiles * p->S * a_step;
+                const int64_t lds_d = (int64_t)m.mb_groups * p->LP * 2;
+                // residency x LDS budget (two or one workgroups per CU) x steps per item
+                for (int opt = 0; opt < 8; ++opt) {
+                    const int resident = opt < 2;
+                    const int64_t budget = (opt & 1) ? kLdsOneWG : kLdsPerWG;
+                    const int smax = resident ? 0 : std::min(p->S, 4 >> ((opt - 2) >> 1));
+                    if (!resident && opt >= 4 && smax == std::min(p->S, 4 >> ((opt - 4) >> 1))) continue;
+                    int64_t cc, lds_patch, lds_buf, total;
+                    const int64_t item = resident ? 0
+                        : (int64_t)m.mb_tiles * smax * a_step + (int64_t)m.mb_groups * smax * 64;
+                    if (resident) {
+                        const int64_t free_b = budget - align256(lds_a) - align256(lds_d);
+                        if (free_b <= 0) continue;
+                        cc = free_b / (2 * pch);
+                    } else {
+                        const int64_t free_b = budget / 2 - item - 256;
+                        if (free_b <= 0) continue;
+                        cc = free_b / pch;
+                    }
+                    if (cc > p->Cin) cc = p->Cin;
+                    if (cc < span_req) continue;
+                    lds_patch = (int64_t)cc * pch;
+                    lds_patch = (lds_patch + 15) & ~(int64_t)15;
+                    if (resident) {
+                        lds_buf = lds_patch;
+                        total = align256(lds_a) + align256(lds_d) + 2 * lds_patch;
+                    } else {
+                        lds_buf = align256(lds_patch + item);
+                        total = 2 * lds_buf;
+                    }
+                    if (total > budget) continue;
+                    // cost per output pixel (bytes moved into LDS, weighted)
+                    const double px = (double)kNPIX * nsub;
+                    const int chunks = (int)div_up64(p->Cin, cc);
+                    // short contiguous runs per staged row cost extra load instructions
+                    const double run = (double)rl * p->esize;
+                    const double patch = (double)m.n_mb * p->Cin * pch / px * (1.0 + 32.0 / std::min(run, 128.0));
+                    const double wts = resident ? (double)lds_a * m.n_mb / (px * 16.0) : (double)a_total / px;
+                    const double gathers = (m.split ? (double)p->mt_per_group * p->n_groups / m.T
+                                                    : (double)p->n_groups) * p->S * 64.0;
+                    double cost = ((double)wop / p->Wo) * (patch + wts + 0.3 * gathers);
+                    cost *= 1.0 + 0.05 * (chunks - 1);
+                    if (!resident) cost *= 1.0 + 0.1 * (4 / std::max(smax, 1) - 1);   // items per step
+                    if (budget > kLdsPerWG) cost *= 1.6;                              // one workgroup per CU
+                    if (cost < best * (1 - 1e-9)) {
+                        best = cost;
+                        Plan q = *p;
+                        q.TW = tw; q.TRW = trw; q.Wop = p->is_linear ? div_up(p->Wo, 64) * 64 : wop;
+                        q.NSUB = nsub; q.VEC = p->is_linear ? vw : vec; q.LEFT = left; q.RL = rl;
+                        q.NSLOT = nslot; q.CH_STRIDE = chs; q.CC = (int)cc;
+                        q.split = m.split; q.T = m.T; q.G = m.G; q.msets = m.msets;
+                        q.mb_tiles = m.mb_tiles; q.mb_groups = m.mb_groups; q.mpg_blocks = m.mpg_blocks;
+                        q.n_mb = m.n_mb; q.resident = resident; q.SMAX = smax;
+                        q.lds_a = resident ? (int)align256(lds_a) : 0;
+                        q.lds_d = resident ? (int)align256(lds_d) : 0;
+                        q.lds_patch = (int)lds_patch;
+                        q.lds_buf = (int)lds_buf;
+                        q.lds_total = (int)total;
+                        bestp = q;
+                    }
+                }
+            }
+        }
+    }
+    if (best >= 1e300) return BSP_EUNSUPPORTED;
+    *p = bestp;
     {
         const int vb = p->VEC * p->esize;
         p->gran = vb >= 16 ? 16 : (vb >= 4 ? 4 : 0);
     }
-    p->CH_STRIDE = p->NSLOT * p->RL;
-    {
-        int64_t cc = kLdsBudget / ((int64_t)p->CH_STRIDE * p->esize);
-        if (cc < 1) return BSP_EUNSUPPORTED;
-        p->CC = (int)(cc < p->Cin ? cc : p->Cin);
-    }
-
-    choose_split(p, kTargetWGs);
 
     // dev_tiles layout
     p->off_chunks = kHeaderBytes;
     p->off_desc = align256(p->off_chunks + (int64_t)16 * p->S);
     p->off_desc16 = align256(p->off_desc + (int64_t)4 * p->n_groups * p->LP);
     p->off_a = align256(p->off_desc16 + (int64_t)2 * p->n_groups * p->LP);
-    p->tile_bytes = p->off_a + (int64_t)p->n_groups * p->mt_per_group * p->S * 64 * 8 * p->esize;
+    p->tile_bytes = p->off_a + (int64_t)p->n_groups * p->mt_per_group * p->S * a_step;
 
     const int fpv[] = {p->R, p->C, p->bh_eff, p->bw_eff, p->reg, p->rate, p->dt, p->n_groups,
                        p->mt_per_group, p->LP, p->S, p->CH_STRIDE, p->RL, p->LEFT, p->NSLOT,
                        p->CC, p->KH, p->KW, p->is_linear, p->is_linear ? 0 : p->SW,
-                       p->is_linear ? 0 : p->TW};
+                       p->is_linear ? 0 : p->TW, p->NSUB, p->SMAX, p->resident, p->split, p->T,
+                       p->G, p->msets};
     p->fingerprint = fnv1a(fpv, (int)(sizeof(fpv) / sizeof(fpv[0])));
     return BSP_OK;
-}
-
-void choose_split(Plan *p, int64_t n_pt) {
-    if (n_pt < 1) n_pt = 1;
-    if (p->n_groups >= kWaves && p->mt_per_group <= 4) {
-        p->T = pow2_ceil(p->mt_per_group);
-        p->split = 0;
-        p->mpg_blocks = 1;
-        int g = 4;
-        while (g > 1 && (g * p->T > 4 || n_pt * div_up(p->n_groups, kWaves * g) < kTargetWGs)) g >>= 1;
-        p->G = g;
-        p->n_mb = div_up(p->n_groups, kWaves * p->G);
-    } else {
-        p->G = 1;
-        p->split = 1;
-        int t = pow2_ceil(div_up(p->mt_per_group, kWaves));
-        if (t > 4) t = 4;
-        while (t > 1 && n_pt * p->n_groups * div_up(p->mt_per_group, kWaves * t) < kTargetWGs) t >>= 1;
-        p->T = t;
-        p->mpg_blocks = div_up(p->mt_per_group, kWaves * p->T);
-        p->n_mb = p->n_groups * p->mpg_blocks;
-    }
 }
 
 }  // namespace bsp
