@@ -29,6 +29,41 @@ sys.path.insert(0, ROOT)
 METRIC = "ms/layer + kept-FLOP TFLOP/s (% MFMA roofline), ResNet-50 layers at 4× pruning"
 PEAK_BF16 = 2516.6e12     # dense MFMA bf16, FLOP/s
 PEAK_HBM = 8.0e12         # bytes/s
+KERNEL_TAG = "bsp::(anonymous namespace)::k_conv<"
+CALIB_BYTES = 256 << 20   # plain copy kernel (torch.neg on bf16) that calibrates the HBM counters
+COUNTERS_FILE = os.path.join(ROOT, "profiles", "k_conv_resnet50_b64_hbm_counters.txt")
+
+
+def source_hash() -> str:
+    """Hash of the kernel sources; counter figures taken on other sources are stale."""
+    import hashlib
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2111_11581_amd", "csrc")
+    for d, names in ((csrc, sorted(os.listdir(csrc))), (os.path.join(ROOT, "include"), ["bsp.h"])):
+        for n in names:
+            if n.endswith((".hip", ".cpp", ".h")):
+                with open(os.path.join(d, n), "rb") as f:
+                    h.update(n.encode() + b"\0" + f.read())
+    return h.hexdigest()[:16]
+
+
+def read_counters():
+    """Per-launch HBM bytes of k_conv from the committed counter summary, or None
+    when it is missing or was taken on different kernel sources."""
+    if not os.path.exists(COUNTERS_FILE):
+        return None
+    kv = {}
+    with open(COUNTERS_FILE) as f:
+        for line in f:
+            if ":" in line and not line.startswith("#"):
+                k, v = line.split(":", 1)
+                kv[k.strip()] = v.strip()
+    if kv.get("source_hash") != source_hash():
+        return None
+    try:
+        return float(kv["traffic_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
 
 
 def layer_cost(layer, nnz: int, n_values: int, n_indices: int, n_rowptr: int):
@@ -78,6 +113,84 @@ def cpu_baseline(layers, images: int, threads: int):
     return t_total, kept_flops
 
 
+def _csv_rows(d: str, suffix: str):
+    import csv
+    import glob
+    files = sorted(glob.glob(os.path.join(d, "**", "*" + suffix), recursive=True))
+    if not files:
+        raise SystemExit("no *%s under %s" % (suffix, d))
+    rows = []
+    for fn in files:
+        with open(fn, newline="") as f:
+            rows += list(csv.DictReader(f))
+    return rows
+
+
+def _pmc_per_launch(d: str, counter: str, n_layers: int):
+    """Mean counter value (KiB) per k_conv dispatch of the timed steps (the first,
+    eager step is skipped) and the value of the calibration copy kernel."""
+    rows = [r for r in _csv_rows(d, "counter_collection.csv") if r["Counter_Name"] == counter]
+    rows.sort(key=lambda r: int(r["Dispatch_Id"]))
+    conv = [float(r["Counter_Value"]) for r in rows if KERNEL_TAG in r["Kernel_Name"]]
+    calib = [float(r["Counter_Value"]) for r in rows if "neg" in r["Kernel_Name"]]
+    if len(conv) <= n_layers or not calib:
+        raise SystemExit("%s: %d k_conv dispatches, %d copy dispatches" % (d, len(conv), len(calib)))
+    steady = conv[n_layers:]
+    return sum(steady) / len(steady), len(steady), max(calib)
+
+
+def summarize(args):
+    """Write the k_conv summary (kernel trace statistics and, when given, the HBM
+    counters scaled by the calibration copy) to the profiles folder."""
+    from synthetic import workload
+    n_layers = len(workload(3, batch=args.batch))
+    stats = _csv_rows(args.summarize, "kernel_stats.csv")
+    conv = [r for r in stats if KERNEL_TAG in r["Name"]]
+    calls = sum(int(r["Calls"]) for r in conv)
+    total_ns = sum(float(r["TotalDurationNs"]) for r in conv)
+    lines = ["# k_conv on the ResNet-50 v1.5 layer pass (batch 64, bf16, 54 launches per step)", "",
+             "Kernel trace statistics (rocprofv3 --kernel-trace --stats), command:", "",
+             "    " + args.trace_cmd, "",
+             "| kernel | calls | total us | average us | min us | max us |", "|---|---|---|---|---|---|"]
+    for r in sorted(stats, key=lambda r: -float(r["TotalDurationNs"])):
+        nm = r["Name"]
+        short = nm.replace("void ", "").replace("bsp::(anonymous namespace)::", "").split("(")[0] \
+            if KERNEL_TAG in nm else nm[:60]
+        lines.append("| %s | %s | %.1f | %.3f | %.3f | %.3f |" % (
+            short, r["Calls"], float(r["TotalDurationNs"]) / 1e3, float(r["AverageNs"]) / 1e3,
+            float(r["MinNs"]) / 1e3, float(r["MaxNs"]) / 1e3))
+    lines += ["", "k_conv, all instantiations: %d calls, average %.3f us per launch, %.1f us per step of %d launches"
+              % (calls, total_ns / calls / 1e3, total_ns / calls * n_layers / 1e3, n_layers), ""]
+    kv = {"source_hash": source_hash(), "kernel_avg_us_trace": "%.3f" % (total_ns / calls / 1e3)}
+    if args.pmc_fetch and args.pmc_write:
+        f_kib, nf, f_cal = _pmc_per_launch(args.pmc_fetch, "FETCH_SIZE", n_layers)
+        w_kib, nw, w_cal = _pmc_per_launch(args.pmc_write, "WRITE_SIZE", n_layers)
+        f_scale = CALIB_BYTES / (f_cal * 1024.0)
+        w_scale = CALIB_BYTES / (w_cal * 1024.0)
+        fetch = f_kib * 1024.0 * f_scale
+        write = w_kib * 1024.0 * w_scale
+        lines += ["HBM counters (one rocprofv3 --pmc pass each), commands:", "",
+                  "    " + args.fetch_cmd, "    " + args.write_cmd, "",
+                  "Calibration: a plain copy kernel (torch.neg, %d MiB in, %d MiB out) reads FETCH_SIZE %.0f KiB and "
+                  "WRITE_SIZE %.0f KiB, so the scale factors are %.4f (fetch) and %.4f (write)."
+                  % (CALIB_BYTES >> 20, CALIB_BYTES >> 20, f_cal, w_cal, f_scale, w_scale), "",
+                  "k_conv per launch (mean over %d / %d dispatches of the timed steps): fetch %.3f MB, write %.3f MB, "
+                  "traffic %.3f MB" % (nf, nw, fetch / 1e6, write / 1e6, (fetch + write) / 1e6), ""]
+        kv.update({"fetch_bytes_per_launch": "%.0f" % fetch, "write_bytes_per_launch": "%.0f" % write,
+                   "traffic_bytes_per_launch": "%.0f" % (fetch + write),
+                   "fetch_scale": "%.5f" % f_scale, "write_scale": "%.5f" % w_scale})
+    os.makedirs(os.path.dirname(os.path.abspath(args.out)), exist_ok=True)
+    with open(args.out, "w") as f:
+        f.write("\n".join(lines))
+    if args.pmc_fetch and args.pmc_write:
+        with open(COUNTERS_FILE, "w") as f:
+            f.write("# k_conv HBM bytes per launch on the ResNet-50 layer pass; written by bench.py --summarize\n")
+            f.write("# from the passes listed in %s\n" % os.path.basename(args.out))
+            for k, v in kv.items():
+                f.write("%s: %s\n" % (k, v))
+    print("\n".join(lines))
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -87,7 +200,19 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--batch", type=int, default=64)
     ap.add_argument("--layers-out", default=None, help="write the per-layer table (JSON) here")
+    ap.add_argument("--no-layers", action="store_true", help="skip the per-layer timing (profiling passes)")
+    ap.add_argument("--summarize", default=None, metavar="TRACE_DIR",
+                    help="no GPU: summarize a rocprofv3 --stats output folder (and --pmc-fetch/--pmc-write)")
+    ap.add_argument("--pmc-fetch", default=None)
+    ap.add_argument("--pmc-write", default=None)
+    ap.add_argument("--trace-cmd", default="")
+    ap.add_argument("--fetch-cmd", default="")
+    ap.add_argument("--write-cmd", default="")
+    ap.add_argument("--out", default=os.path.join(ROOT, "profiles", "k_conv_resnet50_b64.md"))
     args = ap.parse_args()
+    if args.summarize:
+        summarize(args)
+        return
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -168,6 +293,13 @@ def main():
         g_layer.append(g)
     torch.cuda.synchronize()
 
+    # plain copy kernel of known size: its HBM counters calibrate the k_conv ones
+    cal_src = torch.zeros(CALIB_BYTES // 2, dtype=torch.bfloat16, device=dev)
+    cal_dst = torch.empty_like(cal_src)
+    torch.neg(cal_src, out=cal_dst)
+    torch.cuda.synchronize()
+    del cal_src, cal_dst
+
     for _ in range(args.warmup):
         g_step.replay()
     torch.cuda.synchronize()
@@ -185,7 +317,7 @@ def main():
 
     # per-layer kernel durations (graph of REPS back-to-back launches, same stream)
     layer_us = []
-    for i in range(len(layers)):
+    for i in range(0 if args.no_layers else len(layers)):
         g_layer[i].replay()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record()
@@ -203,6 +335,7 @@ def main():
     n = len(layers)
     achieved_gbs = b_alg / t_step / 1e9
 
+    traffic = read_counters()
     table = []
     for l, c, us in zip(layers, costs, layer_us):
         table.append({"layer": l.name, "scheme": l.scheme.label(), "us": round(us, 3),
@@ -241,7 +374,9 @@ def main():
                    "batch": args.batch, "layers": n},
         "roofline": {"bound": "hbm", "kernel": "k_conv (all tile instantiations, %d launches per step)" % n,
                      "achieved": round(achieved_gbs, 1), "peak": PEAK_HBM / 1e9, "unit": "GB/s",
-                     "frac": round(achieved_gbs * 1e9 / PEAK_HBM, 4), "traffic": None,
+                     "frac": round(achieved_gbs * 1e9 / PEAK_HBM, 4),
+                     "traffic": None if traffic is None else round(traffic),
+                     "algorithmic_bytes_per_launch": round(b_alg / n),
                      "algorithmic_bytes_per_step": int(b_alg),
                      "avg_launch_us": round(ms_per_step * 1e3 / n, 3)},
         "prep_ms": round(prep_ms, 1),

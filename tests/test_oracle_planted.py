@@ -1,0 +1,189 @@
+"""Planted mistakes in the oracle are caught by its pins (CPU only).
+
+Each case copies an oracle source, plants one plausible mistake in the copy (a
+dropped term, a wrong sign, swapped or transposed indices, a wrong tie rule, a
+floor for a ceiling), builds or loads the copy from a temporary folder, and
+checks that at least one independent pin (pure-Python brute force, torch conv
+in fp64, k-subset enumeration, hand-worked examples) rejects it.  The oracle
+itself is never modified.
+"""
+
+import ctypes
+import importlib.util
+import itertools
+import json
+import math
+import os
+import subprocess
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import brute
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+GOLD = json.load(open(os.path.join(ROOT, "tests", "golden", "hand_examples.json")))
+
+
+# ------------------------------------------------------------ direct conv ---
+DIRECT_MUTATIONS = {
+    "dropped_filter_column": ("for (int s = 0; s < KW; ++s)", "for (int s = 0; s < KW - 1; ++s)"),
+    "wrong_sign_of_padding": ("const int ih = oh * SH - PH + r;", "const int ih = oh * SH + PH + r;"),
+    "swapped_filter_taps": ("w[(((size_t)o * C + c) * KH + r) * KW + s]",
+                            "w[(((size_t)o * C + c) * KH + s) * KW + r]"),
+    "relu_inverted": ("if (relu && acc < 0.0) acc = 0.0;\n                y[",
+                      "if (relu && acc > 0.0) acc = 0.0;\n                y["),
+    "linear_transposed_input": ("x[(size_t)k * B + b]", "x[(size_t)b * K + k]"),
+    "dropped_bias": ("double acc = bias ? bias[o] : 0.0;\n                for (int c",
+                     "double acc = 0.0;\n                for (int c"),
+}
+
+
+def _build_direct(tmp_path, name, old, new):
+    src = open(os.path.join(ROOT, "oracle", "direct.c")).read()
+    assert src.count(old) == 1, name
+    path = tmp_path / ("direct_%s.c" % name)
+    path.write_text(src.replace(old, new))
+    so = tmp_path / ("libdirect_%s.so" % name)
+    subprocess.run(["gcc", "-O1", "-ffp-contract=off", "-shared", "-fPIC", "-o", str(so), str(path)],
+                   check=True)
+    lib = ctypes.CDLL(str(so))
+    d = ctypes.POINTER(ctypes.c_double)
+    lib.oracle_conv2d_f64.argtypes = [d, d, d, d] + [ctypes.c_int] * 13
+    lib.oracle_linear_f64.argtypes = [d, d, d, d] + [ctypes.c_int] * 5
+    return lib
+
+
+def _p(a):
+    return a.ctypes.data_as(ctypes.POINTER(ctypes.c_double))
+
+
+def _conv(lib, x, w, b, s, p, relu):
+    N, C, H, W = x.shape
+    O, _, KH, KW = w.shape
+    Ho, Wo = (H + 2 * p - KH) // s + 1, (W + 2 * p - KW) // s + 1
+    y = np.zeros((N, O, Ho, Wo))
+    x, w, b = (np.ascontiguousarray(v, dtype=np.float64) for v in (x, w, b))
+    assert lib.oracle_conv2d_f64(_p(x), _p(w), _p(b), _p(y), N, C, H, W, O, KH, KW, s, s, p, p,
+                                 int(relu), 1) == 0
+    return y
+
+
+def _linear(lib, x, w, b, relu):
+    K, B = x.shape
+    O = w.shape[0]
+    y = np.zeros((O, B))
+    x, w, b = (np.ascontiguousarray(v, dtype=np.float64) for v in (x, w, b))
+    assert lib.oracle_linear_f64(_p(x), _p(w), _p(b), _p(y), K, B, O, int(relu), 1) == 0
+    return y
+
+
+def _direct_pins_pass(lib) -> bool:
+    """The direct-conv pins of tests/test_oracle_direct.py, on a few shapes."""
+    rng = np.random.default_rng(5)
+    for k, s, p, relu in ((3, 1, 1, False), (3, 2, 1, True), (1, 1, 0, False), (3, 1, 0, True)):
+        x = rng.standard_normal((2, 3, 6, 5))
+        w = rng.standard_normal((4, 3, k, k))
+        b = rng.standard_normal(4)
+        y = _conv(lib, x, w, b, s, p, relu)
+        yb = np.array(brute.conv2d(x.tolist(), w.tolist(), b.tolist(), (s, s), (p, p), relu=relu))
+        if y.shape != yb.shape or not np.allclose(y, yb, rtol=1e-12, atol=1e-12):
+            return False
+        ref = torch.nn.functional.conv2d(torch.from_numpy(x), torch.from_numpy(w), torch.from_numpy(b),
+                                         stride=s, padding=p)
+        if relu:
+            ref = torch.relu(ref)
+        if not np.allclose(y, ref.numpy(), rtol=1e-11, atol=1e-11):
+            return False
+    for relu in (False, True):
+        x, w, b = rng.standard_normal((5, 5)), rng.standard_normal((3, 5)), rng.standard_normal(3)
+        yl = _linear(lib, x, w, b, relu)
+        yb = np.array(brute.linear(x.tolist(), w.tolist(), b.tolist(), relu=relu))
+        if not np.allclose(yl, yb, rtol=1e-12, atol=1e-12):
+            return False
+    return True
+
+
+def test_unmodified_direct_copy_passes_the_pins(tmp_path):
+    assert _direct_pins_pass(_build_direct(tmp_path, "none", "int oracle_conv2d_f64", "int oracle_conv2d_f64"))
+
+
+@pytest.mark.parametrize("name", sorted(DIRECT_MUTATIONS))
+def test_planted_direct_mistake_is_caught(tmp_path, name):
+    old, new = DIRECT_MUTATIONS[name]
+    assert not _direct_pins_pass(_build_direct(tmp_path, name, old, new))
+
+
+# ----------------------------------------------------------------- prune ---
+PRUNE_MUTATIONS = {
+    "scores_over_wrong_axis": ("return np.cumsum(sq, axis=0)[-1]", "return np.cumsum(sq, axis=1)[:, -1]"),
+    "ties_to_higher_index": ('order = np.argsort(-scores, kind="stable")',
+                             'order = (len(scores) - 1 - np.argsort(-scores[::-1], kind="stable"))'),
+    "kept_count_floors": ("return (int(extent) + int(rate) - 1) // int(rate)",
+                          "return max(1, int(extent) // int(rate))"),
+    "abs_instead_of_square": ("sq = block * block", "sq = np.abs(block)"),
+    "keeps_smallest": ("order = np.argsort(-scores, kind=\"stable\")", "order = np.argsort(scores, kind=\"stable\")"),
+}
+
+
+def _load_prune(tmp_path, name, old, new):
+    src = open(os.path.join(ROOT, "oracle", "prune.py")).read()
+    assert src.count(old) == 1, name
+    path = tmp_path / ("prune_%s.py" % name)
+    path.write_text(src.replace(old, new))
+    spec = importlib.util.spec_from_file_location("planted_prune_%s" % name, str(path))
+    mod = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(mod)
+    return mod
+
+
+def _brute_keep(scores, k):
+    best, best_set = None, None
+    for sub in itertools.combinations(range(len(scores)), k):
+        s = math.fsum(scores[i] for i in sub)
+        if best is None or s > best:
+            best, best_set = s, sub
+    return list(best_set)
+
+
+def _prune_pins_pass(P) -> bool:
+    """Golden hand examples + k-subset enumeration of tests/test_oracle_prune.py."""
+    g = GOLD["matrix_4x8"]
+    W = np.array(g["W"], dtype=np.float64)
+    if P.prune_mask(W, 2, 4, P.COL, 2).tolist() != g["col_2x4_rate2"]["mask"]:
+        return False
+    if P.prune_mask(W, 2, 4, P.ROW, 2).tolist() != g["row_2x4_rate2"]["mask"]:
+        return False
+    rng = np.random.default_rng(11)
+    for trial in range(40):
+        bh, bw = int(rng.integers(1, 5)), int(rng.integers(1, 7))
+        R, C = bh * int(rng.integers(1, 3)), bw * int(rng.integers(1, 3))
+        Wt = rng.integers(-2, 3, size=(R, C)).astype(np.float64)
+        rate = int(rng.integers(1, 5))
+        for reg in (P.COL, P.ROW):
+            m = P.prune_mask(Wt, bh, bw, reg, rate)
+            for r0, r1 in P.block_ranges(R, bh):
+                for c0, c1 in P.block_ranges(C, bw):
+                    blk = Wt[r0:r1, c0:c1]
+                    if reg == P.COL:
+                        sc = [math.fsum(float(v) ** 2 for v in blk[:, j]) for j in range(c1 - c0)]
+                        want = _brute_keep(sc, (c1 - c0 + rate - 1) // rate)
+                        got = np.nonzero(m[r0, c0:c1])[0].tolist()
+                    else:
+                        sc = [math.fsum(float(v) ** 2 for v in blk[i, :]) for i in range(r1 - r0)]
+                        want = _brute_keep(sc, (r1 - r0 + rate - 1) // rate)
+                        got = np.nonzero(m[r0:r1, c0])[0].tolist()
+                    if got != want:
+                        return False
+    return True
+
+
+def test_unmodified_prune_copy_passes_the_pins(tmp_path):
+    assert _prune_pins_pass(_load_prune(tmp_path, "none", "import numpy as np", "import numpy as np"))
+
+
+@pytest.mark.parametrize("name", sorted(PRUNE_MUTATIONS))
+def test_planted_prune_mistake_is_caught(tmp_path, name):
+    old, new = PRUNE_MUTATIONS[name]
+    assert not _prune_pins_pass(_load_prune(tmp_path, name, old, new))
