@@ -29,7 +29,7 @@ sys.path.insert(0, ROOT)
 METRIC = "ms/layer + kept-FLOP TFLOP/s (% MFMA roofline), ResNet-50 layers at 4× pruning"
 PEAK_BF16 = 2516.6e12     # dense MFMA bf16, FLOP/s
 PEAK_HBM = 8.0e12         # bytes/s
-KERNEL_TAG = "bsp::(anonymous namespace)::k_conv<"
+KERNEL_TAG = "bsp::fwd::k_fwd<"
 CALIB_BYTES = 256 << 20   # plain copy kernel (torch.neg on bf16) that calibrates the HBM counters
 COUNTERS_FILE = os.path.join(ROOT, "profiles", "k_conv_resnet50_b64_hbm_counters.txt")
 

@@ -118,7 +118,7 @@ bsp_status bsp_linear(const bsp_scheme *scheme, int32_t batch, bsp_dtype in_dt, 
     if ((int64_t)scheme->cols * batch > INT32_MAX || (int64_t)scheme->rows * batch > INT32_MAX)
         return BSP_EUNSUPPORTED;
     if (batch == 0) return BSP_OK;
-    return launch_conv(p, 1, x, (const uint8_t *)dev_tiles, bias, relu ? 1 : 0, out_dt == BSP_BF16,
+    return launch_conv(p, batch, x, (const uint8_t *)dev_tiles, bias, relu ? 1 : 0, out_dt == BSP_BF16,
                        y, S(stream)) == hipSuccess
                ? BSP_OK
                : BSP_EDEVICE;

@@ -6,16 +6,18 @@
 //    GEMM columns.  Column pruning (Sec. 4.1.1 / Eq. 3) gives one list per block-row;
 //    row pruning, dense and unstructured layers use one identity list (all columns)
 //    shared by every m-tile, with pruned weights zero in the weight tiles.
-//  * Pixels are cut into sub-tiles of 64 outputs (TRW output rows x TW columns, rows
-//    flattened over images).  A workgroup (4 waves) owns NSUB vertically stacked
-//    sub-tiles and one "m-block" of m-tiles; wave w works on sub-tile w % NSUB for the
-//    m-set w / NSUB of the m-block.  Workgroups are persistent: each walks a
-//    contiguous range of pixel tiles for its m-block.
-//  * Work items are (tile, chunk): a chunk is a range of 32-wide steps of the kept
-//    lists whose columns fall in at most CC consecutive input channels (and, when
-//    weights are streamed, at most SMAX steps).  Items are double buffered in LDS:
-//    the input patch (and streamed weight / offset slices) of item i+1 load with
-//    asynchronous direct-to-LDS copies while item i computes.
+//  * Output pixels are taken in groups of 4 adjacent pixels of one output row (rows
+//    padded to a multiple of 4); groups are numbered row after row over all images,
+//    so a run of consecutive groups is a run of consecutive output pixels in memory.
+//    A sub-tile is 16 groups (64 pixels); a workgroup tile is NSUB sub-tiles.
+//  * A workgroup (4 waves) owns one tile and one m-block of m-tiles.  Wave w works on
+//    sub-tile w % NSUB; the 4 / NSUB waves of a sub-tile split either the m-block's
+//    m-tiles or the 32-wide steps of the kept lists (then they sum their partial
+//    results at the end).
+//  * The K loop walks "chunks": ranges of steps whose kept columns fall in at most CC
+//    consecutive input channels.  The input rows of a chunk's channels (the patch)
+//    are staged in LDS by asynchronous direct-to-LDS copies while the previous chunk
+//    computes (two buffers); weights and gather offsets come from LDS too.
 #pragma once
 
 #include <stddef.h>
@@ -36,18 +38,20 @@ namespace bsp {
 
 constexpr int kMT = 16;            // MFMA tile rows (M) and pixels per n-tile (N)
 constexpr int kKS = 32;            // kept columns per step
-constexpr int kNPIX = 64;          // output pixels per sub-tile
+constexpr int kGroups = 16;        // 4-pixel groups per sub-tile (64 pixels)
 constexpr int kWaves = 4;
 constexpr int kThreads = 256;
-constexpr int kMaxTileRows = 64;   // NSUB * TRW
-constexpr int kMaxSlots = 160;     // staged input rows per workgroup tile
-constexpr int kLdsPerWG = 76 * 1024;  // dynamic LDS per workgroup (two per CU with the static tables)
-constexpr int kLdsOneWG = 152 * 1024; // dynamic LDS when one workgroup per CU is needed
-constexpr int kSmaxStreamed = 4;   // steps per item when weights are streamed
-constexpr uint32_t kMagic = 0x32505342u;  // "BSP2"
+constexpr int kMaxTileRows = 72;   // output rows one workgroup tile may span
+constexpr int kMaxSlots = 192;     // staged input rows per workgroup tile
+constexpr int kMaxCC = 2047;       // channels of one chunk (11 bits of a granule's decode)
+constexpr int kMaxChunks = 512;    // chunk table entries staged in LDS
+constexpr int kLdsStatic = 12 * 1024;  // static LDS tables of the forward kernel (upper bound)
+constexpr uint32_t kMagic = 0x34505342u;  // "BSP4"
 constexpr int kHeaderBytes = 256;
 constexpr int kZeroOffset = 128;   // 128 zero bytes inside the header: source of padding loads
-constexpr int kTargetWGs = 512;    // two resident workgroups per CU
+constexpr int kNominalImages = 64; // batch the planner tunes conv tilings for
+constexpr int kNominalVectors = 512;  // batch the planner tunes linear tilings for
+constexpr int kLinRow = 64;        // a linear layer's batch is staged as rows of 64 vectors
 
 // Unsigned division by a run-time constant with a multiply-high and a shift
 // (round-up method of Granlund and Montgomery, "Division by invariant integers
@@ -121,21 +125,28 @@ struct Plan {
     int shared;                   // 1 = identity list shared by all m-tiles
     int n_groups, group_rows, mt_per_group;
     int L, LP, S;                 // kept per list, padded to 32, steps
-    // geometry (linear: Cin = C, H = 1, W = batch, KH = KW = 1)
+    // geometry (linear: Cin = C, H = ceil(batch / 64) rows of W = 64 vectors, 1x1)
     int is_linear;
     int Cin, H, W, KH, KW, SH, SW, PH, PW, Ho, Wo;
-    int TW, TRW, Wop;             // sub-tile width/rows, padded output width
-    int NSUB;                     // sub-tiles per workgroup tile (stacked rows)
-    int VEC, LEFT, RL, NSLOT, CH_STRIDE, CC;
-    int gran;                     // patch fill: 16 / 4 = direct-to-LDS granule bytes, 0 = register path
-    int gather;                   // 1: stride-1 8-byte reads, 2: stride-2 16-byte reads, 0: per element
-    // m-blocks: wave w of a workgroup handles m-set w / NSUB (4 / NSUB m-sets)
-    int split;                    // 0: m-sets own G whole groups; 1: m-sets own T m-tiles of one group
-    int T, G;                     // m-tiles per group per wave, groups per wave (powers of two)
-    int msets, mb_tiles, mb_groups, mpg_blocks, n_mb;
-    int resident;                 // 1: the m-block's weights stay in LDS; 0: streamed per item
-    int SMAX;                     // steps per item (0 = unlimited)
-    int lds_a, lds_d, lds_patch, lds_buf, lds_total;   // LDS bytes
+    int Wop, GPR;                 // output row width padded to 4, 4-pixel groups per row
+    int NSUB;                     // 64-pixel sub-tiles per workgroup tile
+    int TRWMAX;                   // output rows a tile may span
+    int NSLOT;                    // staged input rows per tile (worst case)
+    int GE;                       // elements per 16-byte granule
+    int LEFT, RS, RG, CH_STRIDE;  // patch row: left pad, row stride (elements, granules), channel stride
+    int CC;                       // channels of one chunk
+    int gather;                   // 1: stride-1 vector reads, 2: stride-2 16-byte reads, 0: per element
+    // waves and m-blocks
+    int qmode;                    // 0: the 4 / NSUB waves of a sub-tile split m-tiles, 1: split steps
+    int KS;                       // step split (qmode 1), else 1
+    int TM, TPG;                  // m-tiles per wave, m-tiles per list group inside a wave
+    int MBT, MBG, n_mb;           // m-tiles / list groups per workgroup, m-blocks
+    int n_mt_pad, n_g_pad;        // m-tiles / groups with tiles in dev_tiles (padded to whole m-blocks)
+    int resident;                 // 1: the m-block's weights stay in LDS; 0: staged per chunk
+    int NB;                       // LDS buffers of the K loop (2 or 3)
+    int SMAX;                     // steps per chunk when weights are staged (0 = unlimited)
+    int FR;                       // patch granules per thread and chunk
+    int lds_d, lds_a, lds_patch, lds_astage, lds_buf, lds_total;   // dynamic LDS bytes
     // dev_tiles layout (bytes)
     int64_t off_chunks, off_desc, off_desc16, off_a, tile_bytes;
     uint64_t fingerprint;
@@ -157,19 +168,26 @@ struct ConvArgs {
     const float *bias;
     int relu, out_bf16;
     int N, Cin, H, W, R, Ho, Wo, KH, KW, SH, SW, PH, PW;
-    int TW, TRW, NSUB, RL, NSLOT, CH_STRIDE, LEFT;
+    int64_t x_cs, y_cs;           // channel strides of x and y (elements)
+    int64_t x_total;              // elements of x (loads never reach past it)
+    int w_last;                   // valid width of the last input row of an image (linear: batch tail)
+    int w_last_out;               // valid width of the last output row of an image
+    int GPR, NSUB, NSLOT, LEFT, RS, RG, CH_STRIDE, CC, GE, FR;
     int n_groups, group_rows, mt_per_group, LP, S;
-    int split, msets, mb_tiles, mb_groups, mpg_blocks, n_mb;
-    int resident, gran, gather;
-    int lds_a, lds_d, lds_patch, lds_buf;
-    int n_ct, n_wt;               // column tiles, workgroup tiles
-    int wg_per_mb, tiles_per_wg;  // persistent split of the tiles of one m-block
+    int KS, MBT, MBG, n_mb;
+    int resident, NB;
+    int lds_d, lds_a, lds_patch, lds_astage, lds_buf;
+    int64_t n_groups_total;       // 4-pixel groups over all images
+    int n_pt;                     // pixel tiles
+    int tiles_per_wg;             // consecutive pixel tiles one workgroup walks
     int grid_valid;               // number of real workgroups (grid is padded to 8)
     int64_t off_chunks, off_desc16, off_a;
     uint32_t fp_lo, fp_hi;
-    FastDiv div_nslot;            // row -> (channel, slot) in the patch loader
-    FastDiv div_nv;               // granule index -> (row, granule in row)
+    FastDiv div_GPR;              // group -> (row, group in row)
     FastDiv div_Ho;               // flattened output row -> (image, oh)
+    FastDiv div_RG;               // patch granule -> (row, granule in row)
+    FastDiv div_NSLOT;            // patch row -> (channel, slot)
+    FastDiv div_nmb;              // workgroup -> (pixel tile, m-block)
 };
 
 inline int div_up(int a, int b) { return (a + b - 1) / b; }

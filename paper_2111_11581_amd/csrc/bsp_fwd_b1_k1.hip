@@ -1,0 +1,10 @@
+// Instantiations of the forward kernel: bf16, stride-1 gathers, no step split.
+#include "bsp_fwd.h"
+
+namespace bsp {
+namespace fwd {
+
+fwd_fn pick_b1_k1(int TM, int TPG, int KS) { return pick_tm<uint16_t, 1, 2, 4>(TM, TPG, KS); }
+
+}  // namespace fwd
+}  // namespace bsp

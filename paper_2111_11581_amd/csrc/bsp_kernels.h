@@ -16,6 +16,7 @@ bsp_status run_pack(const Plan &p, const void *w, const uint8_t *mask, void *val
 hipError_t launch_unpack(const Plan &p, const void *values, const int32_t *indices,
                          const int32_t *rowptr, void *w_out, hipStream_t st);
 
+// n: images of a conv; batch vectors of a linear layer
 hipError_t launch_conv(const Plan &p, int n, const void *x, const uint8_t *tiles,
                        const float *bias, int relu, int out_bf16, void *y, hipStream_t st);
 

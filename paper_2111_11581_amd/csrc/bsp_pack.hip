@@ -179,7 +179,7 @@ __global__ void k_masked_copy(const E *__restrict__ w, const uint8_t *__restrict
 }
 
 struct DescArgs {
-    int shared, n_groups, L, LP, C, KH, KW, CH_STRIDE, RL, LEFT;
+    int shared, n_groups, L, LP, C, KH, KW, CH_STRIDE, RS;
 };
 
 __global__ void k_desc(DescArgs a, const int32_t *__restrict__ indices, int32_t *__restrict__ desc) {
@@ -191,19 +191,19 @@ __global__ void k_desc(DescArgs a, const int32_t *__restrict__ indices, int32_t 
         const int q = a.shared ? tt : indices[(size_t)g * a.L + tt];
         const int c = q / khw, rs = q - c * khw;
         const int r = rs / a.KW, s = rs - r * a.KW;
-        desc[e] = c * a.CH_STRIDE + r * a.RL + s + a.LEFT;
+        desc[e] = c * a.CH_STRIDE + r * a.RS + s;
     }
 }
 
 struct ATileArgs {
-    int shared, n_groups, mt_per_group, group_rows, S, L, R, C;
+    int shared, n_groups, mt_per_group, n_mt_pad, group_rows, S, L, R, C;
 };
 
 template <typename E>
 __global__ void k_atiles(ATileArgs a, const E *__restrict__ w, const uint8_t *__restrict__ mask,
                          const int32_t *__restrict__ indices, E *__restrict__ A) {
     const int64_t per_mt = (int64_t)a.S * 512;
-    const int64_t n = (int64_t)a.n_groups * a.mt_per_group * per_mt;
+    const int64_t n = (int64_t)a.n_mt_pad * per_mt;   // m-tiles past the last group are zero
     for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < n;
          e += (int64_t)gridDim.x * blockDim.x) {
         const int j = (int)(e & 7), lane = (int)((e >> 3) & 63);
@@ -216,7 +216,7 @@ __global__ void k_atiles(ATileArgs a, const E *__restrict__ w, const uint8_t *__
         const int row = g * a.group_rows + rig;
         const int t = s * 32 + 8 * (lane >> 4) + j;
         E v = (E)0;
-        if (rig < a.group_rows && row < a.R && t < a.L) {
+        if (g < a.n_groups && rig < a.group_rows && row < a.R && t < a.L) {
             const int q = a.shared ? t : indices[(size_t)g * a.L + t];
             const size_t wi = (size_t)row * a.C + q;
             if (mask[wi]) v = w[wi];
@@ -377,10 +377,10 @@ bsp_status pack_t(const Plan &p, const E *w, const uint8_t *mask, E *values, int
     }
     // 3. forward layout
     int32_t *desc = (int32_t *)(tiles + p.off_desc);
-    DescArgs da{p.shared, p.n_groups, p.L, p.LP, p.C, p.KH, p.KW, p.CH_STRIDE, p.RL, p.LEFT};
+    DescArgs da{p.shared, p.n_groups, p.L, p.LP, p.C, p.KH, p.KW, p.CH_STRIDE, p.RS};
     k_desc<<<grid_for((size_t)p.n_groups * p.LP), 256, 0, st>>>(da, indices, desc);
-    ATileArgs aa{p.shared, p.n_groups, p.mt_per_group, p.group_rows, p.S, p.L, p.R, p.C};
-    const size_t na = (size_t)p.n_groups * p.mt_per_group * p.S * 512;
+    ATileArgs aa{p.shared, p.n_groups, p.mt_per_group, p.n_mt_pad, p.group_rows, p.S, p.L, p.R, p.C};
+    const size_t na = (size_t)p.n_mt_pad * p.S * 512;
     k_atiles<E><<<grid_for(na), 256, 0, st>>>(aa, w, mask, indices, (E *)(tiles + p.off_a));
     int4 *table = (int4 *)(tiles + p.off_chunks);
     k_step_spans<<<grid_for(p.S), 256, 0, st>>>(desc, p.n_groups, p.LP, p.S, p.CH_STRIDE, table);
@@ -389,6 +389,12 @@ bsp_status pack_t(const Plan &p, const E *w, const uint8_t *mask, E *values, int
     k_desc16<<<grid_for((size_t)p.n_groups * p.LP), 256, 0, st>>>(
         desc, table, (const int *)(tiles + offsetof(TileHeader, n_chunks)), p.n_groups, p.LP,
         p.CH_STRIDE, (uint16_t *)(tiles + p.off_desc16), flag);
+    if (p.n_g_pad > p.n_groups) {
+        // offsets of the padding groups of the last m-block: 0 (a valid patch position)
+        const size_t nd = (size_t)(p.n_g_pad - p.n_groups) * p.LP;
+        k_fill<uint16_t><<<grid_for(nd), 256, 0, st>>>(
+            (uint16_t *)(tiles + p.off_desc16) + (size_t)p.n_groups * p.LP, nd, (uint16_t)0);
+    }
     if (hipGetLastError() != hipSuccess) return BSP_EDEVICE;
     if (hipMemcpyAsync(&hflag, flag, sizeof(int), hipMemcpyDeviceToHost, st) != hipSuccess ||
         hipStreamSynchronize(st) != hipSuccess)

@@ -1,9 +1,10 @@
 // Host planner: resolves a pruning scheme and a layer geometry into the list
-// structure, the pixel tiling, the LDS layout of the forward, the work split and the
-// dev_tiles layout.  Everything here is a pure function of its arguments (the batch
-// size of a conv does not enter; the batch of a linear layer only picks its vector
-// width).
+// structure, the pixel tiling, the LDS layout of the forward, the wave work split
+// and the dev_tiles layout.  Everything here is a pure function of its arguments:
+// the batch (conv->n, the batch of a linear layer) does not enter, so tiles packed
+// once serve every batch size.  Tiling choices are scored for a nominal batch.
 #include <climits>
+#include <cmath>
 #include <cstring>
 
 #include "bsp_common.h"
@@ -15,13 +16,8 @@ static int gcd_int(int a, int b) {
     return a;
 }
 
-static int pow2_ceil(int v) {
-    int p = 1;
-    while (p < v) p *= 2;
-    return p;
-}
-
 static int64_t align256(int64_t v) { return (v + 255) & ~(int64_t)255; }
+static int round_up(int v, int m) { return (v + m - 1) / m * m; }
 
 static uint64_t fnv1a(const int *v, int n) {
     uint64_t h = 1469598103934665603ull;
@@ -35,57 +31,26 @@ static uint64_t fnv1a(const int *v, int n) {
     return h;
 }
 
-// Worst case number of staged input rows over every phase of a row tiling.
-static int max_slots(int rows, int Ho, int KH, int SH, int PH) {
-    const int period = Ho / gcd_int(Ho, rows);
+// Output rows spanned by a tile of TG groups, worst case over its start phase.
+static int rows_spanned(int TG, int GPR) {
+    const int g = gcd_int(TG, GPR);
+    return (GPR - g + TG - 1) / GPR + 1;
+}
+
+// Staged input rows of the worst tile, over every phase of the tiling inside an
+// image (tiles may cross image boundaries).
+static int max_slots(int TG, int GPR, int Ho, int KH, int SH, int PH) {
+    const int64_t img_groups = (int64_t)Ho * GPR;
+    const int64_t period = img_groups / gcd_int((int)(img_groups % INT_MAX), TG);
     int mx = 0;
-    for (int t = 0; t < period; ++t) {
-        const int v = slot_layout(t * rows, rows, Ho, INT_MAX, KH, SH, PH, nullptr, nullptr, nullptr);
+    for (int64_t t = 0; t < period; ++t) {
+        const int64_t G0 = t * TG;
+        const int g0 = (int)(G0 / GPR), g1 = (int)((G0 + TG - 1) / GPR);
+        const int v = slot_layout(g0, g1 - g0 + 1, Ho, INT_MAX, KH, SH, PH, nullptr, nullptr, nullptr);
         if (v > mx) mx = v;
     }
     return mx;
 }
-
-namespace {
-
-struct MBlock {
-    int split, T, G, msets, mb_tiles, mb_groups, mpg_blocks, n_mb;
-};
-
-// m-block candidates for m-sets of msets waves
-int mblock_candidates(const Plan &p, int msets, MBlock *out) {
-    int n = 0;
-    // accumulator tiles per wave: fp32 and stride-2 gathers hold more registers
-    const int max_tg = (p.esize == 4 || p.gather == 2) ? 2 : 4;
-    if (p.n_groups == 1 || p.mt_per_group > 2) {
-        for (int T = max_tg; T >= 1; T >>= 1) {
-            MBlock m;
-            m.split = 1; m.T = T; m.G = 1; m.msets = msets;
-            m.mb_tiles = msets * T;
-            if (m.mb_tiles > 2 * pow2_ceil(p.mt_per_group) && T > 1) continue;  // mostly idle waves
-            m.mb_groups = 1;
-            m.mpg_blocks = div_up(p.mt_per_group, m.mb_tiles);
-            m.n_mb = p.n_groups * m.mpg_blocks;
-            out[n++] = m;
-        }
-    } else {
-        // per-group lists: at most two accumulator tiles per wave (more spill registers)
-        const int T = pow2_ceil(p.mt_per_group);
-        for (int G = 2 / T; G >= 1; G >>= 1) {
-            MBlock m;
-            m.split = 0; m.T = T; m.G = G; m.msets = msets;
-            m.mb_groups = msets * G;
-            if (m.mb_groups > 2 * pow2_ceil(p.n_groups) && G > 1) continue;
-            m.mb_tiles = m.mb_groups * p.mt_per_group;
-            m.mpg_blocks = 1;
-            m.n_mb = div_up(p.n_groups, m.mb_groups);
-            out[n++] = m;
-        }
-    }
-    return n;
-}
-
-}  // namespace
 
 bsp_status make_plan(const bsp_scheme *s, const bsp_conv_shape *conv, bsp_dtype wdt,
                      int batch_for_linear, Plan *p) {
@@ -140,7 +105,7 @@ bsp_status make_plan(const bsp_scheme *s, const bsp_conv_shape *conv, bsp_dtype 
     if (!conv && batch_for_linear < 0) return BSP_OK;   // list structure only (prune, unpack)
 
     // geometry
-    const int vmax = wdt == BSP_F32 ? 4 : 8;  // elements per 16-byte vector
+    int nominal_rows;   // output rows of the nominal batch, for scoring only
     if (conv) {
         const bsp_conv_shape &c = *conv;
         if (c.cin <= 0 || c.h <= 0 || c.w <= 0 || c.kh <= 0 || c.kw <= 0 || c.stride_h <= 0 ||
@@ -154,20 +119,32 @@ bsp_status make_plan(const bsp_scheme *s, const bsp_conv_shape *conv, bsp_dtype 
         p->Wo = (c.w + 2 * c.pad_w - c.kw) / c.stride_w + 1;
         if (c.h + 2 * c.pad_h < c.kh || c.w + 2 * c.pad_w < c.kw || p->Ho <= 0 || p->Wo <= 0)
             return BSP_EINVAL;
+        if (p->PW > 64) return BSP_EUNSUPPORTED;
         p->gather = p->SW == 1 ? 1 : ((p->SW == 2 && wdt == BSP_BF16) ? 2 : 0);
+        nominal_rows = kNominalImages * p->Ho;
     } else {
+        // a linear layer is a 1x1 conv over rows of 64 batch vectors (feature-major x)
         p->is_linear = 1;
-        p->Cin = p->C; p->H = 1; p->W = batch_for_linear > 0 ? batch_for_linear : 64;
+        p->Cin = p->C; p->H = 1; p->W = kLinRow;
         p->KH = p->KW = p->SH = p->SW = 1;
         p->PH = p->PW = 0;
         p->Ho = 1;
-        p->Wo = p->W;
+        p->Wo = kLinRow;
         p->gather = 1;
+        nominal_rows = kNominalVectors / kLinRow;
     }
-    int vw = 1;
-    while (vw < vmax && p->W % (2 * vw) == 0) vw *= 2;
+    p->GE = 16 / p->esize;
+    p->Wop = round_up(p->Wo, 4);
+    p->GPR = p->Wop / 4;
+    p->LEFT = round_up(p->PW, p->GE);
+    {
+        const int ng = div_up(p->W, p->GE);
+        const int maxpos = p->LEFT - p->PW + (p->Wo - 1) * p->SW + p->KW;   // one past the last used
+        p->RS = round_up(std::max(maxpos, p->LEFT + ng * p->GE), p->GE);
+        p->RG = p->RS / p->GE;
+    }
 
-    // Channels one 32-wide step of a kept list can span: the LDS window of a chunk
+    // Channels one 32-wide step of a kept list can span: a chunk's channel window
     // must hold at least that many.  Identity lists: 32 consecutive columns.  Column
     // blocks keep the same count in every block, so a step covers a known number of
     // blocks; whole-width blocks are data dependent (twice the mean spacing is used).
@@ -181,97 +158,124 @@ bsp_status make_plan(const bsp_scheme *s, const bsp_conv_shape *conv, bsp_dtype 
         span_req = (int)std::min<int64_t>(p->Cin, cols / khw + 2);
     }
 
-    // search: sub-tile width x sub-tiles per workgroup x m-block x weight residency
-    const int a_step = 64 * 8 * p->esize;   // one m-tile, one step
-    const int64_t a_total = (int64_t)p->n_groups * p->mt_per_group * p->S * a_step;
+    const int astep = 64 * 8 * p->esize;   // weight bytes of one m-tile and step
+    const int n_mt = p->n_groups * p->mt_per_group;
+    const int mpg = p->mt_per_group;
+    const double total_groups = (double)nominal_rows * p->GPR;
+    // LDS budgets per workgroup: 1, 2, 3 or 4 workgroups per CU (160 KB, minus static tables)
+    const int budgets[4] = {140 * 1024, 68 * 1024, 40 * 1024, 28 * 1024};
+    const int occs[4] = {1, 2, 3, 4};
+
     double best = 1e300;
     Plan bestp = *p;
-    for (int tw = 4; tw <= 64; tw *= 2) {
-        if (p->is_linear && tw != 64) continue;
-        if (!p->is_linear && tw > 4 && div_up(p->Wo, 4) * 4 <= tw / 2) break;   // wider than needed
-        const int wop = div_up(p->Wo, tw) * tw;
-        // alignment unit of staged rows: the widest vector whose left pad stays <= 1
-        int vec = 1;
-        for (int v = vw; v >= 1; v >>= 1) {
-            if (!p->is_linear && v > tw * p->SW) continue;
-            const int left = (v - p->PW % v) % v;
-            if (left <= 1 || p->PW % v == 0) { vec = v; break; }
-        }
-        const int left = (vec - p->PW % vec) % vec;
-        const int need = left + (tw - 1) * p->SW + p->KW + (p->gather == 2 ? 1 : 0);
-        // linear layers keep RL = 64 for every batch (their vector width varies)
-        const int rl = p->is_linear ? 64 : div_up(need, vec) * vec;
-        const int trw = kNPIX / tw;
-        for (int nsub = 1; nsub <= 4; nsub *= 2) {
-            if (trw * nsub > kMaxTileRows || (p->is_linear && nsub > 1)) continue;
-            const int nslot = max_slots(trw * nsub, p->Ho, p->KH, p->SH, p->PH);
-            if (nslot > kMaxSlots) continue;
-            const int chs = nslot * rl;
-            const int64_t pch = (int64_t)chs * p->esize;   // patch bytes per channel
-            MBlock cand[8];
-            const int nc = mblock_candidates(*p, 4 / nsub, cand);
-            for (int ci = 0; ci < nc; ++ci) {
-                const MBlock &m = cand[ci];
-                const int64_t lds_a = (int64_t)m.mb_tiles * p->S * a_step;
-                const int64_t lds_d = (int64_t)m.mb_groups * p->LP * 2;
-                // residency x LDS budget (two or one workgroups per CU) x steps per item
-                for (int opt = 0; opt < 8; ++opt) {
-                    const int resident = opt < 2;
-                    const int64_t budget = (opt & 1) ? kLdsOneWG : kLdsPerWG;
-                    const int smax = resident ? 0 : std::min(p->S, 4 >> ((opt - 2) >> 1));
-                    if (!resident && opt >= 4 && smax == std::min(p->S, 4 >> ((opt - 4) >> 1))) continue;
-                    int64_t cc, lds_patch, lds_buf, total;
-                    const int64_t item = resident ? 0
-                        : (int64_t)m.mb_tiles * smax * a_step + (int64_t)m.mb_groups * smax * 64;
-                    if (resident) {
-                        const int64_t free_b = budget - align256(lds_a) - align256(lds_d);
+    for (int nsub = 1; nsub <= 4; nsub *= 2) {
+        const int TG = kGroups * nsub;
+        const int trw = rows_spanned(TG, p->GPR);
+        if (trw > kMaxTileRows) continue;
+        const int nslot = max_slots(TG, p->GPR, p->Ho, p->KH, p->SH, p->PH);
+        if (nslot > kMaxSlots) continue;
+        const int chs = nslot * p->RS;                    // patch elements per channel
+        const int64_t pch = (int64_t)chs * p->esize;
+        const int Q = kWaves / nsub;
+        const double n_pt = std::ceil(total_groups / TG);
+        for (int qmode = 0; qmode <= 1; ++qmode) {
+            if (qmode == 1 && Q == 1) continue;
+            const int KS = qmode ? Q : 1;
+            for (int TM = 1; TM <= 4; TM *= 2) {
+                // instantiated kernels: fp32 and per-element gathers at most 2 m-tiles per
+                // wave and no step split; 16-byte stride-2 gathers at most 4 m-tiles
+                const bool narrow = p->esize == 4 || p->gather == 0;
+                if (narrow && (TM > 2 || qmode == 1)) continue;
+                if (p->gather == 2 && TM > 4) continue;
+                int TPG, MBT, MBG, n_mb;
+                MBT = TM * (qmode == 0 ? Q : 1);
+                if (p->shared) {
+                    TPG = TM;
+                    if (MBT > 1 && MBT >= 2 * n_mt) continue;     // mostly idle waves
+                    MBG = 1;
+                    n_mb = div_up(n_mt, MBT);
+                } else {
+                    TPG = std::min(TM, mpg);
+                    if (TM % TPG) continue;
+                    if (MBT % mpg != 0 && mpg % MBT != 0) continue;
+                    if (MBT > 1 && MBT >= 2 * n_mt) continue;
+                    MBG = std::max(1, MBT / mpg);
+                    n_mb = div_up(n_mt, MBT);
+                }
+                const int64_t d_res = align256((int64_t)MBG * p->LP * 2);
+                const int64_t a_all = (int64_t)MBT * p->S * astep;
+                for (int bi = 0; bi < 4; ++bi) {
+                    const int64_t budget = budgets[bi];
+                    for (int opt = 0; opt < 10; ++opt) {
+                        const int nb = opt < 5 ? 3 : 2;   // buffers (two when three do not fit)
+                        const int resident = opt % 5 == 0;
+                        const int smax = resident ? 0 : (1 << (opt % 5 - 1));   // 1, 2, 4, 8
+                        if (!resident && smax > p->S) continue;
+                        const int64_t astage = resident ? 0 : (int64_t)MBT * smax * astep;
+                        const int64_t fixed = d_res + (resident ? align256(a_all) : 0) + 256;
+                        const int64_t free_b = budget - fixed - nb * align256(astage) - nb * 512;
                         if (free_b <= 0) continue;
-                        cc = free_b / (2 * pch);
-                    } else {
-                        const int64_t free_b = budget / 2 - item - 256;
-                        if (free_b <= 0) continue;
-                        cc = free_b / pch;
-                    }
-                    if (cc > p->Cin) cc = p->Cin;
-                    if (cc < span_req) continue;
-                    lds_patch = (int64_t)cc * pch;
-                    lds_patch = (lds_patch + 15) & ~(int64_t)15;
-                    if (resident) {
-                        lds_buf = lds_patch;
-                        total = align256(lds_a) + align256(lds_d) + 2 * lds_patch;
-                    } else {
-                        lds_buf = align256(lds_patch + item);
-                        total = 2 * lds_buf;
-                    }
-                    if (total > budget) continue;
-                    // cost per output pixel (bytes moved into LDS, weighted)
-                    const double px = (double)kNPIX * nsub;
-                    const int chunks = (int)div_up64(p->Cin, cc);
-                    // short contiguous runs per staged row cost extra load instructions
-                    const double run = (double)rl * p->esize;
-                    const double patch = (double)m.n_mb * p->Cin * pch / px * (1.0 + 32.0 / std::min(run, 128.0));
-                    const double wts = resident ? (double)lds_a * m.n_mb / (px * 16.0) : (double)a_total / px;
-                    const double gathers = (m.split ? (double)p->mt_per_group * p->n_groups / m.T
-                                                    : (double)p->n_groups) * p->S * 64.0;
-                    double cost = ((double)wop / p->Wo) * (patch + wts + 0.3 * gathers);
-                    cost *= 1.0 + 0.05 * (chunks - 1);
-                    if (!resident) cost *= 1.0 + 0.1 * (4 / std::max(smax, 1) - 1);   // items per step
-                    if (budget > kLdsPerWG) cost *= 1.6;                              // one workgroup per CU
-                    if (cost < best * (1 - 1e-9)) {
-                        best = cost;
-                        Plan q = *p;
-                        q.TW = tw; q.TRW = trw; q.Wop = p->is_linear ? div_up(p->Wo, 64) * 64 : wop;
-                        q.NSUB = nsub; q.VEC = p->is_linear ? vw : vec; q.LEFT = left; q.RL = rl;
-                        q.NSLOT = nslot; q.CH_STRIDE = chs; q.CC = (int)cc;
-                        q.split = m.split; q.T = m.T; q.G = m.G; q.msets = m.msets;
-                        q.mb_tiles = m.mb_tiles; q.mb_groups = m.mb_groups; q.mpg_blocks = m.mpg_blocks;
-                        q.n_mb = m.n_mb; q.resident = resident; q.SMAX = smax;
-                        q.lds_a = resident ? (int)align256(lds_a) : 0;
-                        q.lds_d = resident ? (int)align256(lds_d) : 0;
-                        q.lds_patch = (int)lds_patch;
-                        q.lds_buf = (int)lds_buf;
-                        q.lds_total = (int)total;
-                        bestp = q;
+                        int64_t cc = free_b / (nb * pch);
+                        cc = std::min<int64_t>(cc, std::min(p->Cin, kMaxCC));
+                        cc = std::min<int64_t>(cc, 65536 / chs);                       // 16-bit offsets
+                        if (cc < span_req || cc < 1) continue;
+                        const int fr = (int)div_up64(cc * nslot * p->RG, kThreads);
+                        const int64_t lds_patch = align256(cc * pch + 128);
+                        const int64_t lds_buf = lds_patch + align256(astage);
+                        int64_t total = fixed + nb * lds_buf;
+                        if (qmode == 1) total = std::max<int64_t>(total, (int64_t)2 * TM * 4096);   // partial sums
+                        if (total > budget) continue;
+
+                        // ---- score (nominal batch), in CU cycles ----
+                        // persistent workgroups: occ per CU, each walking tpw pixel tiles
+                        const int occ = std::min(TM == 1 ? 3 : 2, (160 * 1024) / (int)(total + kLdsStatic));
+                        if (occ < 1) continue;
+                        double wpm = std::max(1.0, std::ceil(256.0 * occ / n_mb));
+                        if (KS > 1 || wpm > n_pt) wpm = n_pt;
+                        const double tpw = std::ceil(n_pt / wpm);
+                        const double n_wg = std::ceil(n_pt / tpw) * n_mb;
+                        double nch = std::ceil((double)p->Cin / cc);
+                        if (!resident) nch = std::max(nch, std::ceil((double)p->S / smax));
+                        // bytes into LDS: patch rows (data only) per tile, weights per tile or
+                        // once per workgroup when resident, offsets once per workgroup
+                        const double patch_b = (double)p->Cin * nslot * p->W * p->esize * 1.15;
+                        const double l2_bytes = n_pt * n_mb * patch_b +
+                                                (resident ? n_wg : n_pt * n_mb) * (double)a_all +
+                                                n_wg * MBG * p->LP * 2.0;
+                        const double t_l2 = l2_bytes / (256.0 * 40.0);
+                        // LDS reads per tile: gathers, weights, offsets of every stage
+                        const int GW = TM / TPG;
+                        const double stages = (double)p->S / KS * GW * kWaves;          // per tile, all waves
+                        const double lds_b = n_pt * n_mb * stages *
+                                             (8.0 * 64 * (p->gather == 2 ? 16 : 8) * 1.3 + TPG * 1024.0 + 1024.0);
+                        const double t_lds = lds_b / (256.0 * 100.0);
+                        const double mfma = n_pt * n_mb * (double)p->S * (kWaves / KS) * TM * 4 *
+                                            (p->esize == 4 ? 32.0 : 16.0) / 4.0;           // per SIMD-cycle
+                        const double t_mfma = mfma / (256.0 * 0.7);
+                        const double hbm = ((double)nominal_rows / p->Ho * p->Cin * p->H * p->W * p->esize +
+                                            total_groups * 4 * p->R * 2.0) / 5.5e12 * 2.4e9;
+                        // per chunk: barrier, fill wait and pipeline refill, hidden by occ - 1 others
+                        const double sync = n_pt * n_mb * nch * 900.0 / (256.0 * occ) * (occ > 1 ? 0.6 : 1.0);
+                        // per workgroup: header, tables, first fill
+                        const double start = std::ceil(n_wg / (256.0 * occ)) * 6000.0;
+                        double cyc = std::max(std::max(t_l2, t_lds), std::max(t_mfma, hbm)) + sync * (nb == 2 ? 1.6 : 1.0) + start;
+                        if (qmode == 1) cyc += 1500.0;                                   // partial-sum reduction
+                        if (cyc < best * (1 - 1e-9)) {
+                            best = cyc;
+                            Plan q = *p;
+                            q.NSUB = nsub; q.TRWMAX = trw; q.NSLOT = nslot; q.CH_STRIDE = chs;
+                            q.CC = (int)cc; q.FR = fr;
+                            q.qmode = qmode; q.KS = KS; q.TM = TM; q.TPG = TPG;
+                            q.MBT = MBT; q.MBG = MBG; q.n_mb = n_mb;
+                            q.resident = resident; q.SMAX = smax; q.NB = nb;
+                            q.lds_d = (int)d_res;
+                            q.lds_a = resident ? (int)align256(a_all) : 0;
+                            q.lds_patch = (int)lds_patch;
+                            q.lds_astage = (int)align256(astage);
+                            q.lds_buf = (int)lds_buf;
+                            q.lds_total = (int)total;
+                            bestp = q;
+                        }
                     }
                 }
             }
@@ -279,23 +283,21 @@ bsp_status make_plan(const bsp_scheme *s, const bsp_conv_shape *conv, bsp_dtype 
     }
     if (best >= 1e300) return BSP_EUNSUPPORTED;
     *p = bestp;
-    {
-        const int vb = p->VEC * p->esize;
-        p->gran = vb >= 16 ? 16 : (vb >= 4 ? 4 : 0);
-    }
+    p->n_mt_pad = p->n_mb * p->MBT;
+    p->n_g_pad = p->shared ? 1 : std::max(p->n_groups, p->n_mb * p->MBG);
+    if (p->shared) p->n_mt_pad = std::max(p->n_mt_pad, n_mt);
 
     // dev_tiles layout
     p->off_chunks = kHeaderBytes;
     p->off_desc = align256(p->off_chunks + (int64_t)16 * p->S);
     p->off_desc16 = align256(p->off_desc + (int64_t)4 * p->n_groups * p->LP);
-    p->off_a = align256(p->off_desc16 + (int64_t)2 * p->n_groups * p->LP);
-    p->tile_bytes = p->off_a + (int64_t)p->n_groups * p->mt_per_group * p->S * a_step;
+    p->off_a = align256(p->off_desc16 + (int64_t)2 * p->n_g_pad * p->LP);
+    p->tile_bytes = p->off_a + (int64_t)p->n_mt_pad * p->S * astep;
 
     const int fpv[] = {p->R, p->C, p->bh_eff, p->bw_eff, p->reg, p->rate, p->dt, p->n_groups,
-                       p->mt_per_group, p->LP, p->S, p->CH_STRIDE, p->RL, p->LEFT, p->NSLOT,
-                       p->CC, p->KH, p->KW, p->is_linear, p->is_linear ? 0 : p->SW,
-                       p->is_linear ? 0 : p->TW, p->NSUB, p->SMAX, p->resident, p->split, p->T,
-                       p->G, p->msets};
+                       p->mt_per_group, p->LP, p->S, p->CH_STRIDE, p->RS, p->LEFT, p->NSLOT,
+                       p->CC, p->KH, p->KW, p->is_linear, p->SW, p->NSUB, p->SMAX, p->resident,
+                       p->MBT, p->MBG, p->n_mt_pad, p->n_g_pad, p->GE, p->NB, 5};
     p->fingerprint = fnv1a(fpv, (int)(sizeof(fpv) / sizeof(fpv[0])));
     return BSP_OK;
 }
