@@ -133,7 +133,10 @@ struct Plan {
     int TRWMAX;                   // output rows a tile may span
     int NSLOT;                    // staged input rows per tile (worst case)
     int GE;                       // elements per 16-byte granule
-    int LEFT, RS, RG, CH_STRIDE;  // patch row: left pad, row stride (elements, granules), channel stride
+    int LEFT, RS, RG, CH_STRIDE;  // patch row: left pad (0), row stride (elements, granules), channel stride
+    int V;                        // copies of each staged row (stride 1: min(KW, 4), shifted by 0..V-1)
+    int VS;                       // patch stride between the copies of one channel
+    int POFF;                     // patch offset of output column 0 for filter column 0 (V == 1)
     int CC;                       // channels of one chunk
     int gather;                   // 1: stride-1 vector reads, 2: stride-2 16-byte reads, 0: per element
     // waves and m-blocks
@@ -147,6 +150,11 @@ struct Plan {
     int SMAX;                     // steps per chunk when weights are staged (0 = unlimited)
     int FR;                       // patch granules per thread and chunk
     int lds_d, lds_a, lds_patch, lds_astage, lds_buf, lds_total;   // dynamic LDS bytes
+    // pointwise kernel (1x1 without padding, stride 1 or 2; linear layers)
+    int pw;                       // 1: the pointwise kernel runs this layer
+    int NGR;                      // 16-byte granules per patch row (one channel of a tile)
+    int gpg;                      // 4-pixel groups per granule
+    int occ;                      // workgroups per CU the plan is sized for
     // dev_tiles layout (bytes)
     int64_t off_chunks, off_desc, off_desc16, off_a, tile_bytes;
     uint64_t fingerprint;
@@ -186,9 +194,51 @@ struct ConvArgs {
     FastDiv div_GPR;              // group -> (row, group in row)
     FastDiv div_Ho;               // flattened output row -> (image, oh)
     FastDiv div_RG;               // patch granule -> (row, granule in row)
-    FastDiv div_NSLOT;            // patch row -> (channel, slot)
+    FastDiv div_CHG;              // patch granule -> (channel, granule in channel)
+    FastDiv div_VSG;              // granule in channel -> (filter column, granule in copy)
+    int CHG, VSG;                 // granules per channel, per shifted copy
+    int V, POFF;                  // copies per staged row, patch offset of output column 0
     FastDiv div_nmb;              // workgroup -> (pixel tile, m-block)
 };
+
+// Launch arguments of the pointwise kernel.  Output pixels are numbered in groups
+// of 4: at stride 1 the pixels of an image are one row of Ho * Wo pixels; at stride
+// 2 each output row is a row of groups.  Rows hold GPR groups.
+struct PwArgs {
+    const void *x;
+    void *y;
+    const uint8_t *tiles;
+    const float *bias;
+    int relu, out_bf16;
+    int R;                        // output rows of the GEMM (filters, out features)
+    int Ho;                       // group rows per image
+    int Wo;                       // output pixels per group row
+    int GPR;                      // groups per group row
+    int in_row;                   // input elements from one group row to the next
+    int SW;                       // stride
+    int64_t x_is, y_is;           // image strides of x and y (elements)
+    int64_t x_cs, y_cs;           // channel strides of x and y (elements)
+    int64_t x_total;              // elements of x (copies never reach past it)
+    int64_t n_groups_total;       // groups over all images
+    int NSUB, lg_nsub, NGR, lg_ngr, gpg, FR;
+    int n_groups, group_rows, mt_per_group, LP, S;
+    int MBT, MBG, n_mb, resident, NB;
+    int lds_d, lds_a, lds_patch, lds_astage, lds_buf;
+    int n_pt;                     // pixel tiles
+    int tiles_per_wg;             // consecutive pixel tiles one workgroup walks
+    int grid_valid;
+    int64_t off_chunks, off_desc16, off_a;
+    uint32_t fp_lo, fp_hi;
+    FastDiv div_GPR;              // group -> (group row, group in row)
+    FastDiv div_Ho;               // group row -> (image, row in image)
+    FastDiv div_nmb;              // workgroup -> (pixel tile, m-block)
+};
+
+// Workgroups per CU the pointwise kernel's register budget allows (its launch
+// bound): element size, gather mode (1: stride 1, 2: stride 2), m-tiles per wave.
+BSP_HD constexpr int pw_occ(int esize, int mode, int tm) {
+    return esize == 4 ? (tm == 1 ? 3 : 2) : (tm == 4 ? 2 : (tm == 2 || mode == 2 ? 3 : 4));
+}
 
 inline int div_up(int a, int b) { return (a + b - 1) / b; }
 inline int64_t div_up64(int64_t a, int64_t b) { return (a + b - 1) / b; }

@@ -1,9 +1,17 @@
 // Launcher of the forward kernel: argument set-up and instantiation choice.  The
 // kernel template lives in bsp_fwd.h; its instantiations are compiled in
 // bsp_fwd_*.hip (one translation unit per element type and gather mode).
-#include "bsp_fwd.h"
+#include "bsp_pw.h"
 
 namespace bsp {
+namespace pw {
+
+pw_fn pick_b1(int TM, int TPG, int KS);
+pw_fn pick_b2(int TM, int TPG, int KS);
+pw_fn pick_f(int TM, int TPG, int KS);
+
+}  // namespace pw
+
 namespace fwd {
 
 // instantiation sets, one per translation unit (bsp_fwd_*.hip)
@@ -22,8 +30,92 @@ static fwd_fn pick(int dt, int mode, int TM, int TPG, int KS) {
 
 }  // namespace fwd
 
+static int log2_int(int v) {
+    int l = 0;
+    while ((1 << l) < v) ++l;
+    return l;
+}
+
+// Pointwise layers: the image (stride 1) or each output row (stride 2) is a run of
+// 4-pixel groups; a linear layer's batch is one image of n pixels.
+static hipError_t launch_pw(const Plan &p, int n, const void *x, const uint8_t *tiles, const float *bias,
+                            int relu, int out_bf16, void *y, hipStream_t st) {
+    PwArgs a;
+    memset(&a, 0, sizeof(a));
+    a.x = x;
+    a.y = y;
+    a.tiles = tiles;
+    a.bias = bias;
+    a.relu = relu;
+    a.out_bf16 = out_bf16;
+    a.R = p.R;
+    a.SW = p.SW;
+    int64_t images;
+    if (p.is_linear) {
+        images = 1;
+        a.Ho = 1; a.Wo = n; a.in_row = 0;
+        a.x_cs = n; a.y_cs = n; a.x_is = 0; a.y_is = 0;
+    } else if (p.SW == 1) {
+        images = n;
+        a.Ho = 1; a.Wo = p.H * p.W; a.in_row = 0;
+        a.x_cs = (int64_t)p.H * p.W; a.y_cs = a.x_cs;
+        a.x_is = (int64_t)p.Cin * a.x_cs; a.y_is = (int64_t)p.R * a.y_cs;
+    } else {
+        images = n;
+        a.Ho = p.Ho; a.Wo = p.Wo; a.in_row = p.SH * p.W;
+        a.x_cs = (int64_t)p.H * p.W; a.y_cs = (int64_t)p.Ho * p.Wo;
+        a.x_is = (int64_t)p.Cin * a.x_cs; a.y_is = (int64_t)p.R * a.y_cs;
+    }
+    a.GPR = p.SW == 1 ? (div_up(a.Wo, 4) + p.gpg - 1) / p.gpg * p.gpg : div_up(a.Wo, 4);
+    a.x_total = (p.is_linear ? (int64_t)p.Cin * n : images * a.x_is);
+    a.n_groups_total = images * a.Ho * a.GPR;
+    const int64_t n_pt = div_up64(a.n_groups_total, (int64_t)kGroups * p.NSUB);
+    if (n_pt <= 0) return hipSuccess;
+    // persistent workgroups: about occ per CU; each walks a range of pixel tiles of
+    // its m-block (one tile when the waves split the steps)
+    int64_t wpm = std::max<int64_t>(1, div_up64((int64_t)256 * p.occ, p.n_mb));
+    if (p.KS > 1 || wpm > n_pt) wpm = n_pt;
+    const int64_t tpw = div_up64(n_pt, wpm);
+    const int64_t gv = div_up64(n_pt, tpw) * p.n_mb;
+    if (gv > INT32_MAX - 8 || n_pt > INT32_MAX || images * a.Ho > INT32_MAX ||
+        a.n_groups_total + kGroups * 4 > INT32_MAX)
+        return hipErrorInvalidValue;
+    a.n_pt = (int)n_pt;
+    a.tiles_per_wg = (int)tpw;
+    a.NSUB = p.NSUB; a.lg_nsub = log2_int(p.NSUB);
+    a.NGR = p.NGR; a.lg_ngr = log2_int(p.NGR);
+    a.gpg = p.gpg; a.FR = p.FR;
+    a.n_groups = p.n_groups; a.group_rows = p.group_rows; a.mt_per_group = p.mt_per_group;
+    a.LP = p.LP; a.S = p.S;
+    a.MBT = p.MBT; a.MBG = p.MBG; a.n_mb = p.n_mb; a.resident = p.resident; a.NB = p.NB;
+    a.lds_d = p.lds_d; a.lds_a = p.lds_a; a.lds_patch = p.lds_patch; a.lds_astage = p.lds_astage;
+    a.lds_buf = p.lds_buf;
+    a.grid_valid = (int)gv;
+    a.off_chunks = p.off_chunks;
+    a.off_desc16 = p.off_desc16;
+    a.off_a = p.off_a;
+    a.fp_lo = (uint32_t)p.fingerprint;
+    a.fp_hi = (uint32_t)(p.fingerprint >> 32);
+    a.div_GPR = make_fastdiv((uint32_t)a.GPR);
+    a.div_Ho = make_fastdiv((uint32_t)a.Ho);
+    a.div_nmb = make_fastdiv((uint32_t)p.n_mb);
+    pw::pw_fn fn = nullptr;
+    if (p.dt == BSP_F32) fn = p.SW == 1 ? pw::pick_f(p.TM, p.TPG, p.KS) : nullptr;
+    else fn = p.SW == 1 ? pw::pick_b1(p.TM, p.TPG, p.KS) : pw::pick_b2(p.TM, p.TPG, p.KS);
+    if (!fn) return hipErrorInvalidValue;
+    const int grid = (int)(div_up64(gv, 8) * 8);
+    if (p.lds_total > 48 * 1024) {
+        hipError_t e = hipFuncSetAttribute((const void *)fn, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                           p.lds_total);
+        if (e != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL(fn, dim3(grid), dim3(kThreads), (size_t)p.lds_total, st, a);
+    return hipGetLastError();
+}
+
 hipError_t launch_conv(const Plan &p, int n, const void *x, const uint8_t *tiles, const float *bias,
                        int relu, int out_bf16, void *y, hipStream_t st) {
+    if (p.pw) return launch_pw(p, n, x, tiles, bias, relu, out_bf16, y, st);
     ConvArgs a;
     memset(&a, 0, sizeof(a));
     a.x = x;
@@ -81,7 +173,13 @@ hipError_t launch_conv(const Plan &p, int n, const void *x, const uint8_t *tiles
     a.div_GPR = make_fastdiv((uint32_t)p.GPR);
     a.div_Ho = make_fastdiv((uint32_t)a.Ho);
     a.div_RG = make_fastdiv((uint32_t)p.RG);
-    a.div_NSLOT = make_fastdiv((uint32_t)p.NSLOT);
+
+    a.VSG = p.NSLOT * p.RG;
+    a.CHG = p.V * a.VSG;
+    a.V = p.V;
+    a.POFF = p.POFF;
+    a.div_CHG = make_fastdiv((uint32_t)a.CHG);
+    a.div_VSG = make_fastdiv((uint32_t)a.VSG);
     a.div_nmb = make_fastdiv((uint32_t)p.n_mb);
     fwd::fwd_fn fn = fwd::pick(p.dt, p.gather, p.TM, p.TPG, p.KS);
     if (!fn) return hipErrorInvalidValue;

@@ -89,6 +89,44 @@ __device__ __forceinline__ void dma_run(const unsigned char *src, uint32_t dst, 
     }
 }
 
+// Batches of asynchronous 16-byte copies global -> LDS with one M0 (LDS base) for up
+// to four copies: copy k of a batch writes LDS bytes m0 + 1024 k + 16 l for lane l and
+// reads 16 bytes at its own source address.  The immediate offset 1024 k moves both
+// the LDS destination and the source, so each source is passed lowered by it.  Every
+// lane takes part; each copy is one vector memory operation of the wave, so waits can
+// count them.  Rewriting M0 before every copy would stall issue on the previous copy.
+__device__ __forceinline__ void dma_b4(const unsigned char *s0, const unsigned char *s1, const unsigned char *s2,
+                                       const unsigned char *s3, uint32_t m0, int n) {
+    uint32_t sv;
+    const int base = uni((int)m0);
+    switch (uni(n)) {
+        case 1:
+            asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %2\n\ts_nop 0\n\t"
+                         "global_load_lds_dwordx4 %1, off\n\ts_mov_b32 m0, %0"
+                         : "=&s"(sv) : "v"(s0), "s"(base) : "memory");
+            break;
+        case 2:
+            asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %3\n\ts_nop 0\n\t"
+                         "global_load_lds_dwordx4 %1, off\n\tglobal_load_lds_dwordx4 %2, off offset:1024\n\t"
+                         "s_mov_b32 m0, %0"
+                         : "=&s"(sv) : "v"(s0), "v"(s1 - 1024), "s"(base) : "memory");
+            break;
+        case 3:
+            asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %4\n\ts_nop 0\n\t"
+                         "global_load_lds_dwordx4 %1, off\n\tglobal_load_lds_dwordx4 %2, off offset:1024\n\t"
+                         "global_load_lds_dwordx4 %3, off offset:2048\n\ts_mov_b32 m0, %0"
+                         : "=&s"(sv) : "v"(s0), "v"(s1 - 1024), "v"(s2 - 2048), "s"(base) : "memory");
+            break;
+        default:
+            asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %5\n\ts_nop 0\n\t"
+                         "global_load_lds_dwordx4 %1, off\n\tglobal_load_lds_dwordx4 %2, off offset:1024\n\t"
+                         "global_load_lds_dwordx4 %3, off offset:2048\n\tglobal_load_lds_dwordx4 %4, off offset:3072\n\t"
+                         "s_mov_b32 m0, %0"
+                         : "=&s"(sv) : "v"(s0), "v"(s1 - 1024), "v"(s2 - 2048), "v"(s3 - 3072), "s"(base) : "memory");
+            break;
+    }
+}
+
 // ---- operand gathers -------------------------------------------------------------
 // v[j] holds pixels 0..3 (16 bits each) of kept column j of this lane; B[nt] is the
 // 8-wide k-vector of pixel nt.
@@ -492,96 +530,111 @@ __global__ __launch_bounds__(kThreads, TM == 1 ? 3 : 2) void k_fwd(ConvArgs a) {
         for (int i = used + tid; i < a.NSLOT; i += kThreads) s_slot[sb][i] = make_int2(-1, 0);
     };
 
-    // ---- patch granules: granule v = 256 j + tid of a chunk's patch ----
+    // ---- patch granules.  A chunk's patch holds, per channel, V copies of the tile's
+    // staged input rows: at stride 1 copy m starts at input column m - PW, so the reads
+    // of filter column s (copy s % V) start at a multiple of 4 elements; otherwise one
+    // copy with LEFT zeros before input column 0.  Wave w issues copy slots
+    // w * FR .. + FR - 1; slot u fills granules 64 u .. + 63, lane l granule 64 u + l.
     // off: element offset of the granule in x without the chunk's first channel;
     // meta: channel in the chunk (bits 0-10), elements past the row end (bits 11-13),
-    // kind (bits 14-15).  Decoded from the tile's row table at each use, four granules
-    // at a time so that the table reads overlap.
-    const int total_g = a.CC * a.NSLOT * a.RG;           // granules of a full chunk
+    // elements before the row start (bits 14-16), kind (bits 17-18).  Decoded from the
+    // tile's row table at each use, four granules at a time so the table reads overlap.
+    const int total_g = a.CC * a.CHG;                    // granules of a full chunk
     auto decode = [&](int sb, int j, int &off, int &meta) {
-        const int v = j * kThreads + tid;
-        const int row = (int)fdiv((uint32_t)v, a.div_RG), gi = v - row * a.RG;
-        const int c_rel = (int)fdiv((uint32_t)row, a.div_NSLOT), slot = row - c_rel * a.NSLOT;
-        int kind = kKindNone, tail = 0;
+        const int v = (wave * a.FR + j) * 64 + lane;
+        const int c_rel = (int)fdiv((uint32_t)v, a.div_CHG), rem = v - c_rel * a.CHG;
+        const int s = (int)fdiv((uint32_t)rem, a.div_VSG), rem2 = rem - s * a.VSG;
+        const int slot = (int)fdiv((uint32_t)rem2, a.div_RG), gi = rem2 - slot * a.RG;
+        int kind = kKindNone, tail = 0, head = 0;
         off = 0;
         if (v < total_g) {
             const int2 so = s_slot[sb][slot];
-            const int col0 = gi * a.GE - a.LEFT;
-            if (so.x < 0 || col0 < 0 || col0 >= so.y) {
+            const int col0 = gi * a.GE + (a.V > 1 ? s - a.PW : -a.LEFT);
+            if (so.x < 0 || col0 >= so.y || col0 + a.GE <= 0) {
                 kind = kKindZero;
             } else {
                 kind = kKindData;
                 tail = max(0, col0 + a.GE - so.y);
+                head = max(0, -col0);
                 off = so.x + c_rel * (int)a.x_cs + col0;
             }
         }
-        meta = c_rel | (tail << 11) | (kind << 14);
+        meta = c_rel | (tail << 11) | (head << 14) | (kind << 17);
     };
-    auto kind_of = [&](int m) { return m >> 14; };
+    auto kind_of = [&](int m) { return m >> 17; };
     auto crel_of = [&](int m) { return m & 0x7ff; };
     auto tail_of = [&](int m) { return (m >> 11) & 7; };
+    auto head_of = [&](int m) { return (m >> 14) & 7; };
     auto for_granules = [&](int sb, auto act) {
         for (int j0 = 0; j0 < a.FR; j0 += 4) {
             int off[4], meta[4];
 #pragma unroll
             for (int u = 0; u < 4; ++u)
                 if (j0 + u < a.FR) decode(sb, j0 + u, off[u], meta[u]);
-#pragma unroll
-            for (int u = 0; u < 4; ++u)
-                if (j0 + u < a.FR) act(j0 + u, off[u], meta[u]);
+            act(j0, off, meta);
         }
     };
-    // copies one wave issues for a chunk's patch: instruction j is issued when its
-    // first lane holds a granule of the patch
-    int n_patch = 0;
-    for (int j = 0; j < a.FR; ++j) n_patch += (j * kThreads + wave * 64 < total_g) ? 1 : 0;
+    // copies one wave issues for a chunk's patch: every slot
+    const int n_patch = a.FR;
 
-    // issue the copies of one chunk into buf (patch: data, zero rows and pads, channels
-    // past the chunk's count read zeros; weights when staged); returns the wave's count
+    // issue the copies of one chunk into buf (patch: data; zero rows, pads, channels past
+    // the chunk's count and slots past the patch read zeros; weights when staged);
+    // returns the wave's count
     auto fill = [&](int sb, int4 cd, unsigned char *buf) {
         const int64_t cbase = (int64_t)cd.z * a.x_cs;
-        const uint32_t pbase = ldsa(buf) + (uint32_t)(wave * 64 * 16);
-        for_granules(sb, [&](int j, int off, int meta) {
-            if (j * kThreads + wave * 64 < total_g) {
-                const int kind = kind_of(meta);
-                if (kind != kKindNone) {
-                    const int64_t e = (int64_t)off + cbase;
-                    const bool data = kind == kKindData && crel_of(meta) < cd.w && e + a.GE <= a.x_total;
-                    dma16(data ? xb + e * (int)sizeof(E) : zero, pbase + (uint32_t)(j * kThreads * 16));
-                }
+        const uint32_t pbase = ldsa(buf) + (uint32_t)(wave * a.FR * 1024);
+        for_granules(sb, [&](int j0, const int *off, const int *meta) {
+            const unsigned char *src[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int64_t e = (int64_t)off[u] + cbase;
+                const bool data = kind_of(meta[u]) == kKindData && crel_of(meta[u]) < cd.w && e >= 0 &&
+                                  e + a.GE <= a.x_total;
+                src[u] = data ? xb + e * (int)sizeof(E) : zero;
             }
+            dma_b4(src[0], src[1], src[2], src[3], pbase + (uint32_t)(j0 * 1024), min(4, a.FR - j0));
         });
         int n = n_patch;
         if (!a.resident) {
-            const int ns = cd.y - cd.x;
-            const unsigned char *ast = buf + a.lds_patch;
-            const int per_m = ns * AI;
-            // copy index i = m * per_m + r goes to wave i % 4
-            int i0 = 0;
-            for (int m = 0; m < a.MBT; ++m, i0 += per_m) {
-                const unsigned char *src = A_g + ((size_t)(mt_first + m) * a.S + cd.x) * ASTEP + lane * 16;
-                for (int r = (wave - i0 % kWaves + kWaves) % kWaves; r < per_m; r += kWaves) {
-                    dma16(src + (size_t)r * 1024, ldsa(ast) + (uint32_t)(i0 + r) * 1024);
-                    ++n;
-                }
+            // weight copies: per m-tile a contiguous run of ns * AI KB in both places;
+            // wave w takes copies w * naw .. + naw - 1, in batches inside one run
+            const int per_m = (cd.y - cd.x) * AI;
+            const int na = a.MBT * per_m;
+            const int naw = (na + kWaves - 1) / kWaves;
+            const uint32_t ab = ldsa(buf + a.lds_patch);
+            int c = wave * naw;
+            const int c_end = min(na, c + naw);
+            while (c < c_end) {
+                const int m = c / per_m, r = c - m * per_m;
+                const int nb = min(4, min(c_end - c, per_m - r));
+                const unsigned char *src = A_g + ((size_t)(mt_first + m) * a.S + cd.x) * ASTEP + (size_t)r * 1024 + lane * 16;
+                dma_b4(src, src + 1024, src + 2048, src + 3072, ab + (uint32_t)c * 1024, nb);
+                n += nb;
+                c += nb;
             }
         }
         return n;
     };
-    // after the copies landed: zero the part of a row's last granule past the row end,
-    // and load granules that would read past the end of x element by element
+    // after the copies landed: zero the elements of a granule before the row start and
+    // past the row end, and load granules that would read outside x element by element
     auto fixup = [&](int sb, int4 cd, unsigned char *buf) {
         const int64_t cbase = (int64_t)cd.z * a.x_cs;
-        for_granules(sb, [&](int j, int off, int meta) {
-            const int tail = tail_of(meta);
-            if (kind_of(meta) == kKindData && crel_of(meta) < cd.w) {
-                E *dst = (E *)(buf + (size_t)(j * kThreads + tid) * 16);
-                const int64_t e = (int64_t)off + cbase;
-                if (e + a.GE > a.x_total) {
-                    const E *src = (const E *)a.x + e;
-                    for (int i = 0; i < a.GE - tail; ++i) dst[i] = src[i];
-                } else if (tail) {
-                    for (int i = a.GE - tail; i < a.GE; ++i) dst[i] = (E)0;
+        for_granules(sb, [&](int j0, const int *off, const int *meta) {
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                if (j0 + u < a.FR && kind_of(meta[u]) == kKindData && crel_of(meta[u]) < cd.w) {
+                    const int tail = tail_of(meta[u]), head = head_of(meta[u]);
+                    E *dst = (E *)(buf + ((size_t)(wave * a.FR + j0 + u) * 64 + lane) * 16);
+                    const int64_t e = (int64_t)off[u] + cbase;
+                    if (e < 0 || e + a.GE > a.x_total) {
+                        const E *src = (const E *)a.x + e;
+                        for (int i2 = 0; i2 < a.GE; ++i2)
+                            dst[i2] = (i2 >= head && i2 < a.GE - tail && e + i2 >= 0 && e + i2 < a.x_total)
+                                          ? src[i2] : (E)0;
+                    } else if (head | tail) {
+                        for (int i2 = 0; i2 < head; ++i2) dst[i2] = (E)0;
+                        for (int i2 = a.GE - tail; i2 < a.GE; ++i2) dst[i2] = (E)0;
+                    }
                 }
             }
         });
@@ -597,7 +650,7 @@ __global__ __launch_bounds__(kThreads, TM == 1 ? 3 : 2) void k_fwd(ConvArgs a) {
         const int64_t gc = min(grp, G1);
         const int grow = (int)fdiv((uint32_t)gc, a.div_GPR);
         const int col4 = (int)(gc - (int64_t)grow * a.GPR);
-        pixoff = s_rowbase[sb][min(grow - g0, g1 - g0)] * a.RS + a.LEFT - a.PW + 4 * col4 * a.SW;
+        pixoff = s_rowbase[sb][min(grow - g0, g1 - g0)] * a.RS + a.POFF + 4 * col4 * a.SW;
     };
 
     f32x4 acc[TM][4];

@@ -179,7 +179,7 @@ __global__ void k_masked_copy(const E *__restrict__ w, const uint8_t *__restrict
 }
 
 struct DescArgs {
-    int shared, n_groups, L, LP, C, KH, KW, CH_STRIDE, RS;
+    int shared, n_groups, L, LP, C, KH, KW, CH_STRIDE, RS, VS, V;
 };
 
 __global__ void k_desc(DescArgs a, const int32_t *__restrict__ indices, int32_t *__restrict__ desc) {
@@ -191,7 +191,7 @@ __global__ void k_desc(DescArgs a, const int32_t *__restrict__ indices, int32_t 
         const int q = a.shared ? tt : indices[(size_t)g * a.L + tt];
         const int c = q / khw, rs = q - c * khw;
         const int r = rs / a.KW, s = rs - r * a.KW;
-        desc[e] = c * a.CH_STRIDE + r * a.RS + s;
+        desc[e] = c * a.CH_STRIDE + (s % a.V) * a.VS + r * a.RS + (s / a.V) * a.V;
     }
 }
 
@@ -377,7 +377,7 @@ bsp_status pack_t(const Plan &p, const E *w, const uint8_t *mask, E *values, int
     }
     // 3. forward layout
     int32_t *desc = (int32_t *)(tiles + p.off_desc);
-    DescArgs da{p.shared, p.n_groups, p.L, p.LP, p.C, p.KH, p.KW, p.CH_STRIDE, p.RS};
+    DescArgs da{p.shared, p.n_groups, p.L, p.LP, p.C, p.KH, p.KW, p.CH_STRIDE, p.RS, p.VS, std::max(p.V, 1)};
     k_desc<<<grid_for((size_t)p.n_groups * p.LP), 256, 0, st>>>(da, indices, desc);
     ATileArgs aa{p.shared, p.n_groups, p.mt_per_group, p.n_mt_pad, p.group_rows, p.S, p.L, p.R, p.C};
     const size_t na = (size_t)p.n_mt_pad * p.S * 512;

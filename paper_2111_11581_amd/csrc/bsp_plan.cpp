@@ -52,6 +52,158 @@ static int max_slots(int TG, int GPR, int Ho, int KH, int SH, int PH) {
     return mx;
 }
 
+// Padding of the m-tile range, dev_tiles layout and the fingerprint the kernels
+// check against the packed header.
+static void finish_layout(Plan *p, int n_mt, int astep) {
+    p->n_mt_pad = p->n_mb * p->MBT;
+    p->n_g_pad = p->shared ? 1 : std::max(p->n_groups, p->n_mb * p->MBG);
+    if (p->shared) p->n_mt_pad = std::max(p->n_mt_pad, n_mt);
+
+    p->off_chunks = kHeaderBytes;
+    p->off_desc = align256(p->off_chunks + (int64_t)16 * p->S);
+    p->off_desc16 = align256(p->off_desc + (int64_t)4 * p->n_groups * p->LP);
+    p->off_a = align256(p->off_desc16 + (int64_t)2 * p->n_g_pad * p->LP);
+    p->tile_bytes = p->off_a + (int64_t)p->n_mt_pad * p->S * astep;
+
+    const int fpv[] = {p->R, p->C, p->bh_eff, p->bw_eff, p->reg, p->rate, p->dt, p->n_groups,
+                       p->mt_per_group, p->LP, p->S, p->CH_STRIDE, p->RS, p->LEFT, p->NSLOT,
+                       p->CC, p->KH, p->KW, p->is_linear, p->SW, p->NSUB, p->SMAX, p->resident,
+                       p->MBT, p->MBG, p->n_mt_pad, p->n_g_pad, p->GE, p->NB, p->pw, p->NGR, p->VS, p->V, 8};
+    p->fingerprint = fnv1a(fpv, (int)(sizeof(fpv) / sizeof(fpv[0])));
+}
+
+// Tiling of a pointwise layer for the pointwise kernel.  The patch row of a channel
+// is the tile's granules (NGR of them, no padding), so a tiling is NSUB, the wave
+// split, the m-block, the weight staging and the channels per chunk.  Scored for the
+// nominal batch with a model of the chip: HBM, L2-to-LDS copies, LDS reads of the
+// gathers, MFMA issue, and the copy latency of each chunk, hidden by the other
+// workgroups of a CU.  Returns false when nothing fits.
+static bool plan_pointwise(Plan *p, int span_req, int n_mt, int mpg, int astep) {
+    const int GE = 16 / p->esize;
+    const int gpg = p->SW == 1 ? GE / 4 : 1;
+    int64_t groups_nom;   // groups of the nominal batch
+    double hbm_bytes;
+    if (p->is_linear) {
+        groups_nom = round_up(div_up(kNominalVectors, 4), gpg);
+        hbm_bytes = ((double)p->Cin + p->R) * kNominalVectors * p->esize;
+    } else if (p->SW == 1) {
+        groups_nom = (int64_t)kNominalImages * round_up(div_up(p->H * p->W, 4), gpg);
+        hbm_bytes = ((double)p->Cin + p->R) * kNominalImages * p->H * p->W * p->esize;
+    } else {
+        groups_nom = (int64_t)kNominalImages * p->Ho * div_up(p->Wo, 4);
+        hbm_bytes = ((double)p->Cin * p->H * p->W / 2 + (double)p->R * p->Ho * p->Wo) * kNominalImages * p->esize;
+    }
+    hbm_bytes += (double)n_mt * p->S * astep;
+    const double t_hbm = hbm_bytes / 5.5e12 * 2.4e9;
+    const double mfma_cyc = p->esize == 4 ? 32.0 : 16.0;   // one step of one m-tile and n-tile
+
+    double best = 1e300;
+    Plan bestp = *p;
+    for (int nsub = 1; nsub <= 4; nsub *= 2) {
+        const int TG = kGroups * nsub;
+        const int ngr = TG / gpg;
+        const int rb = ngr * 16;               // patch bytes per channel
+        const int chs = ngr * GE;              // patch elements per channel
+        const int Q = kWaves / nsub;
+        const double n_pt = std::ceil((double)groups_nom / TG);
+        for (int qmode = 0; qmode <= 1; ++qmode) {
+            if (qmode == 1 && Q == 1) continue;
+            const int KS = qmode ? Q : 1;
+            for (int TM = 1; TM <= 4; TM *= 2) {
+                if (p->esize == 4 && TM > 2) continue;
+                int TPG, MBT, MBG, n_mb;
+                MBT = TM * (qmode == 0 ? Q : 1);
+                if (MBT > 1 && MBT >= 2 * n_mt) continue;   // mostly idle waves
+                if (p->shared) {
+                    TPG = TM;
+                    MBG = 1;
+                } else {
+                    TPG = std::min(TM, mpg);
+                    if (TM % TPG) continue;
+                    if (MBT % mpg != 0 && mpg % MBT != 0) continue;
+                    MBG = std::max(1, MBT / mpg);
+                }
+                n_mb = div_up(n_mt, MBT);
+                const int64_t d_res = align256((int64_t)MBG * p->LP * 2);
+                const int64_t a_all = (int64_t)MBT * p->S * astep;
+                const int occ_v = pw_occ(p->esize, p->SW == 2 ? 2 : 1, TM);   // register limit of the kernel
+                for (int opt = 0; opt < 5; ++opt) {
+                    const int resident = opt == 0;
+                    const int smax = resident ? 0 : (1 << (opt - 1));   // 1, 2, 4, 8
+                    if (!resident && smax > p->S) continue;
+                    const int64_t astage = resident ? 0 : (int64_t)MBT * smax * astep;
+                    const int64_t fixed = d_res + (resident ? align256(a_all) : 0);
+                    for (int nb = 2; nb <= 3; ++nb) {
+                        for (int occ = 1; occ <= occ_v; ++occ) {
+                            const int64_t budget = (160 * 1024) / occ - 1280;   // minus static LDS
+                            const int64_t free_b = budget - fixed - nb * align256(astage) - nb * 256;
+                            if (free_b <= 0) continue;
+                            // patches are whole 1 KB copy slots of four waves (256 granules)
+                            int64_t cc = free_b / (nb * 4096) * kThreads / ngr;
+                            cc = std::min<int64_t>(cc, std::min(p->Cin, kMaxCC));
+                            cc = std::min<int64_t>(cc, 65535 / chs);
+                            if (p->shared && cc < p->Cin) cc = cc / kKS * kKS;
+                            if (cc < span_req || cc < 1) continue;
+                            // whole 1 KB copy slots of four waves
+                            const int64_t lds_patch = div_up64(cc * ngr, kThreads) * 4096;
+                            const int64_t lds_buf = lds_patch + align256(astage);
+                            int64_t total = fixed + nb * lds_buf;
+                            if (KS > 1) total = std::max<int64_t>(total, (int64_t)2 * TM * 4096);
+                            if (total > budget) continue;
+                            double nch = std::ceil((double)p->Cin / cc);
+                            if (!resident) nch = std::max(nch, std::ceil((double)p->S / smax));
+                            // persistent workgroups, as the launcher splits them
+                            double wpm = std::max(1.0, std::ceil(256.0 * occ / n_mb));
+                            if (KS > 1 || wpm > n_pt) wpm = n_pt;
+                            const double tpw = std::ceil(n_pt / wpm);
+                            const double n_wg = std::ceil(n_pt / tpw) * n_mb;
+                            const double tiles = n_pt * n_mb;
+                            // L2 -> LDS copies: patches per tile, weights per workgroup when
+                            // resident (else per tile), offsets per workgroup
+                            const double l2 = tiles * (double)p->Cin * rb + (resident ? n_wg : tiles) * (double)a_all +
+                                              n_wg * MBG * p->LP * 2.0;
+                            const double t_l2 = l2 / (256.0 * 64.0);
+                            const int GW = TM / TPG;
+                            const double stages = (double)p->S / KS * GW * kWaves;   // per tile, all waves
+                            const double t_lds = tiles * stages * (8.0 * 64 * (p->SW == 2 ? 16 : 8) + TPG * 1024.0 + 1024.0) /
+                                                 (256.0 * 128.0);
+                            const double t_mfma = tiles * MBT * nsub * (double)p->S * 4 * mfma_cyc / (4.0 * 256 * 0.75);
+                            // latency chain of one workgroup: nb - 1 chunks in flight, each item at
+                            // least its own multiply; workgroups beyond occ per CU run in rounds
+                            const double rounds = std::ceil(n_wg / (256.0 * occ));
+                            const double item_mfma = TM * std::ceil((double)p->S / nch / KS) * 4 * mfma_cyc;
+                            const double item = std::max(3000.0 / (nb - 1), item_mfma * std::min(occ, 4) / 4.0 + 400.0);
+                            const double t_lat = rounds * (tpw * nch * item + 6000.0);
+                            const double cyc = std::max(std::max(t_hbm, t_l2), std::max(std::max(t_lds, t_mfma), t_lat)) +
+                                               (KS > 1 ? 1500.0 : 0.0);
+                            if (cyc < best * (1 - 1e-9)) {
+                                best = cyc;
+                                Plan q = *p;
+                                q.pw = 1; q.NGR = ngr; q.gpg = gpg; q.occ = occ;
+                                q.NSUB = nsub; q.CH_STRIDE = chs; q.CC = (int)cc;
+                                q.FR = (int)div_up64(cc * ngr, kThreads);
+                                q.qmode = qmode; q.KS = KS; q.TM = TM; q.TPG = TPG;
+                                q.MBT = MBT; q.MBG = MBG; q.n_mb = n_mb;
+                                q.resident = resident; q.SMAX = smax; q.NB = nb;
+                                q.lds_d = (int)d_res;
+                                q.lds_a = resident ? (int)align256(a_all) : 0;
+                                q.lds_patch = (int)lds_patch;
+                                q.lds_astage = (int)align256(astage);
+                                q.lds_buf = (int)lds_buf;
+                                q.lds_total = (int)total;
+                                bestp = q;
+                            }
+                        }
+                    }
+                }
+            }
+        }
+    }
+    if (best >= 1e300) return false;
+    *p = bestp;
+    return true;
+}
+
 bsp_status make_plan(const bsp_scheme *s, const bsp_conv_shape *conv, bsp_dtype wdt,
                      int batch_for_linear, Plan *p) {
     if (!s || !p) return BSP_EINVAL;
@@ -136,13 +288,23 @@ bsp_status make_plan(const bsp_scheme *s, const bsp_conv_shape *conv, bsp_dtype 
     p->GE = 16 / p->esize;
     p->Wop = round_up(p->Wo, 4);
     p->GPR = p->Wop / 4;
-    p->LEFT = round_up(p->PW, p->GE);
-    {
-        const int ng = div_up(p->W, p->GE);
+    // patch rows.  Stride 1: V = min(KW, 4) copies of each staged input row, copy m
+    // starting at input column m - PW; filter column s reads copy s % V at offset
+    // V * (s / V), so every 4-pixel read starts at a multiple of 4 elements.  Other
+    // strides: one copy, LEFT zeros before input column 0.
+    if (p->gather == 1) {
+        p->V = std::min(p->KW, 4);
+        p->LEFT = 0;
+        p->POFF = 0;
+        p->RS = round_up(p->Wop + p->V * ((p->KW - 1) / p->V), p->GE);
+    } else {
+        p->V = 1;
+        p->LEFT = round_up(p->PW, p->GE);
+        p->POFF = p->LEFT - p->PW;
         const int maxpos = p->LEFT - p->PW + (p->Wo - 1) * p->SW + p->KW;   // one past the last used
-        p->RS = round_up(std::max(maxpos, p->LEFT + ng * p->GE), p->GE);
-        p->RG = p->RS / p->GE;
+        p->RS = round_up(std::max(maxpos, p->LEFT + div_up(p->W, p->GE) * p->GE), p->GE);
     }
+    p->RG = p->RS / p->GE;
 
     // Channels one 32-wide step of a kept list can span: a chunk's channel window
     // must hold at least that many.  Identity lists: 32 consecutive columns.  Column
@@ -161,6 +323,15 @@ bsp_status make_plan(const bsp_scheme *s, const bsp_conv_shape *conv, bsp_dtype 
     const int astep = 64 * 8 * p->esize;   // weight bytes of one m-tile and step
     const int n_mt = p->n_groups * p->mt_per_group;
     const int mpg = p->mt_per_group;
+
+    // pointwise layers (1x1 without padding, stride 1 or 2; linear): own kernel
+    if (p->KH == 1 && p->KW == 1 && p->PH == 0 && p->PW == 0 && p->SH == p->SW &&
+        (p->SW == 1 || (p->SW == 2 && p->esize == 2))) {
+        if (plan_pointwise(p, span_req, n_mt, mpg, astep)) {
+            finish_layout(p, n_mt, astep);
+            return BSP_OK;
+        }
+    }
     const double total_groups = (double)nominal_rows * p->GPR;
     // LDS budgets per workgroup: 1, 2, 3 or 4 workgroups per CU (160 KB, minus static tables)
     const int budgets[4] = {140 * 1024, 68 * 1024, 40 * 1024, 28 * 1024};
@@ -168,13 +339,15 @@ bsp_status make_plan(const bsp_scheme *s, const bsp_conv_shape *conv, bsp_dtype 
 
     double best = 1e300;
     Plan bestp = *p;
+    // a second pass admits m-blocks much larger than the layer when nothing else fits
+    for (int relax = 0; relax < 2 && best >= 1e300; ++relax)
     for (int nsub = 1; nsub <= 4; nsub *= 2) {
         const int TG = kGroups * nsub;
         const int trw = rows_spanned(TG, p->GPR);
         if (trw > kMaxTileRows) continue;
         const int nslot = max_slots(TG, p->GPR, p->Ho, p->KH, p->SH, p->PH);
         if (nslot > kMaxSlots) continue;
-        const int chs = nslot * p->RS;                    // patch elements per channel
+        const int chs = p->V * nslot * p->RS;             // patch elements per channel
         const int64_t pch = (int64_t)chs * p->esize;
         const int Q = kWaves / nsub;
         const double n_pt = std::ceil(total_groups / TG);
@@ -191,20 +364,20 @@ bsp_status make_plan(const bsp_scheme *s, const bsp_conv_shape *conv, bsp_dtype 
                 MBT = TM * (qmode == 0 ? Q : 1);
                 if (p->shared) {
                     TPG = TM;
-                    if (MBT > 1 && MBT >= 2 * n_mt) continue;     // mostly idle waves
+                    if (!relax && MBT > 1 && MBT >= 2 * n_mt) continue;     // mostly idle waves
                     MBG = 1;
                     n_mb = div_up(n_mt, MBT);
                 } else {
                     TPG = std::min(TM, mpg);
                     if (TM % TPG) continue;
                     if (MBT % mpg != 0 && mpg % MBT != 0) continue;
-                    if (MBT > 1 && MBT >= 2 * n_mt) continue;
+                    if (!relax && MBT > 1 && MBT >= 2 * n_mt) continue;
                     MBG = std::max(1, MBT / mpg);
                     n_mb = div_up(n_mt, MBT);
                 }
                 const int64_t d_res = align256((int64_t)MBG * p->LP * 2);
                 const int64_t a_all = (int64_t)MBT * p->S * astep;
-                for (int bi = 0; bi < 4; ++bi) {
+                for (int bi = 0; bi < (relax ? 4 : 1); ++bi) {   // measured: one workgroup per CU with large chunks is best
                     const int64_t budget = budgets[bi];
                     for (int opt = 0; opt < 10; ++opt) {
                         const int nb = opt < 5 ? 3 : 2;   // buffers (two when three do not fit)
@@ -215,12 +388,13 @@ bsp_status make_plan(const bsp_scheme *s, const bsp_conv_shape *conv, bsp_dtype 
                         const int64_t fixed = d_res + (resident ? align256(a_all) : 0) + 256;
                         const int64_t free_b = budget - fixed - nb * align256(astage) - nb * 512;
                         if (free_b <= 0) continue;
-                        int64_t cc = free_b / (nb * pch);
+                        // patches are whole 1 KB copy slots of four waves (256 granules)
+                        int64_t cc = free_b / (nb * 4096) * kThreads / ((int64_t)p->V * nslot * p->RG);
                         cc = std::min<int64_t>(cc, std::min(p->Cin, kMaxCC));
                         cc = std::min<int64_t>(cc, 65536 / chs);                       // 16-bit offsets
                         if (cc < span_req || cc < 1) continue;
-                        const int fr = (int)div_up64(cc * nslot * p->RG, kThreads);
-                        const int64_t lds_patch = align256(cc * pch + 128);
+                        const int fr = (int)div_up64(cc * p->V * nslot * p->RG, kThreads);
+                        const int64_t lds_patch = (int64_t)fr * 4096;   // whole 1 KB copy slots of four waves
                         const int64_t lds_buf = lds_patch + align256(astage);
                         int64_t total = fixed + nb * lds_buf;
                         if (qmode == 1) total = std::max<int64_t>(total, (int64_t)2 * TM * 4096);   // partial sums
@@ -238,7 +412,7 @@ bsp_status make_plan(const bsp_scheme *s, const bsp_conv_shape *conv, bsp_dtype 
                         if (!resident) nch = std::max(nch, std::ceil((double)p->S / smax));
                         // bytes into LDS: patch rows (data only) per tile, weights per tile or
                         // once per workgroup when resident, offsets once per workgroup
-                        const double patch_b = (double)p->Cin * nslot * p->W * p->esize * 1.15;
+                        const double patch_b = (double)p->Cin * p->V * nslot * p->RS * p->esize;
                         const double l2_bytes = n_pt * n_mb * patch_b +
                                                 (resident ? n_wg : n_pt * n_mb) * (double)a_all +
                                                 n_wg * MBG * p->LP * 2.0;
@@ -258,12 +432,17 @@ bsp_status make_plan(const bsp_scheme *s, const bsp_conv_shape *conv, bsp_dtype 
                         const double sync = n_pt * n_mb * nch * 900.0 / (256.0 * occ) * (occ > 1 ? 0.6 : 1.0);
                         // per workgroup: header, tables, first fill
                         const double start = std::ceil(n_wg / (256.0 * occ)) * 6000.0;
-                        double cyc = std::max(std::max(t_l2, t_lds), std::max(t_mfma, hbm)) + sync * (nb == 2 ? 1.6 : 1.0) + start;
+                        // copy issue: the waves that compute also issue every copy of a chunk
+                        // (about 100 cycles per 1 KB copy per wave), not hidden by the others
+                        const double issue = std::ceil(n_wg / (256.0 * occ)) * tpw * nch *
+                                             (fr + (resident ? 0.0 : (double)astage / 4096.0)) * 100.0;
+                        double cyc = std::max(std::max(t_l2, t_lds), std::max(t_mfma, hbm)) + sync * (nb == 2 ? 1.6 : 1.0) +
+                                     start + issue;
                         if (qmode == 1) cyc += 1500.0;                                   // partial-sum reduction
                         if (cyc < best * (1 - 1e-9)) {
                             best = cyc;
                             Plan q = *p;
-                            q.NSUB = nsub; q.TRWMAX = trw; q.NSLOT = nslot; q.CH_STRIDE = chs;
+                            q.NSUB = nsub; q.TRWMAX = trw; q.NSLOT = nslot; q.CH_STRIDE = chs; q.VS = nslot * p->RS;
                             q.CC = (int)cc; q.FR = fr;
                             q.qmode = qmode; q.KS = KS; q.TM = TM; q.TPG = TPG;
                             q.MBT = MBT; q.MBG = MBG; q.n_mb = n_mb;
@@ -283,22 +462,7 @@ bsp_status make_plan(const bsp_scheme *s, const bsp_conv_shape *conv, bsp_dtype 
     }
     if (best >= 1e300) return BSP_EUNSUPPORTED;
     *p = bestp;
-    p->n_mt_pad = p->n_mb * p->MBT;
-    p->n_g_pad = p->shared ? 1 : std::max(p->n_groups, p->n_mb * p->MBG);
-    if (p->shared) p->n_mt_pad = std::max(p->n_mt_pad, n_mt);
-
-    // dev_tiles layout
-    p->off_chunks = kHeaderBytes;
-    p->off_desc = align256(p->off_chunks + (int64_t)16 * p->S);
-    p->off_desc16 = align256(p->off_desc + (int64_t)4 * p->n_groups * p->LP);
-    p->off_a = align256(p->off_desc16 + (int64_t)2 * p->n_g_pad * p->LP);
-    p->tile_bytes = p->off_a + (int64_t)p->n_mt_pad * p->S * astep;
-
-    const int fpv[] = {p->R, p->C, p->bh_eff, p->bw_eff, p->reg, p->rate, p->dt, p->n_groups,
-                       p->mt_per_group, p->LP, p->S, p->CH_STRIDE, p->RS, p->LEFT, p->NSLOT,
-                       p->CC, p->KH, p->KW, p->is_linear, p->SW, p->NSUB, p->SMAX, p->resident,
-                       p->MBT, p->MBG, p->n_mt_pad, p->n_g_pad, p->GE, p->NB, 5};
-    p->fingerprint = fnv1a(fpv, (int)(sizeof(fpv) / sizeof(fpv[0])));
+    finish_layout(p, n_mt, astep);
     return BSP_OK;
 }
 

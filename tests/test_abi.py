@@ -133,3 +133,31 @@ def test_fastdiv_and_slot_layout_host(tmp_path):
                     f"-I{ROOT}/paper_2111_11581_amd/csrc", str(src), "-o", str(exe)], check=True)
     r = subprocess.run([str(exe)], capture_output=True, text=True)
     assert r.returncode == 0 and r.stdout.strip() == "ok", r.stdout
+
+
+def test_every_tested_and_benchmarked_layer_gets_a_plan(bsp):
+    """The planner finds a tiling (host only) for every configuration the GPU parity
+    tests and the benchmark workloads run."""
+    from synthetic import workload
+    from tests.test_gpu_parity import CONV_CASES, MATS
+    missing = []
+    for c in CONV_CASES:
+        l = c["layer"]
+        conv = bsp.ConvShape(l.n, l.cin, l.h, l.w, l.kh, l.kw, l.sh, l.sw, l.ph, l.pw)
+        try:
+            bsp.bsp_packed_sizes(l.scheme, conv, bsp.F32 if l.dtype == "f32" else bsp.BF16)
+        except bsp.BspError as e:
+            missing.append((c["name"], str(e)))
+    for name, R, C, bh, bw, reg, rate, dtype, _ in MATS:
+        try:
+            bsp.bsp_packed_sizes(bsp.Scheme(R, C, bh, bw, reg, rate), None, bsp.F32 if dtype == "f32" else bsp.BF16)
+        except bsp.BspError as e:
+            missing.append((name, str(e)))
+    for cfg in (1, 2, 3, 4):
+        for l in workload(cfg):
+            conv = None if l.kind != "conv" else bsp.ConvShape(l.n, l.cin, l.h, l.w, l.kh, l.kw, l.sh, l.sw, l.ph, l.pw)
+            try:
+                bsp.bsp_packed_sizes(l.scheme, conv, bsp.F32 if l.dtype == "f32" else bsp.BF16)
+            except bsp.BspError as e:
+                missing.append((l.name, str(e)))
+    assert not missing, missing
