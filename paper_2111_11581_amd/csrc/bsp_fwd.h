@@ -451,6 +451,8 @@ __device__ __forceinline__ void wait_vm(int n) {
 constexpr int kKindNone = 0, kKindZero = 1, kKindData = 2;
 constexpr int kTableSets = 4;      // tiles in flight: computing, landing, filling, being set up
 constexpr int kMaxMBRows = 256;    // rows of an m-block (bias staged in LDS)
+constexpr int kMaxCHG = 512;       // patch granules per channel (per-tile lookup table)
+constexpr int kNoData = -2147483647 - 1;   // lookup entry of a granule holding no input
 
 template <typename E, int MODE, int TM, int TPG, int KS>
 __global__ __launch_bounds__(kThreads, TM == 1 ? 3 : 2) void k_fwd(ConvArgs a) {
@@ -461,6 +463,7 @@ __global__ __launch_bounds__(kThreads, TM == 1 ? 3 : 2) void k_fwd(ConvArgs a) {
     __shared__ int s_rowbase[kTableSets][kMaxTileRows];
     __shared__ int2 s_slot[kTableSets][kMaxSlots];   // (element offset of the slot's input row or -1, valid width)
     __shared__ float s_bias[kMaxMBRows];
+    __shared__ int2 s_lut[2][kMaxCHG];
 
     // workgroup -> (range of pixel tiles, m-block); ids remapped so that each XCD
     // (hardware places workgroup id on XCD id % 8) gets a contiguous logical range
@@ -540,60 +543,70 @@ __global__ __launch_bounds__(kThreads, TM == 1 ? 3 : 2) void k_fwd(ConvArgs a) {
     // elements before the row start (bits 14-16), kind (bits 17-18).  Decoded from the
     // tile's row table at each use, four granules at a time so the table reads overlap.
     const int total_g = a.CC * a.CHG;                    // granules of a full chunk
-    auto decode = [&](int sb, int j, int &off, int &meta) {
-        const int v = (wave * a.FR + j) * 64 + lane;
-        const int c_rel = (int)fdiv((uint32_t)v, a.div_CHG), rem = v - c_rel * a.CHG;
-        const int s = (int)fdiv((uint32_t)rem, a.div_VSG), rem2 = rem - s * a.VSG;
-        const int slot = (int)fdiv((uint32_t)rem2, a.div_RG), gi = rem2 - slot * a.RG;
-        int kind = kKindNone, tail = 0, head = 0;
-        off = 0;
-        if (v < total_g) {
+    // Per tile, granule r of a channel's patch -> (element offset of its first element in
+    // x for channel 0, or kNoData when it holds only pads / rows outside the image;
+    // elements before the row start | elements past the row end << 3).  Two tables,
+    // by tile parity: the tile being filled and the one being fixed up.
+    auto build_lut = [&](int t) {
+        const int sb = tset(t), ls = t & 1;
+        for (int r = tid; r < a.CHG; r += kThreads) {
+            const int s = (int)fdiv((uint32_t)r, a.div_VSG), rem2 = r - s * a.VSG;
+            const int slot = (int)fdiv((uint32_t)rem2, a.div_RG), gi = rem2 - slot * a.RG;
             const int2 so = s_slot[sb][slot];
             const int col0 = gi * a.GE + (a.V > 1 ? s - a.PW : -a.LEFT);
-            if (so.x < 0 || col0 >= so.y || col0 + a.GE <= 0) {
-                kind = kKindZero;
-            } else {
-                kind = kKindData;
-                tail = max(0, col0 + a.GE - so.y);
-                head = max(0, -col0);
-                off = so.x + c_rel * (int)a.x_cs + col0;
-            }
+            int2 e = make_int2(kNoData, 0);
+            if (so.x >= 0 && col0 < so.y && col0 + a.GE > 0)
+                e = make_int2(so.x + col0, max(0, -col0) | (max(0, col0 + a.GE - so.y) << 3));
+            s_lut[ls][r] = e;
         }
-        meta = c_rel | (tail << 11) | (head << 14) | (kind << 17);
+    };
+    auto decode = [&](int ls, int j, int &off, int &meta) {
+        const int v = (wave * a.FR + j) * 64 + lane;
+        const int c_rel = (int)fdiv((uint32_t)v, a.div_CHG), r = v - c_rel * a.CHG;
+        int kind = kKindNone, pads = 0;
+        off = 0;
+        if (v < total_g) {
+            const int2 e = s_lut[ls][r];
+            kind = e.x == kNoData ? kKindZero : kKindData;
+            off = e.x + c_rel * (int)a.x_cs;
+            pads = e.y;
+        }
+        meta = c_rel | ((pads >> 3) << 11) | ((pads & 7) << 14) | (kind << 17);
     };
     auto kind_of = [&](int m) { return m >> 17; };
     auto crel_of = [&](int m) { return m & 0x7ff; };
     auto tail_of = [&](int m) { return (m >> 11) & 7; };
     auto head_of = [&](int m) { return (m >> 14) & 7; };
-    auto for_granules = [&](int sb, auto act) {
-        for (int j0 = 0; j0 < a.FR; j0 += 4) {
-            int off[4], meta[4];
-#pragma unroll
-            for (int u = 0; u < 4; ++u)
-                if (j0 + u < a.FR) decode(sb, j0 + u, off[u], meta[u]);
-            act(j0, off, meta);
-        }
-    };
     // copies one wave issues for a chunk's patch: every slot
     const int n_patch = a.FR;
 
     // issue the copies of one chunk into buf (patch: data; zero rows, pads, channels past
     // the chunk's count and slots past the patch read zeros; weights when staged);
     // returns the wave's count
-    auto fill = [&](int sb, int4 cd, unsigned char *buf) {
-        const int64_t cbase = (int64_t)cd.z * a.x_cs;
+    // fmask: bit j set when this lane's granule j of the chunk needs fixup() after it
+    // landed (pads inside the granule, or a copy that would read outside x).  Element
+    // offsets fit 32 bits (x holds fewer than 2^31 elements).
+    const uint32_t x_last = (uint32_t)(a.x_total - a.GE);   // last granule start inside x
+    auto fill = [&](int t, int4 cd, unsigned char *buf, uint32_t &fmask) {
+        const int ls = t & 1;
         const uint32_t pbase = ldsa(buf) + (uint32_t)(wave * a.FR * 1024);
-        for_granules(sb, [&](int j0, const int *off, const int *meta) {
+        const int xcs = (int)a.x_cs;
+        fmask = 0;
+        for (int j0 = 0; j0 < a.FR; j0 += 4) {
             const unsigned char *src[4];
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
-                const int64_t e = (int64_t)off[u] + cbase;
-                const bool data = kind_of(meta[u]) == kKindData && crel_of(meta[u]) < cd.w && e >= 0 &&
-                                  e + a.GE <= a.x_total;
-                src[u] = data ? xb + e * (int)sizeof(E) : zero;
+                const int v = (wave * a.FR + j0 + u) * 64 + lane;
+                const int c_rel = (int)fdiv((uint32_t)v, a.div_CHG), r = v - c_rel * a.CHG;
+                const int2 le = s_lut[ls][min(r, a.CHG - 1)];
+                const bool live = v < total_g && le.x != kNoData && c_rel < cd.w;
+                const int e = le.x + (cd.z + c_rel) * xcs;
+                const bool inside = (uint32_t)e <= x_last;
+                src[u] = live && inside ? xb + (int64_t)e * (int)sizeof(E) : zero;
+                if (live && j0 + u < a.FR && (le.y != 0 || !inside)) fmask |= 1u << (j0 + u);
             }
             dma_b4(src[0], src[1], src[2], src[3], pbase + (uint32_t)(j0 * 1024), min(4, a.FR - j0));
-        });
+        }
         int n = n_patch;
         if (!a.resident) {
             // weight copies: per m-tile a contiguous run of ns * AI KB in both places;
@@ -616,28 +629,39 @@ __global__ __launch_bounds__(kThreads, TM == 1 ? 3 : 2) void k_fwd(ConvArgs a) {
         return n;
     };
     // after the copies landed: zero the elements of a granule before the row start and
-    // past the row end, and load granules that would read outside x element by element
-    auto fixup = [&](int sb, int4 cd, unsigned char *buf) {
+    // past the row end, and load granules that would read outside x element by element;
+    // only the granules flagged by fill() are decoded again
+    auto fixup = [&](int t, int4 cd, unsigned char *buf, uint32_t fmask) {
+        const int ls = t & 1;
         const int64_t cbase = (int64_t)cd.z * a.x_cs;
-        for_granules(sb, [&](int j0, const int *off, const int *meta) {
+        while (fmask) {
+            const int j = __builtin_ctz(fmask);
+            fmask &= fmask - 1;
+            int off, meta;
+            decode(ls, j, off, meta);
+            const int tail = tail_of(meta), head = head_of(meta);
+            unsigned char *gp = buf + ((size_t)(wave * a.FR + j) * 64 + lane) * 16;
+            E *dst = (E *)gp;
+            const int64_t e = (int64_t)off + cbase;
+            if (e < 0 || e + a.GE > a.x_total) {
+                const E *src = (const E *)a.x + e;
+                for (int i2 = 0; i2 < a.GE; ++i2)
+                    dst[i2] = (i2 >= head && i2 < a.GE - tail && e + i2 >= 0 && e + i2 < a.x_total) ? src[i2] : (E)0;
+            } else {
+                // keep bytes [head, GE - tail) elements of the 16-byte granule, zero the rest
+                const int lo = head * (int)sizeof(E), hi = 16 - tail * (int)sizeof(E);
+                uint4 v = *(uint4 *)gp;
+                uint32_t w[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                if (j0 + u < a.FR && kind_of(meta[u]) == kKindData && crel_of(meta[u]) < cd.w) {
-                    const int tail = tail_of(meta[u]), head = head_of(meta[u]);
-                    E *dst = (E *)(buf + ((size_t)(wave * a.FR + j0 + u) * 64 + lane) * 16);
-                    const int64_t e = (int64_t)off[u] + cbase;
-                    if (e < 0 || e + a.GE > a.x_total) {
-                        const E *src = (const E *)a.x + e;
-                        for (int i2 = 0; i2 < a.GE; ++i2)
-                            dst[i2] = (i2 >= head && i2 < a.GE - tail && e + i2 >= 0 && e + i2 < a.x_total)
-                                          ? src[i2] : (E)0;
-                    } else if (head | tail) {
-                        for (int i2 = 0; i2 < head; ++i2) dst[i2] = (E)0;
-                        for (int i2 = a.GE - tail; i2 < a.GE; ++i2) dst[i2] = (E)0;
-                    }
+                for (int d = 0; d < 4; ++d) {
+                    uint32_t keep = 0;
+#pragma unroll
+                    for (int b = 0; b < 4; ++b) keep |= (4 * d + b >= lo && 4 * d + b < hi) ? (0xffu << (8 * b)) : 0u;
+                    w[d] &= keep;
                 }
+                *(uint4 *)gp = make_uint4(w[0], w[1], w[2], w[3]);
             }
-        });
+        }
     };
 
     // this lane's pixel group of tile t: patch offset, group index
@@ -777,16 +801,23 @@ __global__ __launch_bounds__(kThreads, TM == 1 ? 3 : 2) void k_fwd(ConvArgs a) {
             s_bias[r] = row < a.R ? a.bias[row] : 0.f;
         }
     __syncthreads();
+    uint32_t fm0 = 0, fm1 = 0;   // fixup masks of the next two items in flight
+    if (nch > 0) {
+        build_lut(item_tile(0));
+        if (NB == 3 && n_items > 1 && item_chunk(1) == 0) build_lut(item_tile(1));
+    }
+    __syncthreads();
     if (nch > 0) {
         dma_run(a.tiles + a.off_desc16 + (size_t)g_first * a.LP * 2, ldsa(D_res), a.MBG * a.LP * 2 / 16);
         if (a.resident)
             dma_run(A_g + (size_t)mt_first * a.S * ASTEP, ldsa(A_res), a.MBT * a.S * ASTEP / 16);
         const int4 cd0 = chunk_at(table, 0);
-        fill(tset(item_tile(0)), cd0, bufp(0));
+        fill(item_tile(0), cd0, bufp(0), fm0);
         int n1 = 0;
-        if (NB == 3 && n_items > 1) n1 = fill(tset(item_tile(1)), chunk_at(table, item_chunk(1)), bufp(1));
+        if (NB == 3 && n_items > 1) n1 = fill(item_tile(1), chunk_at(table, item_chunk(1)), bufp(1), fm1);
         wait_vm(n1);
-        fixup(tset(item_tile(0)), cd0, bufp(0));
+        fixup(item_tile(0), cd0, bufp(0), fm0);
+        fm0 = fm1;
     }
     __syncthreads();
 
@@ -799,15 +830,22 @@ __global__ __launch_bounds__(kThreads, TM == 1 ? 3 : 2) void k_fwd(ConvArgs a) {
         // copies issued after those of item i + 1 (NB == 3: item i + 2's)
         int n2 = 0;
         const int ia = i + NB - 1;
+        if (nch > 0 && ia < n_items && item_chunk(ia) == 0) {   // first copies of a tile
+            build_lut(item_tile(ia));
+            __syncthreads();
+        }
         if (nch > 0 && ia < n_items) {
-            const int nf = fill(tset(item_tile(ia)), chunk_at(table, item_chunk(ia)), bufp(ia));
+            uint32_t fm;
+            const int nf = fill(item_tile(ia), chunk_at(table, item_chunk(ia)), bufp(ia), fm);
+            if (NB == 3) fm1 = fm; else fm0 = fm;
             if (NB == 3) n2 = nf;
         }
         if (nch > 0) compute(chunk_at(table, c), bufp(i), pixoff);
         if (i + NB < n_items && item_chunk(i + NB) == 0) setup_tile(item_tile(i + NB));
         if (nch > 0 && i + 1 < n_items) {
             wait_vm(NB == 3 ? n_st + n2 : 0);
-            fixup(tset(item_tile(i + 1)), chunk_at(table, item_chunk(i + 1)), bufp(i + 1));
+            fixup(item_tile(i + 1), chunk_at(table, item_chunk(i + 1)), bufp(i + 1), fm0);
+            fm0 = fm1;
         }
         __syncthreads();
         // output of a finished tile: its stores overlap the next items

@@ -334,7 +334,8 @@ bsp_status make_plan(const bsp_scheme *s, const bsp_conv_shape *conv, bsp_dtype 
     }
     const double total_groups = (double)nominal_rows * p->GPR;
     // LDS budgets per workgroup: 1, 2, 3 or 4 workgroups per CU (160 KB, minus static tables)
-    const int budgets[4] = {140 * 1024, 68 * 1024, 40 * 1024, 28 * 1024};
+    const int budgets[4] = {160 * 1024 - kLdsStatic, 80 * 1024 - kLdsStatic, 53 * 1024 - kLdsStatic,
+                            40 * 1024 - kLdsStatic};
     const int occs[4] = {1, 2, 3, 4};
 
     double best = 1e300;
@@ -348,6 +349,7 @@ bsp_status make_plan(const bsp_scheme *s, const bsp_conv_shape *conv, bsp_dtype 
         const int nslot = max_slots(TG, p->GPR, p->Ho, p->KH, p->SH, p->PH);
         if (nslot > kMaxSlots) continue;
         const int chs = p->V * nslot * p->RS;             // patch elements per channel
+        if (p->V * nslot * p->RG > 512) continue;         // granules per channel: per-tile lookup table
         const int64_t pch = (int64_t)chs * p->esize;
         const int Q = kWaves / nsub;
         const double n_pt = std::ceil(total_groups / TG);
@@ -393,7 +395,12 @@ bsp_status make_plan(const bsp_scheme *s, const bsp_conv_shape *conv, bsp_dtype 
                         cc = std::min<int64_t>(cc, std::min(p->Cin, kMaxCC));
                         cc = std::min<int64_t>(cc, 65536 / chs);                       // 16-bit offsets
                         if (cc < span_req || cc < 1) continue;
-                        const int fr = (int)div_up64(cc * p->V * nslot * p->RG, kThreads);
+                        int fr = (int)div_up64(cc * p->V * nslot * p->RG, kThreads);
+                        if (fr > 32) {   // copies per wave and chunk: one bit each in the fixup mask
+                            cc = 32 * kThreads / ((int64_t)p->V * nslot * p->RG);
+                            if (cc < span_req || cc < 1) continue;
+                            fr = (int)div_up64(cc * p->V * nslot * p->RG, kThreads);
+                        }
                         const int64_t lds_patch = (int64_t)fr * 4096;   // whole 1 KB copy slots of four waves
                         const int64_t lds_buf = lds_patch + align256(astage);
                         int64_t total = fixed + nb * lds_buf;
