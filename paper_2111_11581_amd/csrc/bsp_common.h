@@ -45,7 +45,7 @@ constexpr int kMaxTileRows = 72;   // output rows one workgroup tile may span
 constexpr int kMaxSlots = 192;     // staged input rows per workgroup tile
 constexpr int kMaxCC = 2047;       // channels of one chunk (11 bits of a granule's decode)
 constexpr int kMaxChunks = 512;    // chunk table entries staged in LDS
-constexpr int kLdsStatic = 20 * 1024;  // static LDS tables of the forward kernel (upper bound)
+constexpr int kLdsStatic = 17 * 1024;  // static LDS tables of the general kernel (16.1 KB) and slack
 constexpr uint32_t kMagic = 0x34505342u;  // "BSP4"
 constexpr int kHeaderBytes = 256;
 constexpr int kZeroOffset = 128;   // 128 zero bytes inside the header: source of padding loads

@@ -18,6 +18,7 @@ namespace fwd {
 fwd_fn pick_b1_k1(int TM, int TPG, int KS);
 fwd_fn pick_b1_k24(int TM, int TPG, int KS);
 fwd_fn pick_b2(int TM, int TPG, int KS);
+fwd_fn pick_b3(int TM, int TPG, int KS);
 fwd_fn pick_b0(int TM, int TPG, int KS);
 fwd_fn pick_f(int mode, int TM, int TPG, int KS);
 
@@ -25,6 +26,7 @@ static fwd_fn pick(int dt, int mode, int TM, int TPG, int KS) {
     if (dt == BSP_F32) return pick_f(mode == 2 ? 0 : mode, TM, TPG, KS);
     if (mode == 1) return KS == 1 ? pick_b1_k1(TM, TPG, KS) : pick_b1_k24(TM, TPG, KS);
     if (mode == 2) return pick_b2(TM, TPG, KS);
+    if (mode == 3) return pick_b3(TM, TPG, KS);
     return pick_b0(TM, TPG, KS);
 }
 

@@ -149,16 +149,19 @@ __device__ __forceinline__ void offsets(uint4 d, int pixoff, int *ad) {
 }
 
 // Gathers, split in two halves so that the LDS reads of the next stage can be in
-// flight while the current stage re-packs and multiplies.  MODE 1: stride 1 (one
-// 8-byte read per kept column, 16 bytes for fp32), MODE 2: stride 2 (16-byte reads,
-// even elements), MODE 0: any stride (one read per element).
+// flight while the current stage re-packs and multiplies.  MODE 1: stride 1, reads
+// start at a multiple of 4 elements (one 8-byte read per kept column, 16 bytes for
+// fp32); MODE 3: stride 1 at any element (the two aligned 8-byte words around the 4
+// elements, joined by a byte shift: misaligned 8-byte LDS reads cost about four
+// aligned ones on gfx950); MODE 2: stride 2 (16-byte reads, even elements); MODE 0:
+// any stride (one read per element).
 template <typename E, int MODE>
 struct Gat;
 
 template <int MODE>
 struct Gat<uint16_t, MODE> {
-    typedef typename std::conditional<MODE == 2, uint4, uint2>::type R1;
-    struct Raw { R1 v[8]; };
+    typedef typename std::conditional<MODE >= 2, uint4, uint2>::type R1;
+    struct Raw { R1 v[8]; uint32_t sh; };
     typedef uint4 AReg;
     static __device__ __forceinline__ void read(Raw &r, const unsigned char *patch_b, uint4 d, int pixoff,
                                                 int SW) {
@@ -171,6 +174,13 @@ struct Gat<uint16_t, MODE> {
                 const uint16_t *p = patch + ad[j];
                 r.v[j].x = (uint32_t)p[0] | ((uint32_t)p[SW] << 16);
                 r.v[j].y = (uint32_t)p[2 * SW] | ((uint32_t)p[3 * SW] << 16);
+            } else if constexpr (MODE == 3) {
+                // the two aligned 8-byte words around the 4 elements; shift kept in sh
+                const int b = ad[j] & ~3;
+                const uint2 lo = *(const uint2 *)(patch + b), hi = *(const uint2 *)(patch + b + 4);
+                r.v[j] = make_uint4(lo.x, lo.y, hi.x, hi.y);
+                if (j == 0) r.sh = 0;
+                r.sh |= (uint32_t)(ad[j] & 3) << (2 * j);
             } else {
                 __builtin_memcpy(&r.v[j], patch + ad[j], sizeof(R1));
             }
@@ -187,6 +197,15 @@ struct Gat<uint16_t, MODE> {
             if constexpr (MODE == 2) {
                 v[j].x = perm(r.v[j].y, r.v[j].x, 0x05040100u);
                 v[j].y = perm(r.v[j].w, r.v[j].z, 0x05040100u);
+            } else if constexpr (MODE == 3) {
+                // elements sh .. sh + 3 of the 8: pick the dword pair, then shift by bytes
+                const uint32_t sh = (r.sh >> (2 * j)) & 3;
+                const uint32_t w0 = sh < 2 ? r.v[j].x : r.v[j].y;
+                const uint32_t w1 = sh < 2 ? r.v[j].y : r.v[j].z;
+                const uint32_t w2 = sh < 2 ? r.v[j].z : r.v[j].w;
+                const uint32_t bs = (sh & 1) * 2;
+                v[j].x = __builtin_amdgcn_alignbyte(w1, w0, bs);
+                v[j].y = __builtin_amdgcn_alignbyte(w2, w1, bs);
             } else {
                 v[j] = r.v[j];
             }
@@ -453,6 +472,8 @@ constexpr int kTableSets = 4;      // tiles in flight: computing, landing, filli
 constexpr int kMaxMBRows = 256;    // rows of an m-block (bias staged in LDS)
 constexpr int kMaxCHG = 512;       // patch granules per channel (per-tile lookup table)
 constexpr int kNoData = -2147483647 - 1;   // lookup entry of a granule holding no input
+static_assert(kTableSets * kMaxTileRows * 4 + kTableSets * kMaxSlots * 8 + kMaxMBRows * 4 + 2 * kMaxCHG * 8 <=
+                  kLdsStatic, "static LDS tables exceed the planner's reserve");
 
 template <typename E, int MODE, int TM, int TPG, int KS>
 __global__ __launch_bounds__(kThreads, TM == 1 ? 3 : 2) void k_fwd(ConvArgs a) {

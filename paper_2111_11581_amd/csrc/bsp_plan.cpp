@@ -272,6 +272,7 @@ bsp_status make_plan(const bsp_scheme *s, const bsp_conv_shape *conv, bsp_dtype 
         if (c.h + 2 * c.pad_h < c.kh || c.w + 2 * c.pad_w < c.kw || p->Ho <= 0 || p->Wo <= 0)
             return BSP_EINVAL;
         if (p->PW > 64) return BSP_EUNSUPPORTED;
+        // gather mode (stride 1 may become 3 below, when the rows are staged once)
         p->gather = p->SW == 1 ? 1 : ((p->SW == 2 && wdt == BSP_BF16) ? 2 : 0);
         nominal_rows = kNominalImages * p->Ho;
     } else {
@@ -292,17 +293,29 @@ bsp_status make_plan(const bsp_scheme *s, const bsp_conv_shape *conv, bsp_dtype 
     // starting at input column m - PW; filter column s reads copy s % V at offset
     // V * (s / V), so every 4-pixel read starts at a multiple of 4 elements.  Other
     // strides: one copy, LEFT zeros before input column 0.
-    if (p->gather == 1) {
-        p->V = std::min(p->KW, 4);
-        p->LEFT = 0;
-        p->POFF = 0;
-        p->RS = round_up(p->Wop + p->V * ((p->KW - 1) / p->V), p->GE);
-    } else {
-        p->V = 1;
-        p->LEFT = round_up(p->PW, p->GE);
-        p->POFF = p->LEFT - p->PW;
-        const int maxpos = p->LEFT - p->PW + (p->Wo - 1) * p->SW + p->KW;   // one past the last used
-        p->RS = round_up(std::max(maxpos, p->LEFT + div_up(p->W, p->GE) * p->GE), p->GE);
+    // Copies cost patch space and copy issue, misaligned reads cost gather time: the
+    // copies are taken when their rows are at most 1.6 times the single copy's (measured
+    // on gfx950: narrow images gain, wide ones lose).
+    {
+        const int left1 = round_up(p->PW, p->GE);
+        const int maxpos = left1 - p->PW + (p->Wo - 1) * p->SW + p->KW;   // one past the last used
+        const int rs1 = round_up(std::max(maxpos, left1 + div_up(p->W, p->GE) * p->GE), p->GE);
+        const int vc = std::min(p->KW, 4);
+        const int rsv = round_up(p->Wop + vc * ((p->KW - 1) / vc), p->GE);
+        if (p->gather == 1 && vc > 1 && 10 * vc * rsv <= 16 * rs1) {
+            p->V = vc;
+            p->LEFT = 0;
+            p->POFF = 0;
+            p->RS = rsv;
+        } else {
+            p->V = 1;
+            p->LEFT = left1;
+            p->POFF = left1 - p->PW;
+            p->RS = rs1;
+            // bf16 reads at any element: aligned words joined by a shift (the pointwise
+            // kernel, planned below, reads aligned groups and ignores the mode)
+            if (p->gather == 1 && p->esize == 2) p->gather = 3;
+        }
     }
     p->RG = p->RS / p->GE;
 
@@ -403,7 +416,7 @@ bsp_status make_plan(const bsp_scheme *s, const bsp_conv_shape *conv, bsp_dtype 
                         }
                         const int64_t lds_patch = (int64_t)fr * 4096;   // whole 1 KB copy slots of four waves
                         const int64_t lds_buf = lds_patch + align256(astage);
-                        int64_t total = fixed + nb * lds_buf;
+                        int64_t total = fixed + nb * lds_buf + (p->gather == 3 ? 256 : 0);   // MODE 3 reads run past the patch
                         if (qmode == 1) total = std::max<int64_t>(total, (int64_t)2 * TM * 4096);   // partial sums
                         if (total > budget) continue;
 
@@ -428,7 +441,7 @@ bsp_status make_plan(const bsp_scheme *s, const bsp_conv_shape *conv, bsp_dtype 
                         const int GW = TM / TPG;
                         const double stages = (double)p->S / KS * GW * kWaves;          // per tile, all waves
                         const double lds_b = n_pt * n_mb * stages *
-                                             (8.0 * 64 * (p->gather == 2 ? 16 : 8) * 1.3 + TPG * 1024.0 + 1024.0);
+                                             (8.0 * 64 * (p->gather >= 2 ? 16 : 8) * 1.3 + TPG * 1024.0 + 1024.0);
                         const double t_lds = lds_b / (256.0 * 100.0);
                         const double mfma = n_pt * n_mb * (double)p->S * (kWaves / KS) * TM * 4 *
                                             (p->esize == 4 ? 32.0 : 16.0) / 4.0;           // per SIMD-cycle

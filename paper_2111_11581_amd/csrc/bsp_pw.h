@@ -101,15 +101,20 @@ __global__ __launch_bounds__(kThreads, pw_occ((int)sizeof(E), MODE, TM)) void k_
     // the chunk and positions past the last group read zeros; a granule that would read
     // past the end of x reads zeros here and is completed by tail()), then (when staged)
     // the chunk's weights.  Returns the number of copies the wave issued.
+    // element offsets fit 32 bits (x holds fewer than 2^31 elements)
+    const uint32_t x_last = (uint32_t)(a.x_total - GE);   // last granule start inside x
     auto fill = [&](int t, int4 cd, unsigned char *buf) {
         int64_t off0 = 0;
         const bool g_ok = granule(t, off0);
         const uint32_t pb = ldsa(buf);
+        const int xcs = (int)a.x_cs;
+        const int ebase = (int)off0 + (cd.z + c_lane) * xcs;   // channel c_lane of the chunk
+        const int cw = g_ok ? cd.w : 0;
         auto src_of = [&](int v) {
             const int c_rel = v * c_slot + c_lane;
-            const int64_t e = off0 + (int64_t)(cd.z + c_rel) * a.x_cs;
-            const bool data = g_ok && c_rel < cd.w && e + GE <= a.x_total;
-            return data ? xb + e * (int64_t)sizeof(E) : zero;
+            const int e = ebase + v * c_slot * xcs;
+            const bool data = c_rel < cw && (uint32_t)e <= x_last;
+            return data ? xb + (int64_t)e * (int)sizeof(E) : zero;
         };
         for (int k = 0; k < a.FR; k += 4) {
             const int v = slot0 + k;
