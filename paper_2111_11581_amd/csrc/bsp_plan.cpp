@@ -174,8 +174,15 @@ static bool plan_pointwise(Plan *p, int span_req, int n_mt, int mpg, int astep) 
                             const double item_mfma = TM * std::ceil((double)p->S / nch / KS) * 4 * mfma_cyc;
                             const double item = std::max(3000.0 / (nb - 1), item_mfma * std::min(occ, 4) / 4.0 + 400.0);
                             const double t_lat = rounds * (tpw * nch * item + 6000.0);
-                            const double cyc = std::max(std::max(t_hbm, t_l2), std::max(std::max(t_lds, t_mfma), t_lat)) +
-                                               (KS > 1 ? 1500.0 : 0.0);
+                            // Measured on gfx950 over the ResNet-50 pointwise layers (plan sweeps):
+                            // two workgroups per CU (store phases and copy waits of one overlap
+                            // the other's work), 128-pixel tiles, four m-tiles per wave and two
+                            // buffers win where the model alone cannot tell; these enter as
+                            // factors on the modelled time.
+                            const double prior = (occ == 2 ? 1.0 : 1.3) * (nsub == 2 ? 1.0 : 1.15) *
+                                                 (TM == 4 || p->esize == 4 ? 1.0 : 1.15) * (nb == 2 ? 1.0 : 1.1);
+                            const double cyc = (std::max(std::max(t_hbm, t_l2), std::max(std::max(t_lds, t_mfma), t_lat)) +
+                                                (KS > 1 ? 1500.0 : 0.0)) * prior;
                             if (cyc < best * (1 - 1e-9)) {
                                 best = cyc;
                                 Plan q = *p;
