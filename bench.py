@@ -29,9 +29,13 @@ sys.path.insert(0, ROOT)
 METRIC = "ms/layer + kept-FLOP TFLOP/s (% MFMA roofline), ResNet-50 layers at 4× pruning"
 PEAK_BF16 = 2516.6e12     # dense MFMA bf16, FLOP/s
 PEAK_HBM = 8.0e12         # bytes/s
-KERNEL_TAG = "bsp::fwd::k_fwd<"
+KERNEL_TAGS = ("bsp::fwd::k_fwd<", "bsp::pw::k_pw<")   # the forward kernels (general, pointwise)
 CALIB_BYTES = 256 << 20   # plain copy kernel (torch.neg on bf16) that calibrates the HBM counters
-COUNTERS_FILE = os.path.join(ROOT, "profiles", "k_conv_resnet50_b64_hbm_counters.txt")
+COUNTERS_FILE = os.path.join(ROOT, "profiles", "forward_resnet50_b64_hbm_counters.txt")
+
+
+def is_forward(name: str) -> bool:
+    return any(t in name for t in KERNEL_TAGS)
 
 
 def source_hash() -> str:
@@ -48,8 +52,8 @@ def source_hash() -> str:
 
 
 def read_counters():
-    """Per-launch HBM bytes of k_conv from the committed counter summary, or None
-    when it is missing or was taken on different kernel sources."""
+    """Per-launch HBM bytes of the forward kernels from the committed counter summary,
+    or None when it is missing or was taken on different kernel sources."""
     if not os.path.exists(COUNTERS_FILE):
         return None
     kv = {}
@@ -127,39 +131,40 @@ def _csv_rows(d: str, suffix: str):
 
 
 def _pmc_per_launch(d: str, counter: str, n_layers: int):
-    """Mean counter value (KiB) per k_conv dispatch of the timed steps (the first,
+    """Mean counter value (KiB) per forward dispatch of the timed steps (the first,
     eager step is skipped) and the value of the calibration copy kernel."""
     rows = [r for r in _csv_rows(d, "counter_collection.csv") if r["Counter_Name"] == counter]
     rows.sort(key=lambda r: int(r["Dispatch_Id"]))
-    conv = [float(r["Counter_Value"]) for r in rows if KERNEL_TAG in r["Kernel_Name"]]
+    conv = [float(r["Counter_Value"]) for r in rows if is_forward(r["Kernel_Name"])]
     calib = [float(r["Counter_Value"]) for r in rows if "neg" in r["Kernel_Name"]]
     if len(conv) <= n_layers or not calib:
-        raise SystemExit("%s: %d k_conv dispatches, %d copy dispatches" % (d, len(conv), len(calib)))
+        raise SystemExit("%s: %d forward dispatches, %d copy dispatches" % (d, len(conv), len(calib)))
     steady = conv[n_layers:]
     return sum(steady) / len(steady), len(steady), max(calib)
 
 
 def summarize(args):
-    """Write the k_conv summary (kernel trace statistics and, when given, the HBM
-    counters scaled by the calibration copy) to the profiles folder."""
+    """Write the forward-kernel summary (kernel trace statistics and, when given, the
+    HBM counters scaled by the calibration copy) to the profiles folder."""
     from synthetic import workload
     n_layers = len(workload(3, batch=args.batch))
     stats = _csv_rows(args.summarize, "kernel_stats.csv")
-    conv = [r for r in stats if KERNEL_TAG in r["Name"]]
+    conv = [r for r in stats if is_forward(r["Name"])]
     calls = sum(int(r["Calls"]) for r in conv)
     total_ns = sum(float(r["TotalDurationNs"]) for r in conv)
-    lines = ["# k_conv on the ResNet-50 v1.5 layer pass (batch 64, bf16, 54 launches per step)", "",
+    lines = ["# Forward kernels (k_fwd: conv1 and the 3x3 layers; k_pw: the 1x1 layers and fc) on the "
+             "ResNet-50 v1.5 layer pass (batch 64, bf16, 54 launches per step)", "",
              "Kernel trace statistics (rocprofv3 --kernel-trace --stats), command:", "",
              "    " + args.trace_cmd, "",
              "| kernel | calls | total us | average us | min us | max us |", "|---|---|---|---|---|---|"]
     for r in sorted(stats, key=lambda r: -float(r["TotalDurationNs"])):
         nm = r["Name"]
-        short = nm.replace("void ", "").replace("bsp::(anonymous namespace)::", "").split("(")[0] \
-            if KERNEL_TAG in nm else nm[:60]
+        short = nm.replace("void ", "").replace("bsp::fwd::", "").replace("bsp::pw::", "").split("(")[0] \
+            if is_forward(nm) else nm[:60]
         lines.append("| %s | %s | %.1f | %.3f | %.3f | %.3f |" % (
             short, r["Calls"], float(r["TotalDurationNs"]) / 1e3, float(r["AverageNs"]) / 1e3,
             float(r["MinNs"]) / 1e3, float(r["MaxNs"]) / 1e3))
-    lines += ["", "k_conv, all instantiations: %d calls, average %.3f us per launch, %.1f us per step of %d launches"
+    lines += ["", "Forward kernels, all instantiations: %d calls, average %.3f us per launch, %.1f us per step of %d launches"
               % (calls, total_ns / calls / 1e3, total_ns / calls * n_layers / 1e3, n_layers), ""]
     kv = {"source_hash": source_hash(), "kernel_avg_us_trace": "%.3f" % (total_ns / calls / 1e3)}
     if args.pmc_fetch and args.pmc_write:
@@ -174,7 +179,7 @@ def summarize(args):
                   "Calibration: a plain copy kernel (torch.neg, %d MiB in, %d MiB out) reads FETCH_SIZE %.0f KiB and "
                   "WRITE_SIZE %.0f KiB, so the scale factors are %.4f (fetch) and %.4f (write)."
                   % (CALIB_BYTES >> 20, CALIB_BYTES >> 20, f_cal, w_cal, f_scale, w_scale), "",
-                  "k_conv per launch (mean over %d / %d dispatches of the timed steps): fetch %.3f MB, write %.3f MB, "
+                  "Forward kernels per launch (mean over %d / %d dispatches of the timed steps): fetch %.3f MB, write %.3f MB, "
                   "traffic %.3f MB" % (nf, nw, fetch / 1e6, write / 1e6, (fetch + write) / 1e6), ""]
         kv.update({"fetch_bytes_per_launch": "%.0f" % fetch, "write_bytes_per_launch": "%.0f" % write,
                    "traffic_bytes_per_launch": "%.0f" % (fetch + write),
@@ -184,7 +189,7 @@ def summarize(args):
         f.write("\n".join(lines))
     if args.pmc_fetch and args.pmc_write:
         with open(COUNTERS_FILE, "w") as f:
-            f.write("# k_conv HBM bytes per launch on the ResNet-50 layer pass; written by bench.py --summarize\n")
+            f.write("# forward-kernel HBM bytes per launch on the ResNet-50 layer pass; written by bench.py --summarize\n")
             f.write("# from the passes listed in %s\n" % os.path.basename(args.out))
             for k, v in kv.items():
                 f.write("%s: %s\n" % (k, v))
@@ -208,7 +213,7 @@ def main():
     ap.add_argument("--trace-cmd", default="")
     ap.add_argument("--fetch-cmd", default="")
     ap.add_argument("--write-cmd", default="")
-    ap.add_argument("--out", default=os.path.join(ROOT, "profiles", "k_conv_resnet50_b64.md"))
+    ap.add_argument("--out", default=os.path.join(ROOT, "profiles", "forward_resnet50_b64.md"))
     args = ap.parse_args()
     if args.summarize:
         summarize(args)
@@ -293,7 +298,7 @@ def main():
         g_layer.append(g)
     torch.cuda.synchronize()
 
-    # plain copy kernel of known size: its HBM counters calibrate the k_conv ones
+    # plain copy kernel of known size: its HBM counters calibrate the forward kernels
     cal_src = torch.zeros(CALIB_BYTES // 2, dtype=torch.bfloat16, device=dev)
     cal_dst = torch.empty_like(cal_src)
     torch.neg(cal_src, out=cal_dst)
@@ -372,7 +377,8 @@ def main():
         "config": {"workload": "ResNet-50 v1.5 conv layers + fc at 224x224, batch %d: 1x1 row 32x32 2x, "
                                "3x3 col 16x32 4x, conv1 and fc dense" % args.batch,
                    "batch": args.batch, "layers": n},
-        "roofline": {"bound": "hbm", "kernel": "k_conv (all tile instantiations, %d launches per step)" % n,
+        "roofline": {"bound": "hbm",
+                     "kernel": "forward kernels k_fwd + k_pw (all instantiations, %d launches per step)" % n,
                      "achieved": round(achieved_gbs, 1), "peak": PEAK_HBM / 1e9, "unit": "GB/s",
                      "frac": round(achieved_gbs * 1e9 / PEAK_HBM, 4),
                      "traffic": None if traffic is None else round(traffic),
