@@ -240,6 +240,14 @@ BSP_HD constexpr int pw_occ(int esize, int mode, int tm) {
     return esize == 4 ? (tm == 1 ? 3 : 2) : (tm == 4 ? 2 : (tm == 2 || mode == 2 ? 3 : 4));
 }
 
+// Workgroups per CU the general kernel's register budget allows (its launch bound):
+// gather mode of the plan (2: stride 2, any element), m-tiles per wave, m-tiles per
+// list.  Stride-2 gathers with four m-tiles of separate lists (four dwords per kept
+// column in flight for each) take one workgroup per CU.
+BSP_HD constexpr int fwd_occ(int gather, int tm, int tpg) {
+    return tm == 1 ? 3 : (gather == 2 && tm == 4 && tpg == 1 ? 1 : 2);
+}
+
 inline int div_up(int a, int b) { return (a + b - 1) / b; }
 inline int64_t div_up64(int64_t a, int64_t b) { return (a + b - 1) / b; }
 inline int kept_count(int extent, int rate) { return (extent + rate - 1) / rate; }

@@ -156,7 +156,7 @@ hipError_t launch_conv(const Plan &p, int n, const void *x, const uint8_t *tiles
     if (n_pt <= 0) return hipSuccess;
     // persistent workgroups: about one wave of workgroups over the chip; each walks a
     // range of pixel tiles of its m-block (one tile when waves split the steps)
-    const int occ = std::max(1, std::min(p.TM == 1 ? 3 : 2, (160 * 1024) / (p.lds_total + kLdsStatic)));
+    const int occ = std::max(1, std::min(fwd_occ(p.gather, p.TM, p.TPG), (160 * 1024) / (p.lds_total + kLdsStatic)));
     int64_t wpm = std::max<int64_t>(1, div_up64((int64_t)256 * occ, p.n_mb));
     if (p.KS > 1 || wpm > n_pt) wpm = n_pt;
     const int64_t tpw = div_up64(n_pt, wpm);

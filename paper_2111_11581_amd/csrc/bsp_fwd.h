@@ -149,18 +149,23 @@ __device__ __forceinline__ void offsets(uint4 d, int pixoff, int *ad) {
 }
 
 // Gathers, split in two halves so that the LDS reads of the next stage can be in
-// flight while the current stage re-packs and multiplies.  MODE 1: stride 1, reads
-// start at a multiple of 4 elements (one 8-byte read per kept column, 16 bytes for
-// fp32); MODE 3: stride 1 at any element (the two aligned 8-byte words around the 4
-// elements, joined by a byte shift: misaligned 8-byte LDS reads cost about four
-// aligned ones on gfx950); MODE 2: stride 2 (16-byte reads, even elements); MODE 0:
-// any stride (one read per element).
+// flight while the current stage re-packs and multiplies.  Every LDS read is aligned
+// to its own size: on gfx950 a misaligned multi-dword LDS read costs about twenty
+// aligned ones.  MODE 1: stride 1, reads start at a multiple of 4 elements (one 8-byte
+// read per kept column, 16 bytes for fp32); MODE 3: stride 1 at any element (the
+// dwords holding the 4 elements, joined by a byte shift of 0 or 2); MODE 2: stride 2,
+// 16-byte reads at a multiple of 8 elements (even elements kept); MODE 4: stride 2 at
+// any element (the 4 dwords holding elements e, e + 2, e + 4, e + 6, halves picked by
+// the parity of e); MODE 0: any stride (one read per element).
 template <typename E, int MODE>
 struct Gat;
 
+struct U3 { uint32_t x, y, z; };
+
 template <int MODE>
 struct Gat<uint16_t, MODE> {
-    typedef typename std::conditional<MODE >= 2, uint4, uint2>::type R1;
+    typedef typename std::conditional<MODE == 2 || MODE == 4, uint4,
+                                      typename std::conditional<MODE == 3, U3, uint2>::type>::type R1;
     struct Raw { R1 v[8]; uint32_t sh; };
     typedef uint4 AReg;
     static __device__ __forceinline__ void read(Raw &r, const unsigned char *patch_b, uint4 d, int pixoff,
@@ -175,12 +180,18 @@ struct Gat<uint16_t, MODE> {
                 r.v[j].x = (uint32_t)p[0] | ((uint32_t)p[SW] << 16);
                 r.v[j].y = (uint32_t)p[2 * SW] | ((uint32_t)p[3 * SW] << 16);
             } else if constexpr (MODE == 3) {
-                // the two aligned 8-byte words around the 4 elements; shift kept in sh
-                const int b = ad[j] & ~3;
-                const uint2 lo = *(const uint2 *)(patch + b), hi = *(const uint2 *)(patch + b + 4);
-                r.v[j] = make_uint4(lo.x, lo.y, hi.x, hi.y);
+                // dwords ad/2 .. ad/2 + 2 (the third is needed when ad is odd); bit 2j + 1
+                // of sh: ad odd, i.e. a byte shift of 2 in bits 1..0 of sh >> 2j
+                const uint32_t *w = (const uint32_t *)patch_b + (ad[j] >> 1);
+                r.v[j] = U3{w[0], w[1], w[2]};
                 if (j == 0) r.sh = 0;
-                r.sh |= (uint32_t)(ad[j] & 3) << (2 * j);
+                r.sh |= (uint32_t)(ad[j] & 1) << (2 * j + 1);
+            } else if constexpr (MODE == 4) {
+                // dwords ad/2 .. ad/2 + 3; bit j of sh: ad odd (elements in the high halves)
+                const uint32_t *w = (const uint32_t *)patch_b + (ad[j] >> 1);
+                r.v[j] = make_uint4(w[0], w[1], w[2], w[3]);
+                if (j == 0) r.sh = 0;
+                r.sh |= (uint32_t)(ad[j] & 1) << j;
             } else {
                 __builtin_memcpy(&r.v[j], patch + ad[j], sizeof(R1));
             }
@@ -197,15 +208,14 @@ struct Gat<uint16_t, MODE> {
             if constexpr (MODE == 2) {
                 v[j].x = perm(r.v[j].y, r.v[j].x, 0x05040100u);
                 v[j].y = perm(r.v[j].w, r.v[j].z, 0x05040100u);
+            } else if constexpr (MODE == 4) {
+                const uint32_t sel = ((r.sh >> j) & 1) ? 0x07060302u : 0x05040100u;
+                v[j].x = perm(r.v[j].y, r.v[j].x, sel);
+                v[j].y = perm(r.v[j].w, r.v[j].z, sel);
             } else if constexpr (MODE == 3) {
-                // elements sh .. sh + 3 of the 8: pick the dword pair, then shift by bytes
-                const uint32_t sh = (r.sh >> (2 * j)) & 3;
-                const uint32_t w0 = sh < 2 ? r.v[j].x : r.v[j].y;
-                const uint32_t w1 = sh < 2 ? r.v[j].y : r.v[j].z;
-                const uint32_t w2 = sh < 2 ? r.v[j].z : r.v[j].w;
-                const uint32_t bs = (sh & 1) * 2;
-                v[j].x = __builtin_amdgcn_alignbyte(w1, w0, bs);
-                v[j].y = __builtin_amdgcn_alignbyte(w2, w1, bs);
+                const uint32_t bs = r.sh >> (2 * j);   // alignbyte uses bits 1..0
+                v[j].x = __builtin_amdgcn_alignbyte(r.v[j].y, r.v[j].x, bs);
+                v[j].y = __builtin_amdgcn_alignbyte(r.v[j].z, r.v[j].y, bs);
             } else {
                 v[j] = r.v[j];
             }
@@ -336,11 +346,12 @@ __device__ __forceinline__ void stage(f32x4 (&acc)[TM][4], const unsigned char *
 //       m-tile t at step k: Ab + t * a_mstr + k * KS * ASTEP
 //   Db: LDS gather offsets (this lane's 8) of the first list group at the first step;
 //       group gw: + gw * d_gstr bytes, step k: + k * KS * 64 bytes
-template <typename E, int MODE, int TM, int TPG, int KS>
+//   hook(): called after each step (other work of the wave, e.g. copy batches)
+template <typename E, int MODE, int TM, int TPG, int KS, typename Hook>
 __device__ __forceinline__ void compute_chunk(f32x4 (&acc)[TM][4], const unsigned char *patch,
                                               const unsigned char *Ab, int a_mstr,
                                               const unsigned char *Db, int d_gstr, int nsteps,
-                                              int pixoff, int SW) {
+                                              int pixoff, int SW, Hook &&hook) {
     typedef Gat<E, MODE> GT;
     constexpr int GW = TM / TPG;
     constexpr bool APF = TPG <= 2;
@@ -379,18 +390,23 @@ __device__ __forceinline__ void compute_chunk(f32x4 (&acc)[TM][4], const unsigne
             if constexpr (GW >= 4) { BSP_STAGE2(2) }
             if constexpr (GW >= 8) { BSP_STAGE2(4) BSP_STAGE2(6) }
 #undef BSP_STAGE2
+            hook();
         }
     } else {
         int k = 0;
         for (; k + 1 < nsteps; k += 2) {
             stage<E, MODE, TM, TPG, 0, APF>(acc, patch, Ab + k * (KS * ASTEP), aptr(k + 1), a_mstr, dptr(k + 2),
                                             pixoff, SW, r0, r1, d1, d0, a0, a1);
+            hook();
             stage<E, MODE, TM, TPG, 0, APF>(acc, patch, Ab + (k + 1) * (KS * ASTEP), aptr(k + 2), a_mstr,
                                             dptr(k + 3), pixoff, SW, r1, r0, d0, d1, a1, a0);
+            hook();
         }
-        if (k < nsteps)
+        if (k < nsteps) {
             stage<E, MODE, TM, TPG, 0, APF>(acc, patch, Ab + k * (KS * ASTEP), aptr(k + 1), a_mstr, dptr(k + 2),
                                             pixoff, SW, r0, r1, d1, d0, a0, a1);
+            hook();
+        }
     }
 }
 
@@ -466,8 +482,6 @@ __device__ __forceinline__ void wait_vm(int n) {
     }
 }
 
-// Granule kinds of the per-thread patch decode.
-constexpr int kKindNone = 0, kKindZero = 1, kKindData = 2;
 constexpr int kTableSets = 4;      // tiles in flight: computing, landing, filling, being set up
 constexpr int kMaxMBRows = 256;    // rows of an m-block (bias staged in LDS)
 constexpr int kMaxCHG = 512;       // patch granules per channel (per-tile lookup table)
@@ -475,8 +489,11 @@ constexpr int kNoData = -2147483647 - 1;   // lookup entry of a granule holding 
 static_assert(kTableSets * kMaxTileRows * 4 + kTableSets * kMaxSlots * 8 + kMaxMBRows * 4 + 2 * kMaxCHG * 8 <=
                   kLdsStatic, "static LDS tables exceed the planner's reserve");
 
+// Granule kinds of the per-thread patch decode.
+constexpr int kKindNone = 0, kKindZero = 1, kKindData = 2;
+
 template <typename E, int MODE, int TM, int TPG, int KS>
-__global__ __launch_bounds__(kThreads, TM == 1 ? 3 : 2) void k_fwd(ConvArgs a) {
+__global__ __launch_bounds__(kThreads, fwd_occ(MODE == 4 ? 2 : MODE, TM, TPG)) void k_fwd(ConvArgs a) {
     constexpr int AB = 8 * (int)sizeof(E);   // weight bytes per lane, one m-tile and step
     constexpr int ASTEP = 64 * AB;           // one m-tile, one step
     constexpr int AI = ASTEP / 1024;         // 1 KB copies per m-tile and step
@@ -558,11 +575,9 @@ __global__ __launch_bounds__(kThreads, TM == 1 ? 3 : 2) void k_fwd(ConvArgs a) {
     // staged input rows: at stride 1 copy m starts at input column m - PW, so the reads
     // of filter column s (copy s % V) start at a multiple of 4 elements; otherwise one
     // copy with LEFT zeros before input column 0.  Wave w issues copy slots
-    // w * FR .. + FR - 1; slot u fills granules 64 u .. + 63, lane l granule 64 u + l.
-    // off: element offset of the granule in x without the chunk's first channel;
-    // meta: channel in the chunk (bits 0-10), elements past the row end (bits 11-13),
-    // elements before the row start (bits 14-16), kind (bits 17-18).  Decoded from the
-    // tile's row table at each use, four granules at a time so the table reads overlap.
+    // w * FR .. + FR - 1; slot u fills granules 64 u .. + 63, lane l granule 64 u + l
+    // (channel v / CHG of the chunk, granule v % CHG of that channel's patch, looked up
+    // in the tile's table below at each use).
     const int total_g = a.CC * a.CHG;                    // granules of a full chunk
     // Per tile, granule r of a channel's patch -> (element offset of its first element in
     // x for channel 0, or kNoData when it holds only pads / rows outside the image;
@@ -594,12 +609,8 @@ __global__ __launch_bounds__(kThreads, TM == 1 ? 3 : 2) void k_fwd(ConvArgs a) {
         }
         meta = c_rel | ((pads >> 3) << 11) | ((pads & 7) << 14) | (kind << 17);
     };
-    auto kind_of = [&](int m) { return m >> 17; };
-    auto crel_of = [&](int m) { return m & 0x7ff; };
     auto tail_of = [&](int m) { return (m >> 11) & 7; };
     auto head_of = [&](int m) { return (m >> 14) & 7; };
-    // copies one wave issues for a chunk's patch: every slot
-    const int n_patch = a.FR;
 
     // issue the copies of one chunk into buf (patch: data; zero rows, pads, channels past
     // the chunk's count and slots past the patch read zeros; weights when staged);
@@ -608,46 +619,86 @@ __global__ __launch_bounds__(kThreads, TM == 1 ? 3 : 2) void k_fwd(ConvArgs a) {
     // landed (pads inside the granule, or a copy that would read outside x).  Element
     // offsets fit 32 bits (x holds fewer than 2^31 elements).
     const uint32_t x_last = (uint32_t)(a.x_total - a.GE);   // last granule start inside x
-    auto fill = [&](int t, int4 cd, unsigned char *buf, uint32_t &fmask) {
-        const int ls = t & 1;
-        const uint32_t pbase = ldsa(buf) + (uint32_t)(wave * a.FR * 1024);
-        const int xcs = (int)a.x_cs;
-        fmask = 0;
-        for (int j0 = 0; j0 < a.FR; j0 += 4) {
-            const unsigned char *src[4];
-#pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                const int v = (wave * a.FR + j0 + u) * 64 + lane;
-                const int c_rel = (int)fdiv((uint32_t)v, a.div_CHG), r = v - c_rel * a.CHG;
-                const int2 le = s_lut[ls][min(r, a.CHG - 1)];
-                const bool live = v < total_g && le.x != kNoData && c_rel < cd.w;
-                const int e = le.x + (cd.z + c_rel) * xcs;
-                const bool inside = (uint32_t)e <= x_last;
-                src[u] = live && inside ? xb + (int64_t)e * (int)sizeof(E) : zero;
-                if (live && j0 + u < a.FR && (le.y != 0 || !inside)) fmask |= 1u << (j0 + u);
-            }
-            dma_b4(src[0], src[1], src[2], src[3], pbase + (uint32_t)(j0 * 1024), min(4, a.FR - j0));
-        }
-        int n = n_patch;
+    // The copies of one chunk go out in batches (four copies per lane) from a small
+    // per-wave state: fill_begin() sets it up, each fill_step() issues one batch, so the
+    // batches can be spread over the multiply of another chunk (a burst of copies from
+    // every CU at once stalls issue until the memory system drains it).
+    int fj = 0, fc = 0, fc_end = 0, fcount = 0, fls = 0, fper_m = 1;
+    int4 fcd = make_int4(0, 0, 0, 0);
+    uint32_t fpbase = 0, fab = 0, fmask_acc = 0;
+    int fFR = 0;   // patch copies of the chunk in progress (0: none)
+    auto fill_begin = [&](int t, int4 cd, unsigned char *buf) {
+        fls = t & 1;
+        fcd = cd;
+        fpbase = ldsa(buf) + (uint32_t)(wave * a.FR * 1024);
+        fj = 0;
+        fFR = a.FR;
+        fmask_acc = 0;
+        fcount = 0;
+        fc = fc_end = 0;
         if (!a.resident) {
             // weight copies: per m-tile a contiguous run of ns * AI KB in both places;
             // wave w takes copies w * naw .. + naw - 1, in batches inside one run
-            const int per_m = (cd.y - cd.x) * AI;
-            const int na = a.MBT * per_m;
+            fper_m = (cd.y - cd.x) * AI;
+            const int na = a.MBT * fper_m;
             const int naw = (na + kWaves - 1) / kWaves;
-            const uint32_t ab = ldsa(buf + a.lds_patch);
-            int c = wave * naw;
-            const int c_end = min(na, c + naw);
-            while (c < c_end) {
-                const int m = c / per_m, r = c - m * per_m;
-                const int nb = min(4, min(c_end - c, per_m - r));
-                const unsigned char *src = A_g + ((size_t)(mt_first + m) * a.S + cd.x) * ASTEP + (size_t)r * 1024 + lane * 16;
-                dma_b4(src, src + 1024, src + 2048, src + 3072, ab + (uint32_t)c * 1024, nb);
-                n += nb;
-                c += nb;
-            }
+            fc = wave * naw;
+            fc_end = min(na, fc + naw);
+            fab = ldsa(buf + a.lds_patch);
         }
-        return n;
+    };
+    auto fill_step = [&]() -> bool {
+        const bool patch = fj < fFR;
+        if (!patch && fc >= fc_end) return false;
+        const unsigned char *src[4];
+        uint32_t dst;
+        int nb;
+        if (patch) {
+            const int xcs = (int)a.x_cs;
+            int2 le[4];
+            int crel[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int v = (wave * a.FR + fj + u) * 64 + lane;
+                crel[u] = (int)fdiv((uint32_t)v, a.div_CHG);
+                const int r = v - crel[u] * a.CHG;
+                le[u] = s_lut[fls][min(r, a.CHG - 1)];
+                if (v >= total_g) crel[u] = fcd.w;   // past the patch: no data
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const bool live = (le[u].x != kNoData) & (crel[u] < fcd.w);
+                const int e = le[u].x + (fcd.z + crel[u]) * xcs;
+                const bool inside = (uint32_t)e <= x_last;
+                src[u] = (live & inside) ? xb + (int64_t)e * (int)sizeof(E) : zero;
+                const uint32_t need = (uint32_t)(live & (fj + u < fFR) & ((le[u].y != 0) | !inside));
+                fmask_acc |= need << (fj + u);
+            }
+            nb = min(4, fFR - fj);
+            dst = fpbase + (uint32_t)(fj * 1024);
+        } else {
+            const int m = fc / fper_m, r = fc - m * fper_m;
+            nb = min(4, min(fc_end - fc, fper_m - r));
+            src[0] = A_g + ((size_t)(mt_first + m) * a.S + fcd.x) * ASTEP + (size_t)r * 1024 + lane * 16;
+            src[1] = src[0] + 1024;
+            src[2] = src[0] + 2048;
+            src[3] = src[0] + 3072;
+            dst = fab + (uint32_t)fc * 1024;
+        }
+        dma_b4(src[0], src[1], src[2], src[3], dst, nb);
+        fcount += nb;
+        fj += patch ? 4 : 0;
+        fc += patch ? 0 : nb;
+        return true;
+    };
+    // all copies of one chunk at once; returns the wave's count
+    auto fill = [&](int t, int4 cd, unsigned char *buf, uint32_t &fmask) {
+        fill_begin(t, cd, buf);
+        while (fill_step()) {
+        }
+        fmask = fmask_acc;
+        fFR = 0;
+        return fcount;
     };
     // after the copies landed: zero the elements of a granule before the row start and
     // past the row end, and load granules that would read outside x element by element;
@@ -786,7 +837,7 @@ __global__ __launch_bounds__(kThreads, TM == 1 ? 3 : 2) void k_fwd(ConvArgs a) {
     };
 
     // compute one chunk from buf for the lane's pixel group at pixoff
-    auto compute = [&](int4 cd, const unsigned char *buf, int pixoff) {
+    auto compute = [&](int4 cd, const unsigned char *buf, int pixoff, auto &&hook) {
         const int s0 = cd.x, s1 = cd.y;
         const int sf = s0 + s_off;
         if (sf >= s1) return;
@@ -804,7 +855,7 @@ __global__ __launch_bounds__(kThreads, TM == 1 ? 3 : 2) void k_fwd(ConvArgs a) {
         const unsigned char *Db = D_res + (gl0 * a.LP + sf * kKS + kg * 8) * 2;
         const int d_gstr = TPG >= a.mt_per_group ? a.LP * 2 : 0;   // next list group of the wave
         compute_chunk<E, MODE, TM, TPG, KS>(acc, buf, Ab + lane * AB, a_mstr, Db, d_gstr,
-                                            (s1 - sf + KS - 1) / KS, pixoff, a.SW);
+                                            (s1 - sf + KS - 1) / KS, pixoff, a.SW, hook);
     };
 
     // ---- work items (tile, chunk): NB buffers, copies NB - 1 items ahead ----
@@ -855,13 +906,21 @@ __global__ __launch_bounds__(kThreads, TM == 1 ? 3 : 2) void k_fwd(ConvArgs a) {
             build_lut(item_tile(ia));
             __syncthreads();
         }
+        // the copies of item ia go out in batches between the steps of item i (two per
+        // step), the rest after it
+        if (nch > 0 && ia < n_items) fill_begin(item_tile(ia), chunk_at(table, item_chunk(ia)), bufp(ia));
+        if (nch > 0) compute(chunk_at(table, c), bufp(i), pixoff, [&] {
+            if (fill_step()) fill_step();
+        });
         if (nch > 0 && ia < n_items) {
-            uint32_t fm;
-            const int nf = fill(item_tile(ia), chunk_at(table, item_chunk(ia)), bufp(ia), fm);
-            if (NB == 3) fm1 = fm; else fm0 = fm;
-            if (NB == 3) n2 = nf;
+            while (fill_step()) {
+            }
+            fFR = 0;
+            const uint32_t fmn = fmask_acc;
+            fm1 = NB == 3 ? fmn : fm1;
+            fm0 = NB == 3 ? fm0 : fmn;
+            n2 = NB == 3 ? fcount : 0;
         }
-        if (nch > 0) compute(chunk_at(table, c), bufp(i), pixoff);
         if (i + NB < n_items && item_chunk(i + NB) == 0) setup_tile(item_tile(i + NB));
         if (nch > 0 && i + 1 < n_items) {
             wait_vm(NB == 3 ? n_st + n2 : 0);

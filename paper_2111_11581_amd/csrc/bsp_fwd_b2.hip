@@ -1,10 +1,10 @@
-// Instantiations of the forward kernel: bf16, stride-2 gathers.
+// Instantiations of the forward kernel: bf16, stride-2 gathers at any element (aligned dword reads).
 #include "bsp_fwd.h"
 
 namespace bsp {
 namespace fwd {
 
-fwd_fn pick_b2(int TM, int TPG, int KS) { return pick_tm<uint16_t, 2, 2 | 4 | 16, 4>(TM, TPG, KS); }
+fwd_fn pick_b2(int TM, int TPG, int KS) { return pick_tm<uint16_t, 4, 2 | 4 | 16, 4>(TM, TPG, KS); }
 
 }  // namespace fwd
 }  // namespace bsp

@@ -356,7 +356,6 @@ bsp_status make_plan(const bsp_scheme *s, const bsp_conv_shape *conv, bsp_dtype 
     // LDS budgets per workgroup: 1, 2, 3 or 4 workgroups per CU (160 KB, minus static tables)
     const int budgets[4] = {160 * 1024 - kLdsStatic, 80 * 1024 - kLdsStatic, 53 * 1024 - kLdsStatic,
                             40 * 1024 - kLdsStatic};
-    const int occs[4] = {1, 2, 3, 4};
 
     double best = 1e300;
     Plan bestp = *p;
@@ -429,7 +428,7 @@ bsp_status make_plan(const bsp_scheme *s, const bsp_conv_shape *conv, bsp_dtype 
 
                         // ---- score (nominal batch), in CU cycles ----
                         // persistent workgroups: occ per CU, each walking tpw pixel tiles
-                        const int occ = std::min(TM == 1 ? 3 : 2, (160 * 1024) / (int)(total + kLdsStatic));
+                        const int occ = std::min(fwd_occ(p->gather, TM, TPG), (160 * 1024) / (int)(total + kLdsStatic));
                         if (occ < 1) continue;
                         double wpm = std::max(1.0, std::ceil(256.0 * occ / n_mb));
                         if (KS > 1 || wpm > n_pt) wpm = n_pt;

@@ -189,7 +189,7 @@ __global__ __launch_bounds__(kThreads, pw_occ((int)sizeof(E), MODE, TM)) void k_
         const unsigned char *Db = D_res + (gl0 * a.LP + sf * kKS + kg * 8) * 2;
         const int d_gstr = TPG >= a.mt_per_group ? a.LP * 2 : 0;
         compute_chunk<E, MODE, TM, TPG, KS>(acc, buf, Ab + lane * AB, a_mstr, Db, d_gstr,
-                                            (s1 - sf + KS - 1) / KS, pixoff, a.SW);
+                                            (s1 - sf + KS - 1) / KS, pixoff, a.SW, [] {});
     };
 
     // bias + ReLU + rounding; each lane stores its group's pixels of its 4 rows per
