@@ -339,6 +339,14 @@ bsp_status make_plan(const bsp_scheme *s, const bsp_conv_shape *conv, bsp_dtype 
         else cols = (int64_t)2 * kKS * p->rate;
         span_req = (int)std::min<int64_t>(p->Cin, cols / khw + 2);
     }
+    // mean channels one step advances (for the chunk count of a channel window)
+    double step_ch;
+    {
+        const int khw = p->KH * p->KW;
+        if (p->shared) step_ch = (double)kKS / khw;
+        else if (p->nbc > 1) step_ch = (double)kKS * p->bw_eff / kept_count(p->bw_eff, p->rate) / khw;
+        else step_ch = (double)kKS * p->rate / khw;
+    }
 
     const int astep = 64 * 8 * p->esize;   // weight bytes of one m-tile and step
     const int n_mt = p->n_groups * p->mt_per_group;
@@ -369,7 +377,6 @@ bsp_status make_plan(const bsp_scheme *s, const bsp_conv_shape *conv, bsp_dtype 
         if (nslot > kMaxSlots) continue;
         const int chs = p->V * nslot * p->RS;             // patch elements per channel
         if (p->V * nslot * p->RG > 512) continue;         // granules per channel: per-tile lookup table
-        const int64_t pch = (int64_t)chs * p->esize;
         const int Q = kWaves / nsub;
         const double n_pt = std::ceil(total_groups / TG);
         for (int qmode = 0; qmode <= 1; ++qmode) {
@@ -434,37 +441,30 @@ bsp_status make_plan(const bsp_scheme *s, const bsp_conv_shape *conv, bsp_dtype 
                         if (KS > 1 || wpm > n_pt) wpm = n_pt;
                         const double tpw = std::ceil(n_pt / wpm);
                         const double n_wg = std::ceil(n_pt / tpw) * n_mb;
-                        double nch = std::ceil((double)p->Cin / cc);
-                        if (!resident) nch = std::max(nch, std::ceil((double)p->S / smax));
-                        // bytes into LDS: patch rows (data only) per tile, weights per tile or
-                        // once per workgroup when resident, offsets once per workgroup
-                        const double patch_b = (double)p->Cin * p->V * nslot * p->RS * p->esize;
-                        const double l2_bytes = n_pt * n_mb * patch_b +
-                                                (resident ? n_wg : n_pt * n_mb) * (double)a_all +
-                                                n_wg * MBG * p->LP * 2.0;
-                        const double t_l2 = l2_bytes / (256.0 * 40.0);
-                        // LDS reads per tile: gathers, weights, offsets of every stage
-                        const int GW = TM / TPG;
-                        const double stages = (double)p->S / KS * GW * kWaves;          // per tile, all waves
-                        const double lds_b = n_pt * n_mb * stages *
-                                             (8.0 * 64 * (p->gather >= 2 ? 16 : 8) * 1.3 + TPG * 1024.0 + 1024.0);
-                        const double t_lds = lds_b / (256.0 * 100.0);
-                        const double mfma = n_pt * n_mb * (double)p->S * (kWaves / KS) * TM * 4 *
-                                            (p->esize == 4 ? 32.0 : 16.0) / 4.0;           // per SIMD-cycle
-                        const double t_mfma = mfma / (256.0 * 0.7);
+                        const double rounds = std::ceil(n_wg / (256.0 * occ));
+                        // steps per chunk: consecutive steps advance step_ch channels each
+                        // (staged weights: at most SMAX); the real count depends on the lists
+                        double spc = std::max(1.0, (cc - 1) / step_ch);
+                        if (!resident) spc = std::min<double>(spc, smax);
+                        const double nch = std::max(1.0, p->S / spc);
+                        // Serial time of one wave per chunk, fitted to measured plans on gfx950
+                        // (ResNet-50 3x3 layers, 4x column pruning): a fixed cost (copy table
+                        // reads, fixups, barrier, pipeline refill), each stage (8 kept columns
+                        // gathered and 4 MFMAs per m-tile list; stride-2 gathers read 4 dwords
+                        // per column), each 1 KB copy (twice when input rows start off 16-byte
+                        // boundaries); three buffers make chunks smaller and cost more per chunk.
+                        const double stages = std::ceil(spc / KS) * (TM / TPG);
+                        const double copies = fr + (resident ? 0.0 : (double)astage / 4096.0);
+                        const bool mis = ((int64_t)p->W * p->esize) % 16 != 0;
+                        double per_chunk = 3000.0 + stages * (p->SW == 2 ? 900.0 : 500.0) + copies * (mis ? 100.0 : 50.0);
+                        if (nb == 3) per_chunk *= 1.2;
+                        if (occ > 1) per_chunk *= 0.8 * occ;                               // workgroups sharing a CU
+                        // per tile: epilogue; per workgroup: header, tables, first fill
+                        double cyc = rounds * (tpw * nch * per_chunk + tpw * 8000.0 + 8000.0);
                         const double hbm = ((double)nominal_rows / p->Ho * p->Cin * p->H * p->W * p->esize +
                                             total_groups * 4 * p->R * 2.0) / 5.5e12 * 2.4e9;
-                        // per chunk: barrier, fill wait and pipeline refill, hidden by occ - 1 others
-                        const double sync = n_pt * n_mb * nch * 900.0 / (256.0 * occ) * (occ > 1 ? 0.6 : 1.0);
-                        // per workgroup: header, tables, first fill
-                        const double start = std::ceil(n_wg / (256.0 * occ)) * 6000.0;
-                        // copy issue: the waves that compute also issue every copy of a chunk
-                        // (about 100 cycles per 1 KB copy per wave), not hidden by the others
-                        const double issue = std::ceil(n_wg / (256.0 * occ)) * tpw * nch *
-                                             (fr + (resident ? 0.0 : (double)astage / 4096.0)) * 100.0;
-                        double cyc = std::max(std::max(t_l2, t_lds), std::max(t_mfma, hbm)) + sync * (nb == 2 ? 1.6 : 1.0) +
-                                     start + issue;
-                        if (qmode == 1) cyc += 1500.0;                                   // partial-sum reduction
+                        cyc = std::max(cyc, hbm);
+                        if (qmode == 1) cyc = cyc * 1.5 + 1500.0;                           // partial-sum reduction
                         if (cyc < best * (1 - 1e-9)) {
                             best = cyc;
                             Plan q = *p;
