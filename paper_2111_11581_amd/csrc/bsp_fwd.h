@@ -11,16 +11,16 @@
 //  * fill: the input rows of the chunk's channels (every staged row is an input row
 //    of the tile, whole width, zero-padded left and right) are copied into LDS with
 //    asynchronous 16-byte direct-to-LDS loads, issued from inline assembly and awaited
-//    explicitly, so that the compute of the previous chunk (other LDS buffer) runs
-//    meanwhile.  Each thread's granules of the patch are decoded once per tile;
+//    explicitly, in batches between the steps of the previous chunk's compute (other
+//    LDS buffer).  Each thread's granules of the patch are decoded once per tile;
 //    padding and out-of-image rows are zeroed once.  When the m-block's weights do not
 //    stay resident in LDS, the chunk's slice of them is copied the same way.
 //  * compute: each wave walks its steps of 32 kept columns.  Lane l owns kept
 //    positions 8*(l/16) .. +7 and the 4 pixels of group l % 16 of its sub-tile: per
-//    kept column one 8-byte LDS read (stride 1; 16 bytes for stride 2) at the
-//    pre-decoded 16-bit offset plus the group's offset, then v_perm re-packs the 8 x 4
-//    values into the B operands of 4 MFMAs.  A list shared by several m-tiles (row
-//    pruning, dense) reuses the gathered operands across them.
+//    kept column aligned LDS reads at the pre-decoded 16-bit offset plus the group's
+//    offset (see Gat below), then v_perm re-packs the 8 x 4 values into the B operands
+//    of 4 MFMAs.  A list shared by several m-tiles (row pruning, dense) reuses the
+//    gathered operands across them.
 //  * when the 4 / NSUB waves of a sub-tile split the steps, they add their partial
 //    sums through LDS at the end;
 //  * epilogue: bias + ReLU + round-to-nearest-even bf16 (or fp32); each lane writes
