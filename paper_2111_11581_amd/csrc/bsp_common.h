@@ -240,13 +240,11 @@ BSP_HD constexpr int pw_occ(int esize, int mode, int tm) {
     return esize == 4 ? (tm == 1 ? 3 : 2) : (tm == 4 ? 2 : (tm == 2 || mode == 2 ? 3 : 4));
 }
 
-// Workgroups per CU the general kernel's register budget allows (its launch bound):
-// gather mode of the plan (2: stride 2, any element), m-tiles per wave, m-tiles per
-// list.  Stride-2 gathers with four m-tiles of separate lists (four dwords per kept
-// column in flight for each) take one workgroup per CU.
-BSP_HD constexpr int fwd_occ(int gather, int tm, int tpg) {
-    return tm == 1 ? 3 : (gather == 2 && tm == 4 && tpg == 1 ? 1 : 2);
-}
+// The general kernel runs workgroups of 8 waves: 4 that multiply and 4 that copy the
+// next chunks into LDS and clear their pads.  Two waves per SIMD leave each wave 256
+// registers: one workgroup per CU (arguments kept for the plan's gather mode and shape).
+constexpr int kFwdThreads = 512;
+BSP_HD constexpr int fwd_occ(int gather, int tm, int tpg) { return (void)gather, (void)tm, (void)tpg, 1; }
 
 inline int div_up(int a, int b) { return (a + b - 1) / b; }
 inline int64_t div_up64(int64_t a, int64_t b) { return (a + b - 1) / b; }

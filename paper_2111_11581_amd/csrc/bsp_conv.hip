@@ -191,7 +191,7 @@ hipError_t launch_conv(const Plan &p, int n, const void *x, const uint8_t *tiles
                                            p.lds_total);
         if (e != hipSuccess) return e;
     }
-    hipLaunchKernelGGL(fn, dim3(grid), dim3(kThreads), (size_t)p.lds_total, st, a);
+    hipLaunchKernelGGL(fn, dim3(grid), dim3(kFwdThreads), (size_t)p.lds_total, st, a);
     return hipGetLastError();
 }
 

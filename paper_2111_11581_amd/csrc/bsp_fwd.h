@@ -493,7 +493,7 @@ static_assert(kTableSets * kMaxTileRows * 4 + kTableSets * kMaxSlots * 8 + kMaxM
 constexpr int kKindNone = 0, kKindZero = 1, kKindData = 2;
 
 template <typename E, int MODE, int TM, int TPG, int KS>
-__global__ __launch_bounds__(kThreads, fwd_occ(MODE == 4 ? 2 : MODE, TM, TPG)) void k_fwd(ConvArgs a) {
+__global__ __launch_bounds__(kFwdThreads, 1) void k_fwd(ConvArgs a) {
     constexpr int AB = 8 * (int)sizeof(E);   // weight bytes per lane, one m-tile and step
     constexpr int ASTEP = 64 * AB;           // one m-tile, one step
     constexpr int AI = ASTEP / 1024;         // 1 KB copies per m-tile and step
@@ -522,8 +522,12 @@ __global__ __launch_bounds__(kThreads, fwd_occ(MODE == 4 ? 2 : MODE, TM, TPG)) v
     const unsigned char *zero = a.tiles + kZeroOffset;
     const unsigned char *xb = (const unsigned char *)a.x;
 
+    // waves 0-3 multiply (and store), waves 4-7 produce: copies, tables, pad fixups
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
+    const bool prod = wave >= kWaves;
+    const int pw = wave - kWaves;             // producer wave 0 .. 3
+    const int ptid = tid - kThreads;          // producer thread 0 .. 255
     const int n16 = lane & 15, kg = lane >> 4;
     const int ps = wave & (a.NSUB - 1), q = wave / a.NSUB;
     const int m_loc0 = KS > 1 ? 0 : q * TM;   // first m-tile of this wave in the m-block
@@ -554,11 +558,11 @@ __global__ __launch_bounds__(kThreads, fwd_occ(MODE == 4 ? 2 : MODE, TM, TPG)) v
         const int img0 = (int)fdiv((uint32_t)g0, a.div_Ho);
         const int kl = (int)fdiv((uint32_t)g1, a.div_Ho) - img0;   // image boundaries crossed
         const int used = (nrows - 1 - kl) * min(a.SH, a.KH) + kl * a.KH + a.KH;
-        if (tid < nrows) {
-            const int g = g0 + tid;
+        if (ptid >= 0 && ptid < nrows) {
+            const int g = g0 + ptid;
             const int img = (int)fdiv((uint32_t)g, a.div_Ho), oh = g - img * a.Ho;
             const int k = img - img0;
-            const int base = (tid - k) * min(a.SH, a.KH) + k * a.KH;
+            const int base = (ptid - k) * min(a.SH, a.KH) + k * a.KH;
             for (int r = 0; r < a.KH; ++r) {
                 const int ih = oh * a.SH - a.PH + r;
                 const bool in = ih >= 0 && ih < a.H;
@@ -566,9 +570,9 @@ __global__ __launch_bounds__(kThreads, fwd_occ(MODE == 4 ? 2 : MODE, TM, TPG)) v
                                                       ih == a.H - 1 ? a.w_last : a.W)
                                           : make_int2(-1, 0);
             }
-            s_rowbase[sb][tid] = base;
+            s_rowbase[sb][ptid] = base;
         }
-        for (int i = used + tid; i < a.NSLOT; i += kThreads) s_slot[sb][i] = make_int2(-1, 0);
+        for (int i = used + ptid; i < a.NSLOT; i += kThreads) s_slot[sb][i] = make_int2(-1, 0);
     };
 
     // ---- patch granules.  A chunk's patch holds, per channel, V copies of the tile's
@@ -585,7 +589,7 @@ __global__ __launch_bounds__(kThreads, fwd_occ(MODE == 4 ? 2 : MODE, TM, TPG)) v
     // by tile parity: the tile being filled and the one being fixed up.
     auto build_lut = [&](int t) {
         const int sb = tset(t), ls = t & 1;
-        for (int r = tid; r < a.CHG; r += kThreads) {
+        for (int r = ptid; r < a.CHG; r += kThreads) {
             const int s = (int)fdiv((uint32_t)r, a.div_VSG), rem2 = r - s * a.VSG;
             const int slot = (int)fdiv((uint32_t)rem2, a.div_RG), gi = rem2 - slot * a.RG;
             const int2 so = s_slot[sb][slot];
@@ -597,7 +601,7 @@ __global__ __launch_bounds__(kThreads, fwd_occ(MODE == 4 ? 2 : MODE, TM, TPG)) v
         }
     };
     auto decode = [&](int ls, int j, int &off, int &meta) {
-        const int v = (wave * a.FR + j) * 64 + lane;
+        const int v = (pw * a.FR + j) * 64 + lane;
         const int c_rel = (int)fdiv((uint32_t)v, a.div_CHG), r = v - c_rel * a.CHG;
         int kind = kKindNone, pads = 0;
         off = 0;
@@ -620,9 +624,7 @@ __global__ __launch_bounds__(kThreads, fwd_occ(MODE == 4 ? 2 : MODE, TM, TPG)) v
     // offsets fit 32 bits (x holds fewer than 2^31 elements).
     const uint32_t x_last = (uint32_t)(a.x_total - a.GE);   // last granule start inside x
     // The copies of one chunk go out in batches (four copies per lane) from a small
-    // per-wave state: fill_begin() sets it up, each fill_step() issues one batch, so the
-    // batches can be spread over the multiply of another chunk (a burst of copies from
-    // every CU at once stalls issue until the memory system drains it).
+    // per-wave state: fill_begin() sets it up, each fill_step() issues one batch.
     int fj = 0, fc = 0, fc_end = 0, fcount = 0, fls = 0, fper_m = 1;
     int4 fcd = make_int4(0, 0, 0, 0);
     uint32_t fpbase = 0, fab = 0, fmask_acc = 0;
@@ -630,7 +632,7 @@ __global__ __launch_bounds__(kThreads, fwd_occ(MODE == 4 ? 2 : MODE, TM, TPG)) v
     auto fill_begin = [&](int t, int4 cd, unsigned char *buf) {
         fls = t & 1;
         fcd = cd;
-        fpbase = ldsa(buf) + (uint32_t)(wave * a.FR * 1024);
+        fpbase = ldsa(buf) + (uint32_t)(pw * a.FR * 1024);
         fj = 0;
         fFR = a.FR;
         fmask_acc = 0;
@@ -642,7 +644,7 @@ __global__ __launch_bounds__(kThreads, fwd_occ(MODE == 4 ? 2 : MODE, TM, TPG)) v
             fper_m = (cd.y - cd.x) * AI;
             const int na = a.MBT * fper_m;
             const int naw = (na + kWaves - 1) / kWaves;
-            fc = wave * naw;
+            fc = pw * naw;
             fc_end = min(na, fc + naw);
             fab = ldsa(buf + a.lds_patch);
         }
@@ -659,7 +661,7 @@ __global__ __launch_bounds__(kThreads, fwd_occ(MODE == 4 ? 2 : MODE, TM, TPG)) v
             int crel[4];
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
-                const int v = (wave * a.FR + fj + u) * 64 + lane;
+                const int v = (pw * a.FR + fj + u) * 64 + lane;
                 crel[u] = (int)fdiv((uint32_t)v, a.div_CHG);
                 const int r = v - crel[u] * a.CHG;
                 le[u] = s_lut[fls][min(r, a.CHG - 1)];
@@ -712,7 +714,7 @@ __global__ __launch_bounds__(kThreads, fwd_occ(MODE == 4 ? 2 : MODE, TM, TPG)) v
             int off, meta;
             decode(ls, j, off, meta);
             const int tail = tail_of(meta), head = head_of(meta);
-            unsigned char *gp = buf + ((size_t)(wave * a.FR + j) * 64 + lane) * 16;
+            unsigned char *gp = buf + ((size_t)(pw * a.FR + j) * 64 + lane) * 16;
             E *dst = (E *)gp;
             const int64_t e = (int64_t)off + cbase;
             if (e < 0 || e + a.GE > a.x_total) {
@@ -837,7 +839,7 @@ __global__ __launch_bounds__(kThreads, fwd_occ(MODE == 4 ? 2 : MODE, TM, TPG)) v
     };
 
     // compute one chunk from buf for the lane's pixel group at pixoff
-    auto compute = [&](int4 cd, const unsigned char *buf, int pixoff, auto &&hook) {
+    auto compute = [&](int4 cd, const unsigned char *buf, int pixoff) {
         const int s0 = cd.x, s1 = cd.y;
         const int sf = s0 + s_off;
         if (sf >= s1) return;
@@ -855,7 +857,7 @@ __global__ __launch_bounds__(kThreads, fwd_occ(MODE == 4 ? 2 : MODE, TM, TPG)) v
         const unsigned char *Db = D_res + (gl0 * a.LP + sf * kKS + kg * 8) * 2;
         const int d_gstr = TPG >= a.mt_per_group ? a.LP * 2 : 0;   // next list group of the wave
         compute_chunk<E, MODE, TM, TPG, KS>(acc, buf, Ab + lane * AB, a_mstr, Db, d_gstr,
-                                            (s1 - sf + KS - 1) / KS, pixoff, a.SW, hook);
+                                            (s1 - sf + KS - 1) / KS, pixoff, a.SW, [] {});
     };
 
     // ---- work items (tile, chunk): NB buffers, copies NB - 1 items ahead ----
@@ -863,26 +865,34 @@ __global__ __launch_bounds__(kThreads, fwd_occ(MODE == 4 ? 2 : MODE, TM, TPG)) v
     const int n_items = (t_end - t_begin) * nchx;
     auto item_tile = [&](int i) { return t_begin + i / nchx; };
     auto item_chunk = [&](int i) { return i - (i / nchx) * nchx; };
-    for (int i = 0; i < NB && i < n_items; ++i)
-        if (i == 0 || item_chunk(i) == 0) setup_tile(item_tile(i));
-    if (a.bias)
+    // Every barrier below is reached by all 8 waves (conditions are uniform over the
+    // workgroup); the roles differ only in the work between barriers.
+    if (prod) {
+        for (int i = 0; i < NB && i < n_items; ++i)
+            if (i == 0 || item_chunk(i) == 0) setup_tile(item_tile(i));
+    } else if (a.bias) {
         for (int r = tid; r < a.MBT * kMT; r += kThreads) {
             const int gm = mt_first + r / kMT;
             const int gidx = gm / a.mt_per_group;
             const int row = gidx * a.group_rows + (gm - gidx * a.mt_per_group) * kMT + r % kMT;
             s_bias[r] = row < a.R ? a.bias[row] : 0.f;
         }
+    }
     __syncthreads();
-    uint32_t fm0 = 0, fm1 = 0;   // fixup masks of the next two items in flight
-    if (nch > 0) {
+    uint32_t fm0 = 0, fm1 = 0;   // fixup masks of the next two items in flight (producers)
+    if (prod && nch > 0) {
         build_lut(item_tile(0));
         if (NB == 3 && n_items > 1 && item_chunk(1) == 0) build_lut(item_tile(1));
     }
     __syncthreads();
-    if (nch > 0) {
-        dma_run(a.tiles + a.off_desc16 + (size_t)g_first * a.LP * 2, ldsa(D_res), a.MBG * a.LP * 2 / 16);
-        if (a.resident)
-            dma_run(A_g + (size_t)mt_first * a.S * ASTEP, ldsa(A_res), a.MBT * a.S * ASTEP / 16);
+    if (prod && nch > 0) {
+        // offsets and resident weights: contiguous runs over the producer waves
+        auto run = [&](const unsigned char *src, uint32_t dst, int n16) {
+            for (int q0 = pw * 64; q0 < n16; q0 += kThreads)
+                if (q0 + lane < n16) dma16(src + (size_t)(q0 + lane) * 16, dst + (uint32_t)q0 * 16);
+        };
+        run(a.tiles + a.off_desc16 + (size_t)g_first * a.LP * 2, ldsa(D_res), a.MBG * a.LP * 2 / 16);
+        if (a.resident) run(A_g + (size_t)mt_first * a.S * ASTEP, ldsa(A_res), a.MBT * a.S * ASTEP / 16);
         const int4 cd0 = chunk_at(table, 0);
         fill(item_tile(0), cd0, bufp(0), fm0);
         int n1 = 0;
@@ -895,44 +905,39 @@ __global__ __launch_bounds__(kThreads, fwd_occ(MODE == 4 ? 2 : MODE, TM, TPG)) v
 
     int pixoff = 0;
     int64_t grp = 0;
-    int n_st = 0;   // stores issued at the end of the previous item (after the copies awaited next)
     for (int i = 0; i < n_items; ++i) {
         const int t = item_tile(i), c = item_chunk(i);
-        if (c == 0) lane_geom(t, pixoff, grp);
-        // copies issued after those of item i + 1 (NB == 3: item i + 2's)
-        int n2 = 0;
-        const int ia = i + NB - 1;
+        if (!prod && c == 0) lane_geom(t, pixoff, grp);
+        const int ia = i + NB - 1;   // item whose copies go out now
         if (nch > 0 && ia < n_items && item_chunk(ia) == 0) {   // first copies of a tile
-            build_lut(item_tile(ia));
+            if (prod) build_lut(item_tile(ia));
             __syncthreads();
         }
-        // the copies of item ia go out in batches between the steps of item i (two per
-        // step), the rest after it
-        if (nch > 0 && ia < n_items) fill_begin(item_tile(ia), chunk_at(table, item_chunk(ia)), bufp(ia));
-        if (nch > 0) compute(chunk_at(table, c), bufp(i), pixoff, [&] {
-            if (fill_step()) fill_step();
-        });
-        if (nch > 0 && ia < n_items) {
-            while (fill_step()) {
+        if (prod) {
+            // copies of item ia (NB - 1 ahead); then item i + 1 landed: wait for every copy
+            // issued before its last one, clear its pads
+            int n2 = 0;
+            if (nch > 0 && ia < n_items) {
+                uint32_t fm;
+                const int nf = fill(item_tile(ia), chunk_at(table, item_chunk(ia)), bufp(ia), fm);
+                fm1 = NB == 3 ? fm : fm1;
+                fm0 = NB == 3 ? fm0 : fm;
+                n2 = NB == 3 ? nf : 0;
             }
-            fFR = 0;
-            const uint32_t fmn = fmask_acc;
-            fm1 = NB == 3 ? fmn : fm1;
-            fm0 = NB == 3 ? fm0 : fmn;
-            n2 = NB == 3 ? fcount : 0;
-        }
-        if (i + NB < n_items && item_chunk(i + NB) == 0) setup_tile(item_tile(i + NB));
-        if (nch > 0 && i + 1 < n_items) {
-            wait_vm(NB == 3 ? n_st + n2 : 0);
-            fixup(item_tile(i + 1), chunk_at(table, item_chunk(i + 1)), bufp(i + 1), fm0);
-            fm0 = fm1;
+            if (i + NB < n_items && item_chunk(i + NB) == 0) setup_tile(item_tile(i + NB));
+            if (nch > 0 && i + 1 < n_items) {
+                wait_vm(n2);
+                fixup(item_tile(i + 1), chunk_at(table, item_chunk(i + 1)), bufp(i + 1), fm0);
+                fm0 = fm1;
+            }
+        } else if (nch > 0) {
+            compute(chunk_at(table, c), bufp(i), pixoff);
         }
         __syncthreads();
         // output of a finished tile: its stores overlap the next items
-        n_st = 0;
         if constexpr (KS == 1) {
-            if (c == nchx - 1) {
-                n_st = epilogue(grp);
+            if (!prod && c == nchx - 1) {
+                epilogue(grp);
                 clear_acc();
             }
         }
@@ -943,14 +948,14 @@ __global__ __launch_bounds__(kThreads, fwd_occ(MODE == 4 ? 2 : MODE, TM, TPG)) v
         f32x4 *red = (f32x4 *)lds;    // [region][TM][4][64 lanes]; the K loop is done with LDS
         const int region = TM * 4 * 64;
         if constexpr (KS == 4) {
-            if (q >= 2) {
+            if (!prod && q >= 2) {
 #pragma unroll
                 for (int t2 = 0; t2 < TM; ++t2)
 #pragma unroll
                     for (int nt = 0; nt < 4; ++nt) red[(q - 2) * region + (t2 * 4 + nt) * 64 + lane] = acc[t2][nt];
             }
             __syncthreads();
-            if (q < 2) {
+            if (!prod && q < 2) {
 #pragma unroll
                 for (int t2 = 0; t2 < TM; ++t2)
 #pragma unroll
@@ -958,14 +963,14 @@ __global__ __launch_bounds__(kThreads, fwd_occ(MODE == 4 ? 2 : MODE, TM, TPG)) v
             }
             __syncthreads();
         }
-        if (q == 1) {
+        if (!prod && q == 1) {
 #pragma unroll
             for (int t2 = 0; t2 < TM; ++t2)
 #pragma unroll
                 for (int nt = 0; nt < 4; ++nt) red[ps * region + (t2 * 4 + nt) * 64 + lane] = acc[t2][nt];
         }
         __syncthreads();
-        if (q != 0) return;
+        if (prod || q != 0) return;
 #pragma unroll
         for (int t2 = 0; t2 < TM; ++t2)
 #pragma unroll
