@@ -1,0 +1,237 @@
+"""Latency model and rule-based block-size selection (Sec. 5.2.1 and 5.2.2).
+
+The latency model is a table of forward latencies measured on this GPU for layer
+settings: layer shape, regularity (row or column), block size (``0`` = the whole
+matrix, i.e. coarse structured pruning) and pruning rate.  It is built once per
+device by timing the library's own forward call (``measure``) and saved as JSON.
+
+The selection rule is host logic over the table (``select_block_size``): the
+latency of each candidate block size is normalised by the layer's dense MACs; a
+candidate is valid when that latency is at most (1 + beta) times the latency of
+structured pruning (whole-matrix blocks) at the same rate and regularity; of the
+valid candidates the smallest block (finest granularity) is selected.  When none
+is valid, structured pruning is returned.
+
+Usage (GPU):
+    python -m paper_2111_11581_amd.latency build --out model.json
+    python -m paper_2111_11581_amd.latency select --model model.json --beta 0.2
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import sys
+from dataclasses import asdict, dataclass
+
+REG_NAMES = {0: "row", 1: "col", 2: "unstructured", 3: "dense"}
+
+
+@dataclass(frozen=True)
+class Setting:
+    """One layer setting of the latency model (a conv; a linear layer is a 1x1 conv
+    over a 1 x batch image with cin = input features)."""
+    cin: int
+    cout: int
+    h: int
+    w: int
+    kh: int
+    kw: int
+    stride: int
+    pad: int
+    batch: int
+    regularity: int   # 0 row, 1 column, 2 unstructured, 3 dense (package constants)
+    bh: int           # block height (0: whole matrix; 1 for unstructured)
+    bw: int           # block width (0: whole matrix; 1 for unstructured)
+    rate: int
+
+    def key(self) -> str:
+        if self.regularity == 3:
+            b = "-"
+        elif self.regularity == 2:
+            b = "1x1"
+        else:
+            b = "whole" if self.bh == 0 and self.bw == 0 else f"{self.bh}x{self.bw}"
+        return (f"{self.kh}x{self.kw}/{self.stride} {self.cin}->{self.cout} {self.h}x{self.w} b{self.batch} "
+                f"{REG_NAMES[self.regularity]} {b} r{self.rate}")
+
+    def layer_key(self) -> str:
+        """The setting without regularity, block and rate: the layer the rule selects for."""
+        return f"{self.kh}x{self.kw}/{self.stride} {self.cin}->{self.cout} {self.h}x{self.w} b{self.batch}"
+
+    @property
+    def ho(self) -> int:
+        return (self.h + 2 * self.pad - self.kh) // self.stride + 1
+
+    @property
+    def wo(self) -> int:
+        return (self.w + 2 * self.pad - self.kw) // self.stride + 1
+
+    def macs(self) -> int:
+        """Dense multiply-accumulates of the layer (the normaliser of Sec. 5.2.2)."""
+        return self.batch * self.cout * self.ho * self.wo * self.cin * self.kh * self.kw
+
+    def area(self) -> int:
+        """Block area in weight elements (whole matrix: rows x cols)."""
+        rows, cols = self.cout, self.cin * self.kh * self.kw
+        return (self.bh or rows) * (self.bw or cols)
+
+
+class LatencyModel:
+    """Measured forward latency (milliseconds) per setting."""
+
+    def __init__(self, entries=None, meta=None):
+        self.ms = {}          # key -> ms
+        self.settings = {}    # key -> Setting
+        self.meta = dict(meta or {})
+        for s, ms in (entries or []):
+            self.add(s, ms)
+
+    def add(self, s: Setting, ms: float):
+        if not (ms > 0 and math.isfinite(ms)):
+            raise ValueError(f"latency of {s.key()} must be a positive number, got {ms}")
+        self.ms[s.key()] = float(ms)
+        self.settings[s.key()] = s
+
+    def latency(self, s: Setting) -> float:
+        return self.ms[s.key()]
+
+    def normalized(self, s: Setting) -> float:
+        """Latency per dense MAC (Sec. 5.2.2)."""
+        return self.ms[s.key()] / s.macs()
+
+    def save(self, path: str):
+        with open(path, "w") as f:
+            json.dump({"meta": self.meta,
+                       "entries": [dict(asdict(self.settings[k]), ms=self.ms[k]) for k in sorted(self.ms)]},
+                      f, indent=1)
+
+    @classmethod
+    def load(cls, path: str) -> "LatencyModel":
+        with open(path) as f:
+            d = json.load(f)
+        m = cls(meta=d.get("meta"))
+        for e in d["entries"]:
+            ms = e.pop("ms")
+            m.add(Setting(**e), ms)
+        return m
+
+
+def select_block_size(model: LatencyModel, layer: Setting, regularity: int, rate: int, beta: float = 0.2):
+    """The smallest block whose normalised latency is within (1 + beta) of structured
+    pruning (whole-matrix blocks) at the same regularity and rate (Sec. 5.2.2).
+
+    ``layer`` gives the layer shape (its regularity, block and rate fields are
+    ignored).  Returns (bh, bw); (0, 0) is structured pruning, also returned when no
+    block size qualifies.  Raises KeyError when the model holds no structured entry
+    for the layer, regularity and rate.
+    """
+    if beta < 0:
+        raise ValueError("beta must be >= 0")
+    lk = layer.layer_key()
+    cands = [s for s in model.settings.values()
+             if s.layer_key() == lk and s.regularity == regularity and s.rate == rate]
+    ref = [s for s in cands if s.bh == 0 and s.bw == 0]
+    if not ref:
+        raise KeyError(f"no structured (whole-matrix) entry for {lk} {REG_NAMES[regularity]} r{rate}")
+    limit = (1.0 + beta) * model.normalized(ref[0])
+    valid = [s for s in cands if not (s.bh == 0 and s.bw == 0) and model.normalized(s) <= limit]
+    if not valid:
+        return (0, 0)
+    best = min(valid, key=lambda s: (s.area(), s.bh, s.bw))
+    return (best.bh, best.bw)
+
+
+# ---- building the model on the GPU ----
+
+def sweep_settings(cin=256, cout=256, h=56, w=56, k=3, batch=64, blocks=(4, 8, 16, 32, 64, 0),
+                   rates=(2, 4, 8, 16), regularities=(0, 1), references=False):
+    """The block-size sweep of one conv layer: square blocks (0 = whole matrix) x
+    regularity x rate (defaults: 3x3 256->256 at 56x56, batch 64).  With
+    ``references``, also unstructured magnitude pruning at each rate and the dense
+    layer (reference points; the selection rule does not use them)."""
+    st = [Setting(cin, cout, h, w, k, k, 1, k // 2, batch, reg, b, b, r)
+          for b in blocks for reg in regularities for r in rates]
+    if references:
+        st += [Setting(cin, cout, h, w, k, k, 1, k // 2, batch, 2, 1, 1, r) for r in rates]
+        st.append(Setting(cin, cout, h, w, k, k, 1, k // 2, batch, 3, 0, 0, 1))
+    return st
+
+
+def measure(settings, reps: int = 10, rounds: int = 3, seed: int = 1234, device=None) -> LatencyModel:
+    """Times the library's forward call for each setting (bf16; a graph of ``reps``
+    back-to-back launches, replayed ``rounds`` times; mean per launch).  Weights and
+    activations are seeded normal draws made on the device: only their shapes matter
+    for the latency."""
+    import torch
+    from . import BF16, ConvShape, Scheme, bsp_version
+    from .layers import PackedLayer
+
+    dev = torch.device(device or "cuda:0")
+    gen = torch.Generator(device=dev)
+    model = LatencyModel(meta={"device": torch.cuda.get_device_name(dev), "library_version": bsp_version(),
+                               "dtype": "bf16", "reps": reps, "rounds": rounds})
+    for s in settings:
+        gen.manual_seed(seed)
+        rows, cols = s.cout, s.cin * s.kh * s.kw
+        wd = (torch.randn(rows, cols, generator=gen, device=dev) * math.sqrt(2.0 / cols)).to(torch.bfloat16)
+        x = torch.randn(s.batch, s.cin, s.h, s.w, generator=gen, device=dev).to(torch.bfloat16)
+        y = torch.empty(s.batch, s.cout, s.ho, s.wo, dtype=torch.bfloat16, device=dev)
+        scheme = Scheme(rows, cols, s.bh, s.bw, s.regularity, s.rate)
+        conv = ConvShape(s.batch, s.cin, s.h, s.w, s.kh, s.kw, s.stride, s.stride, s.pad, s.pad)
+        p = PackedLayer(scheme, BF16, wd, conv=conv)
+        p.conv2d(x, y, s.batch, BF16)
+        torch.cuda.synchronize(dev)
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for _ in range(reps):
+                p.conv2d(x, y, s.batch, BF16)
+        g.replay()
+        torch.cuda.synchronize(dev)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(rounds):
+            g.replay()
+        e1.record()
+        torch.cuda.synchronize(dev)
+        model.add(s, e0.elapsed_time(e1) / (reps * rounds))
+        del g, p
+    return model
+
+
+def _main(argv=None):
+    ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
+    sub = ap.add_subparsers(dest="cmd", required=True)
+    b = sub.add_parser("build", help="measure the block-size sweep of one 3x3 conv on the GPU")
+    b.add_argument("--out", required=True)
+    b.add_argument("--cin", type=int, default=256)
+    b.add_argument("--hw", type=int, default=56)
+    b.add_argument("--batch", type=int, default=64)
+    s = sub.add_parser("select", help="block size per regularity and rate from a saved model")
+    s.add_argument("--model", required=True)
+    s.add_argument("--beta", type=float, default=0.2)
+    a = ap.parse_args(argv)
+    if a.cmd == "build":
+        st = sweep_settings(cin=a.cin, cout=a.cin, h=a.hw, w=a.hw, batch=a.batch, references=True)
+        m = measure(st)
+        m.save(a.out)
+        for k in sorted(m.ms):
+            print(f"{k:56s} {m.ms[k] * 1e3:9.1f} us", flush=True)
+        return 0
+    m = LatencyModel.load(a.model)
+    layers = {x.layer_key(): x for x in m.settings.values()}
+    for lk, layer in sorted(layers.items()):
+        for reg in (0, 1):
+            for rate in sorted({x.rate for x in m.settings.values() if x.layer_key() == lk}):
+                try:
+                    bh, bw = select_block_size(m, layer, reg, rate, a.beta)
+                except KeyError:
+                    continue
+                print(f"{lk} {REG_NAMES[reg]} r{rate}: beta {a.beta:.2f} -> "
+                      f"{'whole matrix' if bh == 0 else f'{bh}x{bw}'}")
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(_main())
