@@ -124,6 +124,10 @@ struct Plan {
     // lists
     int shared;                   // 1 = identity list shared by all m-tiles
     int n_groups, group_rows, mt_per_group;
+    int RK;                       // rows the kernels compute (R, or the kept filters with a row map)
+    int rowmap;                   // 1: row pruning with whole-width blocks (filter pruning): the
+                                  // kernels compute the kept rows only, the epilogue writes row
+                                  // rowmap[i] of the output, a fill writes the pruned rows
     int L, LP, S;                 // kept per list, padded to 32, steps
     // geometry (linear: Cin = C, H = ceil(batch / 64) rows of W = 64 vectors, 1x1)
     int is_linear;
@@ -155,8 +159,9 @@ struct Plan {
     int NGR;                      // 16-byte granules per patch row (one channel of a tile)
     int gpg;                      // 4-pixel groups per granule
     int occ;                      // workgroups per CU the plan is sized for
-    // dev_tiles layout (bytes)
-    int64_t off_chunks, off_desc, off_desc16, off_a, tile_bytes;
+    // dev_tiles layout (bytes); with a row map, off_rowmap holds int32 rowmap[n_mt_pad * 16]
+    // (kept output row of each computed row, 0 past RK) followed by the R - RK pruned rows
+    int64_t off_chunks, off_desc, off_desc16, off_a, off_rowmap, off_pruned, tile_bytes;
     uint64_t fingerprint;
     // canonical sizes (elements)
     int64_t n_values, n_indices, n_rowptr;
@@ -199,6 +204,8 @@ struct ConvArgs {
     int CHG, VSG;                 // granules per channel, per shifted copy
     int V, POFF;                  // copies per staged row, patch offset of output column 0
     FastDiv div_nmb;              // workgroup -> (pixel tile, m-block)
+    const int32_t *rowmap;        // output row of each computed row (row-mapped kernels only)
+    int Rout;                     // output channels (R is the number of computed rows)
 };
 
 // Launch arguments of the pointwise kernel.  Output pixels are numbered in groups
@@ -210,7 +217,7 @@ struct PwArgs {
     const uint8_t *tiles;
     const float *bias;
     int relu, out_bf16;
-    int R;                        // output rows of the GEMM (filters, out features)
+    int R;                        // computed rows of the GEMM (filters, out features)
     int Ho;                       // group rows per image
     int Wo;                       // output pixels per group row
     int GPR;                      // groups per group row
@@ -232,6 +239,7 @@ struct PwArgs {
     FastDiv div_GPR;              // group -> (group row, group in row)
     FastDiv div_Ho;               // group row -> (image, row in image)
     FastDiv div_nmb;              // workgroup -> (pixel tile, m-block)
+    const int32_t *rowmap;        // output row of each computed row (row-mapped kernels only)
 };
 
 // Workgroups per CU the pointwise kernel's register budget allows (its launch

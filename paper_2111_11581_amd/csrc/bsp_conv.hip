@@ -6,31 +6,77 @@
 namespace bsp {
 namespace pw {
 
-pw_fn pick_b1(int TM, int TPG, int KS);
-pw_fn pick_b2(int TM, int TPG, int KS);
-pw_fn pick_f(int TM, int TPG, int KS);
+pw_fn pick_b1(int TM, int TPG, int KS, bool map);
+pw_fn pick_b2(int TM, int TPG, int KS, bool map);
+pw_fn pick_f(int TM, int TPG, int KS, bool map);
 
 }  // namespace pw
 
 namespace fwd {
 
 // instantiation sets, one per translation unit (bsp_fwd_*.hip)
-fwd_fn pick_b1_k1(int TM, int TPG, int KS);
-fwd_fn pick_b1_k24(int TM, int TPG, int KS);
-fwd_fn pick_b2(int TM, int TPG, int KS);
-fwd_fn pick_b3(int TM, int TPG, int KS);
-fwd_fn pick_b0(int TM, int TPG, int KS);
-fwd_fn pick_f(int mode, int TM, int TPG, int KS);
+fwd_fn pick_b1_k1(int TM, int TPG, int KS, bool map);
+fwd_fn pick_b1_k24(int TM, int TPG, int KS, bool map);
+fwd_fn pick_b2(int TM, int TPG, int KS, bool map);
+fwd_fn pick_b3(int TM, int TPG, int KS, bool map);
+fwd_fn pick_b0(int TM, int TPG, int KS, bool map);
+fwd_fn pick_f(int mode, int TM, int TPG, int KS, bool map);
 
-static fwd_fn pick(int dt, int mode, int TM, int TPG, int KS) {
-    if (dt == BSP_F32) return pick_f(mode == 2 ? 0 : mode, TM, TPG, KS);
-    if (mode == 1) return KS == 1 ? pick_b1_k1(TM, TPG, KS) : pick_b1_k24(TM, TPG, KS);
-    if (mode == 2) return pick_b2(TM, TPG, KS);
-    if (mode == 3) return pick_b3(TM, TPG, KS);
-    return pick_b0(TM, TPG, KS);
+static fwd_fn pick(int dt, int mode, int TM, int TPG, int KS, bool map) {
+    if (dt == BSP_F32) return pick_f(mode == 2 ? 0 : mode, TM, TPG, KS, map);
+    if (mode == 1) return KS == 1 ? pick_b1_k1(TM, TPG, KS, map) : pick_b1_k24(TM, TPG, KS, map);
+    if (mode == 2) return pick_b2(TM, TPG, KS, map);
+    if (mode == 3) return pick_b3(TM, TPG, KS, map);
+    return pick_b0(TM, TPG, KS, map);
 }
 
 }  // namespace fwd
+
+// Output rows of the filters that whole-width row pruning removed: every element is
+// the epilogue of a zero sum (bias, ReLU, rounding), as the forward kernels would write
+// it.  A workgroup walks planes (image, pruned row) of `plane` contiguous elements;
+// 16-byte stores where the plane allows them.
+template <typename E>
+__global__ void k_fill_pruned(E *__restrict__ y, const int32_t *__restrict__ pruned, const float *__restrict__ bias,
+                              int relu, int n_pruned, int64_t n_planes, int64_t plane, int64_t img_stride,
+                              int64_t ch_stride) {
+    constexpr int VE = 16 / (int)sizeof(E);
+    for (int64_t pi = blockIdx.x; pi < n_planes; pi += gridDim.x) {
+        const int64_t img = pi / n_pruned;
+        const int o = pruned[pi - img * n_pruned];
+        const float v = fwd::epi(0.f, bias ? bias[o] : 0.f, relu);
+        E ev;
+        if constexpr (sizeof(E) == 2) ev = fwd::f32_to_bf16_rne(v);
+        else ev = v;
+        E *base = y + img * img_stride + (int64_t)o * ch_stride;
+        if (((uintptr_t)base & 15) == 0 && plane % VE == 0) {
+            union { E e[VE]; uint4 u; } w;
+#pragma unroll
+            for (int k = 0; k < VE; ++k) w.e[k] = ev;
+            uint4 *b4 = (uint4 *)base;
+            for (int64_t k = threadIdx.x; k < plane / VE; k += blockDim.x) b4[k] = w.u;
+        } else {
+            for (int64_t k = threadIdx.x; k < plane; k += blockDim.x) base[k] = ev;
+        }
+    }
+}
+
+static hipError_t launch_fill_pruned(const Plan &p, int64_t n_img, int64_t plane, int64_t img_stride,
+                                     int64_t ch_stride, const uint8_t *tiles, const float *bias, int relu,
+                                     int out_bf16, void *y, hipStream_t st) {
+    const int n_pruned = p.R - p.RK;
+    const int64_t n_planes = n_img * n_pruned;
+    if (!p.rowmap || n_planes <= 0 || plane <= 0) return hipSuccess;
+    const int grid = (int)std::min<int64_t>(n_planes, 16384);
+    const int32_t *pr = (const int32_t *)(tiles + p.off_pruned);
+    if (out_bf16)
+        k_fill_pruned<uint16_t><<<grid, 256, 0, st>>>((uint16_t *)y, pr, bias, relu, n_pruned, n_planes, plane,
+                                                      img_stride, ch_stride);
+    else
+        k_fill_pruned<float><<<grid, 256, 0, st>>>((float *)y, pr, bias, relu, n_pruned, n_planes, plane,
+                                                   img_stride, ch_stride);
+    return hipGetLastError();
+}
 
 static int log2_int(int v) {
     int l = 0;
@@ -50,7 +96,8 @@ static hipError_t launch_pw(const Plan &p, int n, const void *x, const uint8_t *
     a.bias = bias;
     a.relu = relu;
     a.out_bf16 = out_bf16;
-    a.R = p.R;
+    a.R = p.RK;
+    a.rowmap = p.rowmap ? (const int32_t *)(tiles + p.off_rowmap) : nullptr;
     a.SW = p.SW;
     int64_t images;
     if (p.is_linear) {
@@ -102,8 +149,9 @@ static hipError_t launch_pw(const Plan &p, int n, const void *x, const uint8_t *
     a.div_Ho = make_fastdiv((uint32_t)a.Ho);
     a.div_nmb = make_fastdiv((uint32_t)p.n_mb);
     pw::pw_fn fn = nullptr;
-    if (p.dt == BSP_F32) fn = p.SW == 1 ? pw::pick_f(p.TM, p.TPG, p.KS) : nullptr;
-    else fn = p.SW == 1 ? pw::pick_b1(p.TM, p.TPG, p.KS) : pw::pick_b2(p.TM, p.TPG, p.KS);
+    const bool map = p.rowmap != 0;
+    if (p.dt == BSP_F32) fn = p.SW == 1 ? pw::pick_f(p.TM, p.TPG, p.KS, map) : nullptr;
+    else fn = p.SW == 1 ? pw::pick_b1(p.TM, p.TPG, p.KS, map) : pw::pick_b2(p.TM, p.TPG, p.KS, map);
     if (!fn) return hipErrorInvalidValue;
     const int grid = (int)(div_up64(gv, 8) * 8);
     if (p.lds_total > 48 * 1024) {
@@ -112,7 +160,9 @@ static hipError_t launch_pw(const Plan &p, int n, const void *x, const uint8_t *
         if (e != hipSuccess) return e;
     }
     hipLaunchKernelGGL(fn, dim3(grid), dim3(kThreads), (size_t)p.lds_total, st, a);
-    return hipGetLastError();
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    return launch_fill_pruned(p, images, a.y_cs, a.y_is, a.y_cs, tiles, bias, relu, out_bf16, y, st);
 }
 
 hipError_t launch_conv(const Plan &p, int n, const void *x, const uint8_t *tiles, const float *bias,
@@ -126,7 +176,8 @@ hipError_t launch_conv(const Plan &p, int n, const void *x, const uint8_t *tiles
     a.bias = bias;
     a.relu = relu;
     a.out_bf16 = out_bf16;
-    a.Cin = p.Cin; a.R = p.R;
+    a.Cin = p.Cin; a.R = p.RK; a.Rout = p.R;
+    a.rowmap = p.rowmap ? (const int32_t *)(tiles + p.off_rowmap) : nullptr;
     a.KH = p.KH; a.KW = p.KW; a.SH = p.SH; a.SW = p.SW; a.PH = p.PH; a.PW = p.PW;
     if (p.is_linear) {
         // batch n vectors of a feature-major [C][n] matrix: rows of 64 vectors
@@ -183,7 +234,7 @@ hipError_t launch_conv(const Plan &p, int n, const void *x, const uint8_t *tiles
     a.div_CHG = make_fastdiv((uint32_t)a.CHG);
     a.div_VSG = make_fastdiv((uint32_t)a.VSG);
     a.div_nmb = make_fastdiv((uint32_t)p.n_mb);
-    fwd::fwd_fn fn = fwd::pick(p.dt, p.gather, p.TM, p.TPG, p.KS);
+    fwd::fwd_fn fn = fwd::pick(p.dt, p.gather, p.TM, p.TPG, p.KS, p.rowmap != 0);
     if (!fn) return hipErrorInvalidValue;
     const int grid = (int)(div_up64(gv, 8) * 8);
     if (p.lds_total > 48 * 1024) {
@@ -192,7 +243,11 @@ hipError_t launch_conv(const Plan &p, int n, const void *x, const uint8_t *tiles
         if (e != hipSuccess) return e;
     }
     hipLaunchKernelGGL(fn, dim3(grid), dim3(kFwdThreads), (size_t)p.lds_total, st, a);
-    return hipGetLastError();
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    // images of the output: conv NCHW planes of Ho * Wo; linear one [R][n] matrix
+    return launch_fill_pruned(p, a.N, p.is_linear ? n : a.y_cs, (int64_t)p.R * a.y_cs, a.y_cs, tiles, bias,
+                              relu, out_bf16, y, st);
 }
 
 }  // namespace bsp

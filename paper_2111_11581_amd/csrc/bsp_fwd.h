@@ -492,7 +492,7 @@ static_assert(kTableSets * kMaxTileRows * 4 + kTableSets * kMaxSlots * 8 + kMaxM
 // Granule kinds of the per-thread patch decode.
 constexpr int kKindNone = 0, kKindZero = 1, kKindData = 2;
 
-template <typename E, int MODE, int TM, int TPG, int KS>
+template <typename E, int MODE, int TM, int TPG, int KS, bool MAP = false>
 __global__ __launch_bounds__(kFwdThreads, 1) void k_fwd(ConvArgs a) {
     constexpr int AB = 8 * (int)sizeof(E);   // weight bytes per lane, one m-tile and step
     constexpr int ASTEP = 64 * AB;           // one m-tile, one step
@@ -774,6 +774,19 @@ __global__ __launch_bounds__(kFwdThreads, 1) void k_fwd(ConvArgs a) {
         const int nvalid = pix_ok ? max(0, min(4, lim - ow)) : 0;
         const float qnan = __builtin_nanf("");
         const bool plain = ok && !a.bias && !a.relu;
+        // row map (kept filter of each computed row): loaded, and waited for, before the
+        // first store, since the kernel counts its outstanding stores by hand
+        int omap[TM][4] = {};
+        if constexpr (MAP) {
+#pragma unroll
+            for (int t = 0; t < TM; ++t) {
+                const int gm = mt_first + m_loc0 + t;
+                const int mt_in = gm - (gm / a.mt_per_group) * a.mt_per_group;
+#pragma unroll
+                for (int i = 0; i < 4; ++i) omap[t][i] = a.rowmap[mt_in * kMT + 4 * kg + i];
+            }
+            wait_vm_all();
+        }
         int n = 0;
 #pragma unroll
         for (int t = 0; t < TM; ++t) {
@@ -784,6 +797,7 @@ __global__ __launch_bounds__(kFwdThreads, 1) void k_fwd(ConvArgs a) {
                 const int rig = mt_in * kMT + 4 * kg + i;              // row inside the list group
                 const int row = gidx * a.group_rows + rig;
                 const bool row_ok = rig < a.group_rows && row < a.R;
+                const int orow = MAP ? omap[t][i] : row;
                 float o[4];
                 if (plain) {
 #pragma unroll
@@ -793,7 +807,7 @@ __global__ __launch_bounds__(kFwdThreads, 1) void k_fwd(ConvArgs a) {
 #pragma unroll
                     for (int nt = 0; nt < 4; ++nt) o[nt] = ok ? epi(acc[t][nt][i], bv, a.relu) : qnan;
                 }
-                const size_t yo = ((size_t)img * a.R + (row_ok ? row : 0)) * a.y_cs + (size_t)oh * a.Wo + ow;
+                const size_t yo = ((size_t)img * a.Rout + (row_ok ? orow : 0)) * a.y_cs + (size_t)oh * a.Wo + ow;
                 const uint64_t full = ballot(row_ok && nvalid == 4);
                 const uint64_t part = ballot(row_ok && nvalid > 0 && nvalid < 4);
                 if (a.out_bf16) {
@@ -875,7 +889,7 @@ __global__ __launch_bounds__(kFwdThreads, 1) void k_fwd(ConvArgs a) {
             const int gm = mt_first + r / kMT;
             const int gidx = gm / a.mt_per_group;
             const int row = gidx * a.group_rows + (gm - gidx * a.mt_per_group) * kMT + r % kMT;
-            s_bias[r] = row < a.R ? a.bias[row] : 0.f;
+            s_bias[r] = row < a.R ? a.bias[MAP ? a.rowmap[row] : row] : 0.f;
         }
     }
     __syncthreads();
@@ -982,18 +996,29 @@ __global__ __launch_bounds__(kFwdThreads, 1) void k_fwd(ConvArgs a) {
 typedef void (*fwd_fn)(ConvArgs);
 
 // Instantiation choice for one element type and gather mode; KSM is the set of step
-// splits (bit KS) instantiated in the including translation unit.
-template <typename E, int MODE, int TM, int TPG, int KSM>
+// splits (bit KS) instantiated in the including translation unit.  MAP: the layer
+// computes kept filters only and writes them through the row map.
+template <typename E, int MODE, int TM, int TPG, int KSM, bool MAP = false>
 fwd_fn pick_ks(int KS) {
-    if constexpr ((KSM & 2) != 0) if (KS == 1) return k_fwd<E, MODE, TM, TPG, 1>;
-    if constexpr ((KSM & 4) != 0) if (KS == 2) return k_fwd<E, MODE, TM, TPG, 2>;
-    if constexpr ((KSM & 16) != 0) if (KS == 4) return k_fwd<E, MODE, TM, TPG, 4>;
+    if constexpr ((KSM & 2) != 0) if (KS == 1) return k_fwd<E, MODE, TM, TPG, 1, MAP>;
+    if constexpr ((KSM & 4) != 0) if (KS == 2) return k_fwd<E, MODE, TM, TPG, 2, MAP>;
+    if constexpr ((KSM & 16) != 0) if (KS == 4) return k_fwd<E, MODE, TM, TPG, 4, MAP>;
     return nullptr;
 }
 
-// TMMAX: most m-tiles per wave instantiated (register budget of the gather mode)
+// TMMAX: most m-tiles per wave instantiated (register budget of the gather mode).
+// Row-mapped layers share one list over all m-tiles, so only TPG == TM exists for them.
 template <typename E, int MODE, int KSM, int TMMAX>
-fwd_fn pick_tm(int TM, int TPG, int KS) {
+fwd_fn pick_tm(int TM, int TPG, int KS, bool map) {
+    if (map) {
+        if (TPG != TM) return nullptr;
+        switch (TM) {
+            case 1: return pick_ks<E, MODE, 1, 1, KSM, true>(KS);
+            case 2: if constexpr (TMMAX >= 2) return pick_ks<E, MODE, 2, 2, KSM, true>(KS); return nullptr;
+            case 4: if constexpr (TMMAX >= 4) return pick_ks<E, MODE, 4, 4, KSM, true>(KS); return nullptr;
+            default: return nullptr;
+        }
+    }
     switch (TM * 16 + TPG) {
         case 0x11: return pick_ks<E, MODE, 1, 1, KSM>(KS);
         case 0x21: if constexpr (TMMAX >= 2) return pick_ks<E, MODE, 2, 1, KSM>(KS); return nullptr;

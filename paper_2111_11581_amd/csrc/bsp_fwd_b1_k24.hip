@@ -4,7 +4,7 @@
 namespace bsp {
 namespace fwd {
 
-fwd_fn pick_b1_k24(int TM, int TPG, int KS) { return pick_tm<uint16_t, 1, 4 | 16, 4>(TM, TPG, KS); }
+fwd_fn pick_b1_k24(int TM, int TPG, int KS, bool map) { return pick_tm<uint16_t, 1, 4 | 16, 4>(TM, TPG, KS, map); }
 
 }  // namespace fwd
 }  // namespace bsp

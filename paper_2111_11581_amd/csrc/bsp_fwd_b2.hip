@@ -4,7 +4,7 @@
 namespace bsp {
 namespace fwd {
 
-fwd_fn pick_b2(int TM, int TPG, int KS) { return pick_tm<uint16_t, 4, 2 | 4 | 16, 4>(TM, TPG, KS); }
+fwd_fn pick_b2(int TM, int TPG, int KS, bool map) { return pick_tm<uint16_t, 4, 2 | 4 | 16, 4>(TM, TPG, KS, map); }
 
 }  // namespace fwd
 }  // namespace bsp

@@ -4,8 +4,8 @@
 namespace bsp {
 namespace fwd {
 
-fwd_fn pick_f(int mode, int TM, int TPG, int KS) {
-    return mode == 1 ? pick_tm<float, 1, 2, 2>(TM, TPG, KS) : pick_tm<float, 0, 2, 2>(TM, TPG, KS);
+fwd_fn pick_f(int mode, int TM, int TPG, int KS, bool map) {
+    return mode == 1 ? pick_tm<float, 1, 2, 2>(TM, TPG, KS, map) : pick_tm<float, 0, 2, 2>(TM, TPG, KS, map);
 }
 
 }  // namespace fwd

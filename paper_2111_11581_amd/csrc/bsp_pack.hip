@@ -197,6 +197,7 @@ __global__ void k_desc(DescArgs a, const int32_t *__restrict__ indices, int32_t 
 
 struct ATileArgs {
     int shared, n_groups, mt_per_group, n_mt_pad, group_rows, S, L, R, C;
+    int rowmap;   // 1: computed row i is weight row indices[i] (kept filters, ascending)
 };
 
 template <typename E>
@@ -218,10 +219,29 @@ __global__ void k_atiles(ATileArgs a, const E *__restrict__ w, const uint8_t *__
         E v = (E)0;
         if (g < a.n_groups && rig < a.group_rows && row < a.R && t < a.L) {
             const int q = a.shared ? t : indices[(size_t)g * a.L + t];
-            const size_t wi = (size_t)row * a.C + q;
+            const int src = a.rowmap ? indices[row] : row;
+            const size_t wi = (size_t)src * a.C + q;
             if (mask[wi]) v = w[wi];
         }
         A[e] = v;
+    }
+}
+
+// Row map of whole-width row pruning.  The kept filters are `kept` ascending
+// (the canonical row lists of the block-rows, in order); output row o is kept iff it
+// is found there, and then it is computed row pos = (kept rows below o).  Otherwise it
+// is pruned row o - pos.  One thread per output row, no atomics.
+__global__ void k_rowmap(const int32_t *__restrict__ kept, int RK, int R, int32_t *__restrict__ rowmap,
+                         int32_t *__restrict__ pruned) {
+    for (int o = blockIdx.x * blockDim.x + threadIdx.x; o < R; o += gridDim.x * blockDim.x) {
+        int lo = 0, hi = RK;   // first position with kept[pos] >= o
+        while (lo < hi) {
+            const int mid = (lo + hi) >> 1;
+            if (kept[mid] < o) lo = mid + 1;
+            else hi = mid;
+        }
+        if (lo < RK && kept[lo] == o) rowmap[lo] = o;
+        else pruned[o - lo] = o;
     }
 }
 
@@ -379,9 +399,15 @@ bsp_status pack_t(const Plan &p, const E *w, const uint8_t *mask, E *values, int
     int32_t *desc = (int32_t *)(tiles + p.off_desc);
     DescArgs da{p.shared, p.n_groups, p.L, p.LP, p.C, p.KH, p.KW, p.CH_STRIDE, p.RS, p.VS, std::max(p.V, 1)};
     k_desc<<<grid_for((size_t)p.n_groups * p.LP), 256, 0, st>>>(da, indices, desc);
-    ATileArgs aa{p.shared, p.n_groups, p.mt_per_group, p.n_mt_pad, p.group_rows, p.S, p.L, p.R, p.C};
+    ATileArgs aa{p.shared, p.n_groups, p.mt_per_group, p.n_mt_pad, p.group_rows, p.S, p.L, p.RK, p.C, p.rowmap};
     const size_t na = (size_t)p.n_mt_pad * p.S * 512;
     k_atiles<E><<<grid_for(na), 256, 0, st>>>(aa, w, mask, indices, (E *)(tiles + p.off_a));
+    if (p.rowmap) {
+        int32_t *rm = (int32_t *)(tiles + p.off_rowmap);
+        const size_t nrm = (size_t)p.n_mt_pad * kMT;
+        k_fill<int32_t><<<grid_for(nrm), 256, 0, st>>>(rm, nrm, 0);
+        k_rowmap<<<grid_for(p.R), 256, 0, st>>>(indices, p.RK, p.R, rm, (int32_t *)(tiles + p.off_pruned));
+    }
     int4 *table = (int4 *)(tiles + p.off_chunks);
     k_step_spans<<<grid_for(p.S), 256, 0, st>>>(desc, p.n_groups, p.LP, p.S, p.CH_STRIDE, table);
     k_build_chunks<<<1, 256, sizeof(int) * 2 * p.S, st>>>(

@@ -63,12 +63,15 @@ static void finish_layout(Plan *p, int n_mt, int astep) {
     p->off_desc = align256(p->off_chunks + (int64_t)16 * p->S);
     p->off_desc16 = align256(p->off_desc + (int64_t)4 * p->n_groups * p->LP);
     p->off_a = align256(p->off_desc16 + (int64_t)2 * p->n_g_pad * p->LP);
-    p->tile_bytes = p->off_a + (int64_t)p->n_mt_pad * p->S * astep;
+    p->off_rowmap = align256(p->off_a + (int64_t)p->n_mt_pad * p->S * astep);
+    p->off_pruned = p->off_rowmap + (int64_t)4 * (p->rowmap ? p->n_mt_pad * kMT : 0);
+    p->tile_bytes = p->off_pruned + (int64_t)4 * (p->rowmap ? p->R - p->RK : 0);
 
     const int fpv[] = {p->R, p->C, p->bh_eff, p->bw_eff, p->reg, p->rate, p->dt, p->n_groups,
                        p->mt_per_group, p->LP, p->S, p->CH_STRIDE, p->RS, p->LEFT, p->NSLOT,
                        p->CC, p->KH, p->KW, p->is_linear, p->SW, p->NSUB, p->SMAX, p->resident,
-                       p->MBT, p->MBG, p->n_mt_pad, p->n_g_pad, p->GE, p->NB, p->pw, p->NGR, p->VS, p->V, 8};
+                       p->MBT, p->MBG, p->n_mt_pad, p->n_g_pad, p->GE, p->NB, p->pw, p->NGR, p->VS, p->V,
+                       p->rowmap, p->RK, 9};
     p->fingerprint = fnv1a(fpv, (int)(sizeof(fpv) / sizeof(fpv[0])));
 }
 
@@ -85,13 +88,13 @@ static bool plan_pointwise(Plan *p, int span_req, int n_mt, int mpg, int astep) 
     double hbm_bytes;
     if (p->is_linear) {
         groups_nom = round_up(div_up(kNominalVectors, 4), gpg);
-        hbm_bytes = ((double)p->Cin + p->R) * kNominalVectors * p->esize;
+        hbm_bytes = ((double)p->Cin + p->RK) * kNominalVectors * p->esize;
     } else if (p->SW == 1) {
         groups_nom = (int64_t)kNominalImages * round_up(div_up(p->H * p->W, 4), gpg);
-        hbm_bytes = ((double)p->Cin + p->R) * kNominalImages * p->H * p->W * p->esize;
+        hbm_bytes = ((double)p->Cin + p->RK) * kNominalImages * p->H * p->W * p->esize;
     } else {
         groups_nom = (int64_t)kNominalImages * p->Ho * div_up(p->Wo, 4);
-        hbm_bytes = ((double)p->Cin * p->H * p->W / 2 + (double)p->R * p->Ho * p->Wo) * kNominalImages * p->esize;
+        hbm_bytes = ((double)p->Cin * p->H * p->W / 2 + (double)p->RK * p->Ho * p->Wo) * kNominalImages * p->esize;
     }
     hbm_bytes += (double)n_mt * p->S * astep;
     const double t_hbm = hbm_bytes / 5.5e12 * 2.4e9;
@@ -257,7 +260,14 @@ bsp_status make_plan(const bsp_scheme *s, const bsp_conv_shape *conv, bsp_dtype 
         p->shared = 1;
         p->n_groups = 1;
         p->group_rows = p->R;
+        // whole-width row blocks keep the same filters for every column: compute only
+        // those (a row map sends them to their output rows)
+        if (p->reg == BSP_ROW && p->nbc == 1 && p->n_indices < p->R) {
+            p->rowmap = 1;
+            p->group_rows = (int)p->n_indices;
+        }
     }
+    p->RK = p->reg == BSP_COL ? p->R : p->group_rows;
     p->mt_per_group = div_up(p->group_rows, kMT);
     p->LP = div_up(p->L, kKS) * kKS;
     p->S = p->LP / kKS;
@@ -462,7 +472,7 @@ bsp_status make_plan(const bsp_scheme *s, const bsp_conv_shape *conv, bsp_dtype 
                         // per tile: epilogue; per workgroup: header, tables, first fill
                         double cyc = rounds * (tpw * nch * per_chunk + tpw * 8000.0 + 8000.0);
                         const double hbm = ((double)nominal_rows / p->Ho * p->Cin * p->H * p->W * p->esize +
-                                            total_groups * 4 * p->R * 2.0) / 5.5e12 * 2.4e9;
+                                            total_groups * 4 * p->RK * 2.0) / 5.5e12 * 2.4e9;
                         cyc = std::max(cyc, hbm);
                         if (qmode == 1) cyc = cyc * 1.5 + 1500.0;                           // partial-sum reduction
                         if (cyc < best * (1 - 1e-9)) {

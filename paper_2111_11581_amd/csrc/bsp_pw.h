@@ -34,7 +34,7 @@ namespace pw {
 
 using namespace bsp::fwd;
 
-template <typename E, int MODE, int TM, int TPG, int KS>
+template <typename E, int MODE, int TM, int TPG, int KS, bool MAP = false>
 __global__ __launch_bounds__(kThreads, pw_occ((int)sizeof(E), MODE, TM)) void k_pw(PwArgs a) {
     constexpr int AB = 8 * (int)sizeof(E);   // weight bytes per lane, one m-tile and step
     constexpr int ASTEP = 64 * AB;           // one m-tile, one step
@@ -206,6 +206,19 @@ __global__ __launch_bounds__(kThreads, pw_occ((int)sizeof(E), MODE, TM)) void k_
         const int p0 = oh * a.Wo + 4 * gi;
         const int nvalid = pix_ok ? max(0, min(4, a.Wo - 4 * gi)) : 0;
         const float qnan = __builtin_nanf("");
+        // row map (kept filter of each computed row): loaded, and waited for, before the
+        // first store, since the kernel counts its outstanding stores by hand
+        int omap[TM][4] = {};
+        if constexpr (MAP) {
+#pragma unroll
+            for (int t2 = 0; t2 < TM; ++t2) {
+                const int gm = mt_first + m_loc0 + t2;
+                const int mt_in = gm - (gm / a.mt_per_group) * a.mt_per_group;
+#pragma unroll
+                for (int i = 0; i < 4; ++i) omap[t2][i] = a.rowmap[mt_in * kMT + 4 * kg + i];
+            }
+            wait_vm_all();
+        }
         int n = 0;
 #pragma unroll
         for (int t2 = 0; t2 < TM; ++t2) {
@@ -214,8 +227,9 @@ __global__ __launch_bounds__(kThreads, pw_occ((int)sizeof(E), MODE, TM)) void k_
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 const int rig = mt_in * kMT + 4 * kg + i;   // row inside the list group
-                const int orow = gidx * a.group_rows + rig;
-                const bool row_ok = rig < a.group_rows && orow < a.R;
+                const int crow = gidx * a.group_rows + rig;
+                const bool row_ok = rig < a.group_rows && crow < a.R;
+                const int orow = MAP ? omap[t2][i] : crow;
                 const float bv = a.bias ? s_bias[(m_loc0 + t2) * kMT + 4 * kg + i] : 0.f;
                 float o[4];
 #pragma unroll
@@ -271,7 +285,7 @@ __global__ __launch_bounds__(kThreads, pw_occ((int)sizeof(E), MODE, TM)) void k_
             const int gm = mt_first + r / kMT;
             const int gidx = gm / a.mt_per_group;
             const int orow = gidx * a.group_rows + (gm - gidx * a.mt_per_group) * kMT + r % kMT;
-            s_bias[r] = orow < a.R ? a.bias[orow] : 0.f;
+            s_bias[r] = orow < a.R ? a.bias[MAP ? a.rowmap[orow] : orow] : 0.f;
         }
     const int NB = a.NB;
     const int nchx = max(nch, 1);
@@ -362,17 +376,27 @@ __global__ __launch_bounds__(kThreads, pw_occ((int)sizeof(E), MODE, TM)) void k_
 
 typedef void (*pw_fn)(PwArgs);
 
-template <typename E, int MODE, int TM, int TPG, int KSM>
+template <typename E, int MODE, int TM, int TPG, int KSM, bool MAP = false>
 pw_fn pw_pick_ks(int KS) {
-    if constexpr ((KSM & 2) != 0) if (KS == 1) return k_pw<E, MODE, TM, TPG, 1>;
-    if constexpr ((KSM & 4) != 0) if (KS == 2) return k_pw<E, MODE, TM, TPG, 2>;
-    if constexpr ((KSM & 16) != 0) if (KS == 4) return k_pw<E, MODE, TM, TPG, 4>;
+    if constexpr ((KSM & 2) != 0) if (KS == 1) return k_pw<E, MODE, TM, TPG, 1, MAP>;
+    if constexpr ((KSM & 4) != 0) if (KS == 2) return k_pw<E, MODE, TM, TPG, 2, MAP>;
+    if constexpr ((KSM & 16) != 0) if (KS == 4) return k_pw<E, MODE, TM, TPG, 4, MAP>;
     return nullptr;
 }
 
-// TMMAX: most m-tiles per wave instantiated
+// TMMAX: most m-tiles per wave instantiated.  MAP (row-mapped layers: one list shared
+// by all m-tiles) exists for TPG == TM only.
 template <typename E, int MODE, int KSM, int TMMAX>
-pw_fn pw_pick_tm(int TM, int TPG, int KS) {
+pw_fn pw_pick_tm(int TM, int TPG, int KS, bool map) {
+    if (map) {
+        if (TPG != TM) return nullptr;
+        switch (TM) {
+            case 1: return pw_pick_ks<E, MODE, 1, 1, KSM, true>(KS);
+            case 2: if constexpr (TMMAX >= 2) return pw_pick_ks<E, MODE, 2, 2, KSM, true>(KS); return nullptr;
+            case 4: if constexpr (TMMAX >= 4) return pw_pick_ks<E, MODE, 4, 4, KSM, true>(KS); return nullptr;
+            default: return nullptr;
+        }
+    }
     switch (TM * 16 + TPG) {
         case 0x11: return pw_pick_ks<E, MODE, 1, 1, KSM>(KS);
         case 0x21: if constexpr (TMMAX >= 2) return pw_pick_ks<E, MODE, 2, 1, KSM>(KS); return nullptr;

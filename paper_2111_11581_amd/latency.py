@@ -159,11 +159,12 @@ def sweep_settings(cin=256, cout=256, h=56, w=56, k=3, batch=64, blocks=(4, 8, 1
     return st
 
 
-def measure(settings, reps: int = 10, rounds: int = 3, seed: int = 1234, device=None) -> LatencyModel:
-    """Times the library's forward call for each setting (bf16; a graph of ``reps``
-    back-to-back launches, replayed ``rounds`` times; mean per launch).  Weights and
-    activations are seeded normal draws made on the device: only their shapes matter
-    for the latency."""
+def measure(settings, reps: int = 10, rounds: int = 10, seed: int = 1234, device=None) -> LatencyModel:
+    """Times the library's forward call for each setting (bf16): a graph of ``reps``
+    back-to-back launches of the layer (the test model of ten layers of one setting,
+    Sec. 5.2.1), replayed ``rounds`` times (100 runs by default); mean per launch.
+    Weights and activations are seeded normal draws made on the device (He-normal
+    weights): the latency depends on the shapes and the kept structure only."""
     import torch
     from . import BF16, ConvShape, Scheme, bsp_version
     from .layers import PackedLayer
@@ -200,6 +201,62 @@ def measure(settings, reps: int = 10, rounds: int = 3, seed: int = 1234, device=
     return model
 
 
+def report(model: LatencyModel, betas=(0.0, 0.1, 0.2, 0.5)) -> str:
+    """Markdown summary of a model: per layer, the latency of every block size and
+    rate (and its ratio to whole-matrix pruning at the same regularity and rate), the
+    reference points, and the rule's choice for each beta."""
+    out = []
+    layers = {}
+    for s in model.settings.values():
+        layers.setdefault(s.layer_key(), []).append(s)
+    for lk in sorted(layers):
+        st = layers[lk]
+        rates = sorted({s.rate for s in st if s.regularity in (0, 1)})
+        out.append(f"### {lk}\n")
+        for reg in (0, 1):
+            rs = [s for s in st if s.regularity == reg]
+            if not rs:
+                continue
+            out.append(f"{REG_NAMES[reg]} pruning: latency in us (ratio to whole-matrix blocks at the same rate)\n")
+            out.append("| block | " + " | ".join(f"{r}x" for r in rates) + " |")
+            out.append("|---|" + "---|" * len(rates))
+            blocks = sorted({(s.bh, s.bw) for s in rs}, key=lambda b: (b == (0, 0), b))
+            for b in blocks:
+                cells = []
+                for r in rates:
+                    x = [s for s in rs if (s.bh, s.bw) == b and s.rate == r]
+                    w = [s for s in rs if (s.bh, s.bw) == (0, 0) and s.rate == r]
+                    if not x:
+                        cells.append("-")
+                        continue
+                    us = model.latency(x[0]) * 1e3
+                    cells.append(f"{us:.1f} ({model.latency(x[0]) / model.latency(w[0]):.2f})" if w else f"{us:.1f}")
+                name = "whole" if b == (0, 0) else f"{b[0]}x{b[1]}"
+                out.append(f"| {name} | " + " | ".join(cells) + " |")
+            out.append("")
+        refs = [s for s in st if s.regularity in (2, 3)]
+        if refs:
+            out.append("reference points: " + ", ".join(
+                f"{'dense' if s.regularity == 3 else f'unstructured {s.rate}x'} {model.latency(s) * 1e3:.1f} us"
+                for s in sorted(refs, key=lambda s: (s.regularity, s.rate))) + "\n")
+        out.append("rule choice (smallest block within (1 + beta) of whole-matrix blocks, latency per dense MAC):\n")
+        out.append("| regularity | rate | " + " | ".join(f"beta {b:g}" for b in betas) + " |")
+        out.append("|---|---|" + "---|" * len(betas))
+        for reg in (0, 1):
+            for r in rates:
+                cells = []
+                for b in betas:
+                    try:
+                        bh, bw = select_block_size(model, st[0], reg, r, b)
+                    except KeyError:
+                        cells.append("-")
+                        continue
+                    cells.append("whole" if (bh, bw) == (0, 0) else f"{bh}x{bw}")
+                out.append(f"| {REG_NAMES[reg]} | {r}x | " + " | ".join(cells) + " |")
+        out.append("")
+    return "\n".join(out)
+
+
 def _main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
     sub = ap.add_subparsers(dest="cmd", required=True)
@@ -211,7 +268,13 @@ def _main(argv=None):
     s = sub.add_parser("select", help="block size per regularity and rate from a saved model")
     s.add_argument("--model", required=True)
     s.add_argument("--beta", type=float, default=0.2)
+    r = sub.add_parser("report", help="markdown summary of a saved model and the rule's choices")
+    r.add_argument("--model", required=True)
+    r.add_argument("--betas", type=float, nargs="+", default=[0.0, 0.1, 0.2, 0.5])
     a = ap.parse_args(argv)
+    if a.cmd == "report":
+        print(report(LatencyModel.load(a.model), tuple(a.betas)))
+        return 0
     if a.cmd == "build":
         st = sweep_settings(cin=a.cin, cout=a.cin, h=a.hw, w=a.hw, batch=a.batch, references=True)
         m = measure(st)

@@ -119,6 +119,13 @@ CONV_CASES = [
     _conv_case("f32 3x3 s2 row", 2, 16, 11, 11, 48, 3, 2, 1, 16, 16, ROW, 2, dtype="f32", out="f32"),
     _conv_case("3x3 col r16 many chunks", 1, 512, 6, 6, 64, 3, 1, 1, 16, 64, COL, 16),
     _conv_case("1x1 col whole r2 4x4 image", 3, 256, 4, 4, 64, 1, 1, 0, 0, 0, COL, 2),
+    # whole-width row blocks: only the kept filters are computed (row map + pruned-row fill)
+    _conv_case("1x1 row whole r4 relu bias", 2, 64, 14, 14, 100, 1, 1, 0, 0, 0, ROW, 4, relu=True, bias=True),
+    _conv_case("1x1 row 32xwhole r2 s2", 2, 64, 14, 14, 96, 1, 2, 0, 32, 0, ROW, 2),
+    _conv_case("3x3 row 16xwhole r3 ragged", 2, 24, 9, 11, 70, 3, 1, 1, 16, 0, ROW, 3, bias=True),
+    _conv_case("3x3 row whole r16 relu", 1, 32, 10, 10, 64, 3, 1, 1, 0, 0, ROW, 16, relu=True),
+    _conv_case("f32 3x3 row whole r4 bias", 1, 16, 12, 12, 40, 3, 1, 1, 0, 0, ROW, 4, dtype="f32", out="f32",
+               bias=True),
 ]
 
 
@@ -153,6 +160,29 @@ def test_conv_matches_oracle(B, case):
     assert np.isfinite(got).all()
     err = rel_l2(got, ref)
     assert err <= TOL[dtype], f"{case['name']}: rel-L2 {err:.3e}"
+
+
+def test_filter_pruning_writes_the_bias_of_pruned_filters_exactly(B):
+    """Whole-matrix row pruning removes whole filters (Sec. 4.4): their outputs are
+    exactly ReLU(b[o]) in the output precision, the kept filters match the oracle."""
+    import torch
+    for relu in (False, True):
+        layer = ConvLayer("fp", 2, 32, 9, 9, 48, 3, 3, 1, 1, 1, 1, 0, 0, ROW, 4, "bf16", ("normal", 0, 1.0),
+                          ("normal", 0, 0.08), relu=relu)
+        d = draw_layer(layer, 8, 77, with_bias=True)
+        bias = d["bias"]
+        L, y = run_conv(B, layer, d["x"], d["w"], "bf16", "bf16", bias, relu)
+        m = L.mask.cpu().numpy().reshape(layer.cout, -1)
+        pruned = np.nonzero(m.sum(axis=1) == 0)[0]
+        assert len(pruned) == 36
+        got = out_to_f64(from_dev(y, "bf16"), "bf16")
+        b32 = bias.astype(np.float32)
+        expect = np.maximum(b32, 0) if relu else b32
+        expect_bf16 = out_to_f64(from_dev(torch.from_numpy(expect).to(torch.bfloat16).cuda(), "bf16"), "bf16")
+        for o in pruned:
+            assert np.all(got[:, o] == expect_bf16[o]), o
+        ref = oracle_conv(d["x"], d["w"], m, "bf16", layer, bias=bias, relu=relu)
+        assert rel_l2(got, ref) <= TOL["bf16"]
 
 
 def test_conv_is_deterministic_and_empty_batch_is_a_noop(B):
@@ -218,6 +248,25 @@ def test_resnet50_layer_full_batch_sampled_images(B, idx, layer):
     assert err <= TOL["bf16"], f"{layer.name}: rel-L2 {err:.3e}"
 
 
+C5_SAMPLED = ["c5 row whole r16", "c5 row 4x4 r16", "c5 row 32x32 r4", "c5 col 4x4 r4", "c5 col whole r8",
+              "c5 col 64x64 r2", "c5 unstructured r4"]
+
+
+@pytest.mark.parametrize("name", C5_SAMPLED)
+def test_c5_sweep_layer_full_batch_sampled_images(B, name):
+    """The block-size sweep's 3x3 256->256 conv at 56x56, batch 64, in the launch
+    configuration the latency model times; images 0 and 63 checked in full."""
+    idx, layer = [(i, l) for i, l in enumerate(workload(5)) if l.name == name][0]
+    d = draw_layer(layer, 5, idx)
+    L, y = run_conv(B, layer, d["x"], d["w"], "bf16", "bf16")
+    m = L.mask.cpu().numpy().reshape(layer.cout, -1)
+    assert np.array_equal(m, oracle_mask(d["w"], "bf16", layer.scheme))
+    ref = oracle_conv(d["x"], d["w"], m, "bf16", layer, images=[0, layer.n - 1])
+    got = out_to_f64(from_dev(y, "bf16"), "bf16")[[0, layer.n - 1]]
+    err = rel_l2(got, ref)
+    assert err <= TOL["bf16"], f"{name}: rel-L2 {err:.3e}"
+
+
 def test_c1_full(B):
     layer = workload(1)[0]
     d = draw_layer(layer, 1, 0)
@@ -256,7 +305,8 @@ def test_c4_fc_layer_sampled_columns(B):
 
 @pytest.mark.parametrize("batch,reg,bh,bw,rate,out_dt,relu", [
     (37, COL, 32, 32, 10, "bf16", False), (100, ROW, 32, 32, 2, "f32", True),
-    (64, DENSE, 0, 0, 1, "bf16", True), (130, COL, 16, 64, 4, "bf16", False)])
+    (64, DENSE, 0, 0, 1, "bf16", True), (130, COL, 16, 64, 4, "bf16", False),
+    (100, ROW, 0, 0, 4, "bf16", True), (70, ROW, 32, 0, 2, "f32", False)])
 def test_linear_small(B, batch, reg, bh, bw, rate, out_dt, relu):
     layer = LinearLayer("fc", batch, 320, 200, bh, bw, reg, rate, "bf16", ("uniform", -1, 1),
                         ("normal", 0, 0.05), relu=relu)
