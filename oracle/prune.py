@@ -12,6 +12,11 @@ Paper passages followed:
 * Sec. 4.4: a 1x1 block is unstructured pruning, the whole matrix as one block
   is structured (filter / channel) pruning.
 * Sec. 6 (tables): the compression rate is the parameter reduction factor.
+* Sec. 4.1.2 and Eq. 4 (block-punched pruning for CONV layers): the weight
+  tensor is cut into blocks of filters x input channels; inside a block the
+  group of kernel location (m, n) is the weight at (m, n) of every kernel of
+  the block, measured by its squared Frobenius norm, and a pruned location is
+  removed from all kernels of the block.
 
 Readings where the paper is silent (each listed in the design notes):
 * kept groups per block = ceil(extent / rate) with an integer rate;
@@ -20,7 +25,10 @@ Readings where the paper is silent (each listed in the design notes):
   bf16 values are exact in fp64, so the order is the only rounding choice);
 * blocks are anchored at (0, 0); a ragged last block keeps
   ceil(its own extent / rate);
-* a block size of 0 means the whole extent.
+* a block size of 0 means the whole extent;
+* block-punched: blocks of bh filters x bw input channels; kept locations per
+  block = ceil(kh*kw / rate); the score of a location sums over the block's
+  (filter, channel) pairs in ascending (filter, channel) order.
 
 Pins: tests/test_oracle_prune.py (brute-force subset enumeration, invariants,
 ties, ragged edges, scale invariance, hand-derived golden masks).
@@ -30,7 +38,7 @@ from __future__ import annotations
 
 import numpy as np
 
-ROW, COL, UNSTRUCTURED, DENSE = 0, 1, 2, 3
+ROW, COL, UNSTRUCTURED, DENSE, PUNCHED = 0, 1, 2, 3, 4
 
 
 def kept_count(extent: int, rate: int) -> int:
@@ -76,11 +84,39 @@ def top_k(scores: np.ndarray, k: int) -> np.ndarray:
     return np.sort(order[:k])
 
 
-def prune_mask(wg: np.ndarray, bh: int, bw: int, regularity: int, rate: int) -> np.ndarray:
-    """Mask (uint8, R x C) of the kept weights of a GEMM-form fp64 matrix."""
+def punched_mask(wg: np.ndarray, khw: int, bh: int, bw: int, rate: int) -> np.ndarray:
+    """Block-punched mask (Sec. 4.1.2, Eq. 4) of a GEMM-form fp64 conv weight
+    (R filters x Cin*khw columns, column = c*khw + location).
+
+    Blocks are bh filters x bw input channels (0: all).  The score of location
+    l in a block is the sum of w[o, c*khw + l]^2 over the block's kernels,
+    taken in ascending (o, c) order; the ceil(khw / rate) best locations are
+    kept in every kernel of the block (ties to the lower location).
+    """
+    wg = np.asarray(wg, dtype=np.float64)
+    R, C = wg.shape
+    if khw < 1 or C % khw:
+        raise ValueError("columns must be Cin * khw")
+    cin = C // khw
+    w3 = wg.reshape(R, cin, khw)
+    k = kept_count(khw, rate)
+    mask = np.zeros((R, cin, khw), dtype=np.uint8)
+    for r0, r1 in block_ranges(R, bh):
+        for c0, c1 in block_ranges(cin, bw):
+            groups = w3[r0:r1, c0:c1, :].reshape(-1, khw)    # rows: kernels (o, c) in order
+            s = np.cumsum(groups * groups, axis=0)[-1]
+            mask[r0:r1, c0:c1, top_k(s, k)] = 1
+    return mask.reshape(R, C)
+
+
+def prune_mask(wg: np.ndarray, bh: int, bw: int, regularity: int, rate: int, khw: int = 1) -> np.ndarray:
+    """Mask (uint8, R x C) of the kept weights of a GEMM-form fp64 matrix
+    (khw: kernel locations per input channel, used by block-punched pruning)."""
     wg = np.asarray(wg, dtype=np.float64)
     R, C = wg.shape
     mask = np.zeros((R, C), dtype=np.uint8)
+    if regularity == PUNCHED:
+        return punched_mask(wg, max(int(khw), 1), bh, bw, rate)
     if regularity == DENSE:
         mask[:] = 1
         return mask
@@ -111,13 +147,27 @@ def unstructured_mask(wg: np.ndarray, rate: int) -> np.ndarray:
     return m.reshape(R, C)
 
 
-def mask_is_valid(mask: np.ndarray, bh: int, bw: int, regularity: int, rate: int) -> bool:
+def mask_is_valid(mask: np.ndarray, bh: int, bw: int, regularity: int, rate: int, khw: int = 1) -> bool:
     """True iff the mask has the block structure of the scheme: every block
-    keeps whole columns (COL) or whole rows (ROW), exactly ceil(extent/rate)."""
+    keeps whole columns (COL) or whole rows (ROW), exactly ceil(extent/rate);
+    block-punched: the same ceil(khw/rate) locations in every kernel of a block."""
     mask = np.asarray(mask, dtype=np.uint8)
     R, C = mask.shape
     if not np.all((mask == 0) | (mask == 1)):
         return False
+    if regularity == PUNCHED:
+        khw = max(int(khw), 1)
+        if C % khw:
+            return False
+        m3 = mask.reshape(R, C // khw, khw)
+        for r0, r1 in block_ranges(R, bh):
+            for c0, c1 in block_ranges(C // khw, bw):
+                blk = m3[r0:r1, c0:c1, :]
+                if not np.all(blk == blk[0:1, 0:1, :]):
+                    return False
+                if int(blk[0, 0].sum()) != kept_count(khw, rate):
+                    return False
+        return True
     if regularity == DENSE:
         return bool(np.all(mask == 1))
     if regularity == UNSTRUCTURED:
@@ -145,6 +195,8 @@ def pack(w_stored: np.ndarray, mask: np.ndarray, bh: int, bw: int, regularity: i
          columns, block by block left to right, ascending inside a block (so
          ascending overall); ``values[rowptr[i]*bh + p*len + t]`` is
          W[i*bh + p, indices[rowptr[i] + t]].
+    PUNCHED: as COL (a block-row keeps whole GEMM columns: the kept locations
+         of each of its channel blocks).
     ROW: for block (i, j) in row-major order, ``indices[rowptr[b]:rowptr[b+1]]``
          are its kept rows ascending; its values are rows of the block,
          ``[t][q_local]``, stored one block after the other.
@@ -158,7 +210,7 @@ def pack(w_stored: np.ndarray, mask: np.ndarray, bh: int, bw: int, regularity: i
         return {"indices": np.zeros(0, np.int32), "rowptr": np.zeros(0, np.int32),
                 "values": vals.reshape(-1).copy()}
     idx, ptr, vals = [], [0], []
-    if regularity == COL:
+    if regularity in (COL, PUNCHED):
         for r0, r1 in block_ranges(R, bh):
             kept = np.nonzero(mask[r0])[0].astype(np.int32)
             idx.append(kept)
@@ -183,7 +235,7 @@ def unpack(packed: dict, R: int, C: int, bh: int, bw: int, regularity: int, like
     if regularity in (DENSE, UNSTRUCTURED):
         return vals.reshape(R, C).copy()
     off = 0
-    if regularity == COL:
+    if regularity in (COL, PUNCHED):
         for i, (r0, r1) in enumerate(block_ranges(R, bh)):
             kept = idx[ptr[i]:ptr[i + 1]]
             n = (r1 - r0) * len(kept)

@@ -15,8 +15,8 @@ from __future__ import annotations
 import math
 from dataclasses import dataclass, field
 
-ROW, COL, UNSTRUCTURED, DENSE = 0, 1, 2, 3
-REG_NAMES = {ROW: "row", COL: "col", UNSTRUCTURED: "unstructured", DENSE: "dense"}
+ROW, COL, UNSTRUCTURED, DENSE, PUNCHED = 0, 1, 2, 3, 4
+REG_NAMES = {ROW: "row", COL: "col", UNSTRUCTURED: "unstructured", DENSE: "dense", PUNCHED: "punched"}
 
 
 @dataclass(frozen=True)
@@ -25,8 +25,10 @@ class Scheme:
     cols: int
     bh: int            # 0 => whole extent
     bw: int            # 0 => whole extent
-    regularity: int    # ROW / COL / UNSTRUCTURED / DENSE
+    regularity: int    # ROW / COL / UNSTRUCTURED / DENSE / PUNCHED
     rate: int          # integer >= 1
+    khw: int = 1       # kernel locations per input channel (block-punched: blocks are
+                       # bh filters x bw input channels)
 
     def label(self) -> str:
         if self.regularity in (UNSTRUCTURED, DENSE):
@@ -88,7 +90,7 @@ class ConvLayer:
     @property
     def scheme(self) -> Scheme:
         return Scheme(self.cout, self.cin * self.kh * self.kw, self.bh, self.bw,
-                      self.regularity, self.rate)
+                      self.regularity, self.rate, self.kh * self.kw)
 
 
 @dataclass(frozen=True)

@@ -43,7 +43,7 @@ def rel_l2(got: np.ndarray, ref: np.ndarray) -> float:
 
 def oracle_mask(w_stored: np.ndarray, dtype: str, scheme) -> np.ndarray:
     wg = as_f64(w_stored, dtype).reshape(scheme.rows, scheme.cols)
-    return OP.prune_mask(wg, scheme.bh, scheme.bw, scheme.regularity, scheme.rate)
+    return OP.prune_mask(wg, scheme.bh, scheme.bw, scheme.regularity, scheme.rate, getattr(scheme, "khw", 1))
 
 
 def oracle_conv(x, w, mask, dtype, layer, bias=None, relu=False, images=None) -> np.ndarray:

@@ -236,3 +236,103 @@ def test_invalid_masks_are_rejected():
     assert P.mask_is_valid(mr, 8, 16, P.ROW, 2)
     bad = mr.copy(); bad[np.nonzero(mr[:, 0])[0][0], 5] = 0
     assert not P.mask_is_valid(bad, 8, 16, P.ROW, 2)
+
+
+# --------------------------------------------------------- block-punched ---
+# Sec. 4.1.2 and Eq. 4: blocks of filters x input channels; the group of a kernel
+# location is that location in every kernel of the block.
+
+def _gemm(w_oihw):
+    w = np.asarray(w_oihw, dtype=np.float64)
+    return w.reshape(w.shape[0], -1)
+
+
+@pytest.mark.parametrize("case", ["whole_block_rate2", "filter_blocks_rate2", "channel_blocks_rate4"])
+def test_punched_golden_masks(case):
+    g = GOLD["punched_2x2x2x2"]
+    ex = g[case]
+    m = P.prune_mask(_gemm(g["W_oihw"]), ex["bh"], ex["bw"], P.PUNCHED, ex["rate"], khw=4)
+    assert m.tolist() == ex["mask"]
+    assert P.mask_is_valid(m, ex["bh"], ex["bw"], P.PUNCHED, ex["rate"], khw=4)
+    if "indices" in ex:
+        pk = P.pack(_gemm(g["W_oihw"]), m, ex["bh"], ex["bw"], P.PUNCHED, ex["rate"])
+        assert pk["indices"].tolist() == ex["indices"]
+        assert pk["rowptr"].tolist() == ex["rowptr"]
+        assert pk["values"].tolist() == ex["values"]
+
+
+@pytest.mark.parametrize("bh,rate,khw", [(2, 2, 9), (4, 3, 9), (0, 9, 9), (3, 2, 25), (0, 4, 4)])
+def test_punched_with_one_channel_blocks_is_column_pruning(bh, rate, khw):
+    """A block of one input channel holds that channel's khw GEMM columns: punched
+    locations are then the columns of a (bh x khw) column block (Eq. 3)."""
+    rng = np.random.default_rng(bh * 100 + rate * 10 + khw)
+    wg = rng.standard_normal((12, 5 * khw))
+    m = P.prune_mask(wg, bh, 1, P.PUNCHED, rate, khw=khw)
+    assert np.array_equal(m, P.prune_mask(wg, bh, khw, P.COL, rate))
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_punched_brute_force_on_small_integer_blocks(seed):
+    """Integer weights make every sum exact; the kept locations of each block must
+    be the k-subset of largest total score, lexicographically smallest on ties."""
+    rng = np.random.default_rng(40 + seed)
+    R, cin, khw = 5, 7, 4 + seed % 3 * 2          # khw 4, 6, 8
+    bh, bw, rate = [(2, 3, 2), (0, 2, 3), (3, 0, 2)][seed % 3]
+    w = rng.integers(-3, 4, size=(R, cin, khw)).astype(np.float64)
+    m = P.prune_mask(w.reshape(R, -1), bh, bw, P.PUNCHED, rate, khw=khw).reshape(R, cin, khw)
+    k = P.kept_count(khw, rate)
+    for r0, r1 in P.block_ranges(R, bh):
+        for c0, c1 in P.block_ranges(cin, bw):
+            s = [sum(w[o, c, l] ** 2 for o in range(r0, r1) for c in range(c0, c1)) for l in range(khw)]
+            best = max(itertools.combinations(range(khw), k), key=lambda t: (sum(s[i] for i in t),
+                                                                              [-i for i in t]))
+            kept = tuple(np.nonzero(m[r0, c0])[0])
+            assert kept == best, (r0, c0, s)
+            assert np.all(m[r0:r1, c0:c1] == m[r0, c0])
+
+
+def test_punched_invariants_and_degenerate_cases():
+    rng = np.random.default_rng(7)
+    R, cin, khw = 16, 12, 9
+    wg = rng.standard_normal((R, cin * khw))
+    for bh, bw, rate in [(4, 4, 2), (8, 5, 3), (0, 0, 4), (3, 7, 9), (16, 1, 5)]:
+        m = P.prune_mask(wg, bh, bw, P.PUNCHED, rate, khw=khw)
+        assert P.mask_is_valid(m, bh, bw, P.PUNCHED, rate, khw=khw)
+        # every kernel keeps ceil(khw / rate) locations
+        assert np.all(m.reshape(R, cin, khw).sum(axis=2) == P.kept_count(khw, rate))
+        # scale by a power of two and sign flip: same mask (exact in fp64)
+        assert np.array_equal(P.prune_mask(-wg * 2.0 ** 5, bh, bw, P.PUNCHED, rate, khw=khw), m)
+    assert P.prune_mask(wg, 4, 4, P.PUNCHED, 1, khw=khw).all()              # rate 1 keeps all
+    assert P.prune_mask(wg, 4, 4, P.PUNCHED, 3, khw=1).all()                # 1x1 kernels: one location
+    # a mask with one kernel off its block's pattern is rejected
+    m = P.prune_mask(wg, 4, 4, P.PUNCHED, 3, khw=khw)
+    bad = m.copy().reshape(R, cin, khw)
+    bad[1, 2] = np.roll(bad[1, 2], 1)
+    assert not P.mask_is_valid(bad.reshape(R, -1), 4, 4, P.PUNCHED, 3, khw=khw)
+
+
+def test_punched_is_invariant_to_kernel_order_inside_a_block():
+    """Integer weights (exact sums): permuting the filters or channels of a block
+    permutes nothing in its kept locations."""
+    rng = np.random.default_rng(11)
+    R, cin, khw = 6, 4, 9
+    w = rng.integers(-4, 5, size=(R, cin, khw)).astype(np.float64)
+    m = P.prune_mask(w.reshape(R, -1), 0, 0, P.PUNCHED, 3, khw=khw).reshape(R, cin, khw)
+    wp = w[rng.permutation(R)][:, rng.permutation(cin)]
+    mp = P.prune_mask(wp.reshape(R, -1), 0, 0, P.PUNCHED, 3, khw=khw).reshape(R, cin, khw)
+    assert np.array_equal(m[0, 0], mp[0, 0])
+
+
+def test_punched_pack_unpack_roundtrip_bitwise():
+    rng = np.random.default_rng(5)
+    R, cin, khw = 20, 9, 9
+    wb = f32_to_bf16_bits(rng.standard_normal((R, cin * khw)).astype(np.float32))
+    wg = P.as_f64(wb, "bf16")
+    for bh, bw, rate in [(8, 4, 3), (0, 2, 2), (6, 0, 9)]:
+        m = P.prune_mask(wg, bh, bw, P.PUNCHED, rate, khw=khw)
+        pk = P.pack(wb, m, bh, bw, P.PUNCHED, rate)
+        # a block-row keeps cin * ceil(khw / rate) whole columns
+        L = cin * P.kept_count(khw, rate)
+        assert np.all(np.diff(pk["rowptr"]) == L)
+        back = P.unpack(pk, R, cin * khw, bh, bw, P.PUNCHED, wb)
+        assert np.array_equal(back, np.where(m == 1, wb, 0).astype(wb.dtype))
