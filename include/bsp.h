@@ -10,6 +10,12 @@
  * (Sec. 5.1).  A block size of 0 means the whole extent, so a whole-matrix
  * block is structured (filter / channel) pruning (Sec. 4.4).
  *
+ * Block-punched pruning (BSP_PUNCHED, Sec. 4.1.2 with the group norm of
+ * Eq. 4) is the conv-layer variant: the weight tensor is cut into blocks of
+ * bh filters x bw input channels, and a kernel location (r, s) is kept or
+ * removed in every kernel of a block at once; its score is the squared norm
+ * of the weights at (r, s) over the block's kernels.
+ *
  * Conventions for every entry point
  *  - Pointers named w, mask, values, indices, rowptr, dev_tiles, x, y, bias
  *    are DEVICE pointers owned by the caller.  The library keeps no state
@@ -50,16 +56,24 @@ typedef enum {
     BSP_ROW = 0,            /* whole rows removed inside each block   (Eq. 2) */
     BSP_COL = 1,            /* whole columns removed inside each block (Eq. 3) */
     BSP_UNSTRUCTURED = 2,   /* magnitude top-k over the whole layer (Sec. 2.1.1) */
-    BSP_DENSE = 3           /* nothing removed                                 */
+    BSP_DENSE = 3,          /* nothing removed                                 */
+    BSP_PUNCHED = 4         /* kernel locations removed per block of filters x
+                               input channels (Sec. 4.1.2, Eq. 4)              */
 } bsp_regularity;
 
 typedef struct {
     int32_t rows, cols;     /* GEMM form: rows = Cout / out_features,
                                cols = Cin*kh*kw / in_features                 */
-    int32_t bh, bw;         /* block size; 0 => whole extent                  */
+    int32_t bh, bw;         /* block size; 0 => whole extent.  BSP_PUNCHED:
+                               bh filters x bw input channels                  */
     int32_t regularity;     /* bsp_regularity                                  */
     int32_t rate;           /* integer >= 1; kept per block = ceil(extent/rate);
-                               UNSTRUCTURED keeps ceil(rows*cols/rate)         */
+                               UNSTRUCTURED keeps ceil(rows*cols/rate);
+                               PUNCHED keeps ceil(khw/rate) locations          */
+    int32_t khw;            /* BSP_PUNCHED: kernel locations per input channel
+                               (kh*kw; cols = Cin*khw, column = c*khw + r*kw + s);
+                               must equal kh*kw of the conv shape.  Ignored by
+                               the other regularities (0 reads as 1).          */
 } bsp_scheme;
 
 /* Convolution geometry: dilation 1, groups 1, NCHW activations, OIHW weights. */
@@ -70,15 +84,17 @@ typedef struct {
 /* Sizes (in elements, and bytes for dev_tiles) of the buffers bsp_pack fills.
  * Host-only, pure.  conv_or_null selects the conv layout (its n is ignored);
  * NULL means a linear layer.  The canonical arrays are
- *   COL: values = nnz, indices = n_block_rows * kept_per_row, rowptr = n_block_rows + 1
+ *   COL, PUNCHED: values = nnz, indices = n_block_rows * kept_per_row,
+ *        rowptr = n_block_rows + 1 (PUNCHED keeps Cin*ceil(khw/rate) per row)
  *   ROW: values = nnz, indices = kept rows summed over blocks, rowptr = n_blocks + 1
  *   DENSE / UNSTRUCTURED: values = rows * cols, indices = rowptr = 0. */
 bsp_status bsp_packed_sizes(const bsp_scheme *scheme, const bsp_conv_shape *conv_or_null,
                             bsp_dtype wdt, int64_t *n_values, int64_t *n_indices,
                             int64_t *n_rowptr, int64_t *dev_tile_bytes);
 
-/* Prune (Sec. 4.1.1 with the group norms of Eqs. 2-3, one-shot magnitude
- * selection of Sec. 5.1): w is the GEMM-form weight matrix, row-major
+/* Prune (Sec. 4.1.1 with the group norms of Eqs. 2-3, Sec. 4.1.2 with the
+ * norm of Eq. 4, one-shot magnitude selection of Sec. 5.1): w is the GEMM-form
+ * weight matrix, row-major
  * rows x cols, of dtype wdt; mask (rows x cols bytes, row-major) receives 1
  * for kept and 0 for removed weights.  Async.  The whole-layer magnitude
  * ranking of BSP_UNSTRUCTURED allocates a small scratch buffer on `stream`
@@ -94,6 +110,8 @@ bsp_status bsp_prune(const bsp_scheme *scheme, bsp_dtype wdt, const void *w, uin
  *     COL: for block-row i, indices[rowptr[i] .. rowptr[i+1]) are its kept
  *          columns in ascending order; values[rowptr[i]*bh + p*len + t] =
  *          W[i*bh + p][indices[rowptr[i] + t]] (len = rowptr[i+1]-rowptr[i]).
+ *     PUNCHED: as COL; block-row i (bh filters) keeps whole GEMM columns, the
+ *          kept locations of each input channel.
  *     ROW: for block b = i*n_block_cols + j, indices[rowptr[b] .. rowptr[b+1])
  *          are its kept rows ascending; its values are those rows restricted
  *          to the block's columns, [t][q_local], blocks stored in order b.

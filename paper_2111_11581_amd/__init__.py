@@ -14,13 +14,13 @@ import ctypes
 import os
 
 __all__ = [
-    "F32", "BF16", "ROW", "COL", "UNSTRUCTURED", "DENSE", "BspError", "Scheme", "ConvShape",
+    "F32", "BF16", "ROW", "COL", "UNSTRUCTURED", "DENSE", "PUNCHED", "BspError", "Scheme", "ConvShape",
     "lib", "lib_path", "bsp_packed_sizes", "bsp_prune", "bsp_pack", "bsp_unpack", "bsp_conv2d",
     "bsp_linear", "bsp_maxpool2x2", "bsp_status_string", "bsp_version",
 ]
 
 F32, BF16 = 0, 1
-ROW, COL, UNSTRUCTURED, DENSE = 0, 1, 2, 3
+ROW, COL, UNSTRUCTURED, DENSE, PUNCHED = 0, 1, 2, 3, 4
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _LIB_PATH = os.path.join(_HERE, "_build", "libbsp.so")
@@ -34,7 +34,7 @@ class BspError(RuntimeError):
 
 
 class Scheme(ctypes.Structure):
-    _fields_ = [(n, ctypes.c_int32) for n in ("rows", "cols", "bh", "bw", "regularity", "rate")]
+    _fields_ = [(n, ctypes.c_int32) for n in ("rows", "cols", "bh", "bw", "regularity", "rate", "khw")]
 
 
 class ConvShape(ctypes.Structure):
@@ -76,7 +76,8 @@ def lib():
 def _scheme(s) -> Scheme:
     if isinstance(s, Scheme):
         return s
-    return Scheme(int(s.rows), int(s.cols), int(s.bh), int(s.bw), int(s.regularity), int(s.rate))
+    return Scheme(int(s.rows), int(s.cols), int(s.bh), int(s.bw), int(s.regularity), int(s.rate),
+                  int(getattr(s, "khw", 1)))
 
 
 def _shape(c) -> ConvShape | None:

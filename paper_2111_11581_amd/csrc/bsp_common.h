@@ -119,7 +119,8 @@ struct TileHeader {
 struct Plan {
     // scheme
     int R, C, bh, bw, reg, rate, dt, esize;
-    int nbr, nbc;                 // number of block-rows / block-cols
+    int nbr, nbc;                 // number of block-rows / block-cols (PUNCHED: channel blocks)
+    int khw;                      // kernel locations per input channel (PUNCHED), else 1
     int bh_eff, bw_eff;           // block size with 0 resolved to the extent
     // lists
     int shared;                   // 1 = identity list shared by all m-tiles

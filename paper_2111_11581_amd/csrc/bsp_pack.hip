@@ -67,6 +67,32 @@ __global__ void k_validate_blocks(const uint8_t *__restrict__ mask, int R, int C
     if (threadIdx.x == 0 && cnt != (ng + rate - 1) / rate) atomicOr(flag, 1);
 }
 
+// Block-punched structure (Sec. 4.1.2): in block (filters [r0, r1) x channels
+// [c0, c1)) every kernel keeps the locations of the block's first kernel, and that
+// kernel keeps exactly k of its khw locations.
+__global__ void k_validate_punched(const uint8_t *__restrict__ mask, int R, int C, int khw, int bh,
+                                   int bw, int nbc, int k, int *flag) {
+    const int b = blockIdx.x;
+    const int bi = b / nbc, bj = b - bi * nbc;
+    const int cin = C / khw;
+    const int r0 = bi * bh, r1 = min(R, r0 + bh), c0 = bj * bw, c1 = min(cin, c0 + bw);
+    const int nk = (r1 - r0) * (c1 - c0);   // kernels of the block
+    const uint8_t *ref = mask + (size_t)r0 * C + (size_t)c0 * khw;
+    int bad = 0;
+    for (int e = threadIdx.x; e < nk * khw; e += blockDim.x) {
+        const int kr = e / khw, l = e - kr * khw;
+        const int o = r0 + kr / (c1 - c0), c = c0 + kr % (c1 - c0);
+        const uint8_t v = mask[(size_t)o * C + (size_t)c * khw + l];
+        bad |= (v > 1) | (v != ref[l]);
+    }
+    if (threadIdx.x == 0) {
+        int cnt = 0;
+        for (int l = 0; l < khw; ++l) cnt += ref[l] == 1;
+        bad |= cnt != k;
+    }
+    if (bad) atomicOr(flag, 1);
+}
+
 __global__ void k_validate_all(const uint8_t *__restrict__ mask, size_t n, int need_ones,
                                int *flag, unsigned int *count) {
     int bad = 0;
@@ -367,7 +393,10 @@ bsp_status pack_t(const Plan &p, const E *w, const uint8_t *mask, E *values, int
         return BSP_EDEVICE;
     const size_t n = (size_t)p.R * p.C;
     // 1. validate the block structure
-    if (p.reg == BSP_COL || p.reg == BSP_ROW) {
+    if (p.reg == BSP_PUNCHED) {
+        k_validate_punched<<<p.nbr * p.nbc, 256, 0, st>>>(mask, p.R, p.C, p.khw, p.bh_eff, p.bw_eff, p.nbc,
+                                                         (p.khw + p.rate - 1) / p.rate, flag);
+    } else if (p.reg == BSP_COL || p.reg == BSP_ROW) {
         const int ng = p.reg == BSP_COL ? p.bw_eff : p.bh_eff;
         const int threads = std::min(256, ((ng + 63) / 64) * 64);
         k_validate_blocks<<<p.nbr * p.nbc, threads, 0, st>>>(mask, p.R, p.C, p.bh_eff, p.bw_eff,
@@ -383,7 +412,7 @@ bsp_status pack_t(const Plan &p, const E *w, const uint8_t *mask, E *values, int
         return BSP_EDEVICE;
     if (hflag) return BSP_EMASK;
     // 2. canonical packing
-    if (p.reg == BSP_COL) {
+    if (p.reg == BSP_COL || p.reg == BSP_PUNCHED) {
         k_col_lists<<<p.nbr, 256, 0, st>>>(mask, p.R, p.C, p.bh_eff, p.nbr, p.L, indices, rowptr, flag);
         k_col_values<E><<<grid_for((size_t)p.R * p.L), 256, 0, st>>>(w, indices, values, p.R, p.C,
                                                                      p.L, p.bh_eff);
@@ -437,7 +466,7 @@ hipError_t unpack_t(const Plan &p, const E *values, const int32_t *indices, E *o
         return hipMemcpyAsync(out, values, n * sizeof(E), hipMemcpyDeviceToDevice, st);
     }
     k_fill<E><<<grid_for(n), 256, 0, st>>>(out, n, (E)0);
-    if (p.reg == BSP_COL)
+    if (p.reg == BSP_COL || p.reg == BSP_PUNCHED)
         k_col_unpack<E><<<grid_for((size_t)p.R * p.L), 256, 0, st>>>(values, indices, out, p.R, p.C,
                                                                      p.L, p.bh_eff);
     else

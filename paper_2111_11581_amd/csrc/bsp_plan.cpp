@@ -71,7 +71,7 @@ static void finish_layout(Plan *p, int n_mt, int astep) {
                        p->mt_per_group, p->LP, p->S, p->CH_STRIDE, p->RS, p->LEFT, p->NSLOT,
                        p->CC, p->KH, p->KW, p->is_linear, p->SW, p->NSUB, p->SMAX, p->resident,
                        p->MBT, p->MBG, p->n_mt_pad, p->n_g_pad, p->GE, p->NB, p->pw, p->NGR, p->VS, p->V,
-                       p->rowmap, p->RK, 9};
+                       p->rowmap, p->RK, p->khw, 10};
     p->fingerprint = fnv1a(fpv, (int)(sizeof(fpv) / sizeof(fpv[0])));
 }
 
@@ -219,8 +219,10 @@ bsp_status make_plan(const bsp_scheme *s, const bsp_conv_shape *conv, bsp_dtype 
     if (!s || !p) return BSP_EINVAL;
     std::memset(p, 0, sizeof(*p));
     if (s->rows <= 0 || s->cols <= 0 || s->bh < 0 || s->bw < 0 || s->rate < 1) return BSP_EINVAL;
-    if (s->regularity < BSP_ROW || s->regularity > BSP_DENSE) return BSP_EINVAL;
+    if (s->regularity < BSP_ROW || s->regularity > BSP_PUNCHED) return BSP_EINVAL;
     if (wdt != BSP_F32 && wdt != BSP_BF16) return BSP_EINVAL;
+    const int khw = s->regularity == BSP_PUNCHED ? std::max(s->khw, 1) : 1;
+    if (s->regularity == BSP_PUNCHED && (s->khw < 0 || s->cols % khw != 0)) return BSP_EINVAL;
     p->R = s->rows;
     p->C = s->cols;
     p->bh = s->bh;
@@ -229,13 +231,29 @@ bsp_status make_plan(const bsp_scheme *s, const bsp_conv_shape *conv, bsp_dtype 
     p->rate = s->rate;
     p->dt = wdt;
     p->esize = wdt == BSP_F32 ? 4 : 2;
+    p->khw = khw;
     p->bh_eff = (s->bh == 0 || s->bh > p->R) ? p->R : s->bh;
-    p->bw_eff = (s->bw == 0 || s->bw > p->C) ? p->C : s->bw;
+    if (p->reg == BSP_PUNCHED) {   // blocks of bh_eff filters x bw_eff input channels
+        const int cin = p->C / khw;
+        p->bw_eff = (s->bw == 0 || s->bw > cin) ? cin : s->bw;
+        p->nbc = div_up(cin, p->bw_eff);
+    } else {
+        p->bw_eff = (s->bw == 0 || s->bw > p->C) ? p->C : s->bw;
+        p->nbc = div_up(p->C, p->bw_eff);
+    }
     p->nbr = div_up(p->R, p->bh_eff);
-    p->nbc = div_up(p->C, p->bw_eff);
 
     // canonical sizes and list structure
-    if (p->reg == BSP_COL) {
+    if (p->reg == BSP_PUNCHED) {
+        // a block-row keeps ceil(khw / rate) locations of every input channel
+        p->L = (p->C / khw) * kept_count(khw, p->rate);
+        p->n_indices = (int64_t)p->nbr * p->L;
+        p->n_values = (int64_t)p->R * p->L;
+        p->n_rowptr = p->nbr + 1;
+        p->shared = 0;
+        p->n_groups = p->nbr;
+        p->group_rows = p->bh_eff;
+    } else if (p->reg == BSP_COL) {
         const int last_w = p->C - (p->nbc - 1) * p->bw_eff;
         p->L = (p->nbc - 1) * kept_count(p->bw_eff, p->rate) + kept_count(last_w, p->rate);
         p->n_indices = (int64_t)p->nbr * p->L;
@@ -267,7 +285,7 @@ bsp_status make_plan(const bsp_scheme *s, const bsp_conv_shape *conv, bsp_dtype 
             p->group_rows = (int)p->n_indices;
         }
     }
-    p->RK = p->reg == BSP_COL ? p->R : p->group_rows;
+    p->RK = p->shared ? p->group_rows : p->R;
     p->mt_per_group = div_up(p->group_rows, kMT);
     p->LP = div_up(p->L, kKS) * kKS;
     p->S = p->LP / kKS;
@@ -281,6 +299,7 @@ bsp_status make_plan(const bsp_scheme *s, const bsp_conv_shape *conv, bsp_dtype 
             c.stride_w <= 0 || c.pad_h < 0 || c.pad_w < 0)
             return BSP_EINVAL;
         if ((int64_t)c.cin * c.kh * c.kw != p->C) return BSP_EINVAL;
+        if (p->reg == BSP_PUNCHED && c.kh * c.kw != p->khw) return BSP_EINVAL;
         p->is_linear = 0;
         p->Cin = c.cin; p->H = c.h; p->W = c.w; p->KH = c.kh; p->KW = c.kw;
         p->SH = c.stride_h; p->SW = c.stride_w; p->PH = c.pad_h; p->PW = c.pad_w;
@@ -340,11 +359,13 @@ bsp_status make_plan(const bsp_scheme *s, const bsp_conv_shape *conv, bsp_dtype 
     // must hold at least that many.  Identity lists: 32 consecutive columns.  Column
     // blocks keep the same count in every block, so a step covers a known number of
     // blocks; whole-width blocks are data dependent (twice the mean spacing is used).
+    // Block-punched lists keep the same number of locations of every channel.
     int span_req;
     {
         const int khw = p->KH * p->KW;
         int64_t cols;
         if (p->shared) cols = kKS;
+        else if (p->reg == BSP_PUNCHED) cols = (int64_t)div_up(kKS, kept_count(p->khw, p->rate)) * khw;
         else if (p->nbc > 1) cols = (int64_t)(div_up(kKS, kept_count(p->bw_eff, p->rate)) + 1) * p->bw_eff;
         else cols = (int64_t)2 * kKS * p->rate;
         span_req = (int)std::min<int64_t>(p->Cin, cols / khw + 2);
@@ -354,6 +375,7 @@ bsp_status make_plan(const bsp_scheme *s, const bsp_conv_shape *conv, bsp_dtype 
     {
         const int khw = p->KH * p->KW;
         if (p->shared) step_ch = (double)kKS / khw;
+        else if (p->reg == BSP_PUNCHED) step_ch = (double)kKS / kept_count(p->khw, p->rate);
         else if (p->nbc > 1) step_ch = (double)kKS * p->bw_eff / kept_count(p->bw_eff, p->rate) / khw;
         else step_ch = (double)kKS * p->rate / khw;
     }

@@ -9,7 +9,11 @@
 // index).  Unstructured pruning (Sec. 2.1.1) keeps the ceil(R*C/rate) largest |w| of
 // the layer: a most-significant-digit radix select over the bit patterns of |w|
 // (order preserving for non-negative floats) finds the threshold, and entries equal
-// to it are admitted in flat-index order.
+// to it are admitted in flat-index order.  Block-punched pruning (Sec. 4.1.2, Eq. 4):
+// one workgroup per block of filters x input channels scores each kernel location
+// over the block's kernels, in ascending (filter, channel) order, keeps the best
+// ceil(khw / rate) by the same rank count and writes them into every kernel of the
+// block.
 #include <hip/hip_runtime.h>
 
 #include "bsp_kernels.h"
@@ -67,6 +71,47 @@ __global__ void k_prune_blocks(const E *__restrict__ w, uint8_t *__restrict__ ma
             uint8_t *mr = mask + (size_t)(r0 + g) * C;
             for (int q = c0; q < c1; ++q) mr[q] = keep;
         }
+    }
+}
+
+template <typename E>
+__global__ void k_prune_punched(const E *__restrict__ w, uint8_t *__restrict__ mask, int R, int C, int khw,
+                                int bh, int bw, int nbc, int rate) {
+    extern __shared__ double sc[];   // khw scores, then khw keep flags
+    uint8_t *keep = (uint8_t *)(sc + khw);
+    const int b = blockIdx.x;
+    const int bi = b / nbc, bj = b - bi * nbc;
+    const int cin = C / khw;
+    const int r0 = bi * bh, r1 = min(R, r0 + bh), c0 = bj * bw, c1 = min(cin, c0 + bw);
+    const int k = (khw + rate - 1) / rate;
+    for (int l = threadIdx.x; l < khw; l += blockDim.x) {
+        double s = 0.0;
+        for (int o = r0; o < r1; ++o) {
+            const size_t base = (size_t)o * C + l;
+            for (int c = c0; c < c1; ++c) {
+                const double v = ld_f64(w, base + (size_t)c * khw);
+                s = fma(v, v, s);
+            }
+        }
+        sc[l] = s;
+    }
+    __syncthreads();
+    for (int l = threadIdx.x; l < khw; l += blockDim.x) {
+        const double s = sc[l];
+        int rank = 0;
+        for (int h = 0; h < khw; ++h) {
+            const double t = sc[h];
+            rank += (t > s) || (t == s && h < l);
+        }
+        keep[l] = rank < k ? 1 : 0;
+    }
+    __syncthreads();
+    const int nc = c1 - c0;
+    const int n = (r1 - r0) * nc * khw;
+    for (int e = threadIdx.x; e < n; e += blockDim.x) {
+        const int kr = e / khw, l = e - kr * khw;
+        const int o = r0 + kr / nc, c = c0 + kr % nc;
+        mask[(size_t)o * C + (size_t)c * khw + l] = keep[l];
     }
 }
 
@@ -227,6 +272,17 @@ hipError_t launch_prune(const Plan &p, const void *w, uint8_t *mask, hipStream_t
     if (p.reg == BSP_UNSTRUCTURED) {
         return p.dt == BSP_F32 ? prune_unstructured(p, (const float *)w, mask, st)
                                : prune_unstructured(p, (const uint16_t *)w, mask, st);
+    }
+    if (p.reg == BSP_PUNCHED) {
+        const size_t lds = (sizeof(double) + 1) * (size_t)p.khw;
+        const int blocks = p.nbr * p.nbc;
+        if (p.dt == BSP_F32)
+            k_prune_punched<float><<<blocks, 256, lds, st>>>((const float *)w, mask, p.R, p.C, p.khw, p.bh_eff,
+                                                             p.bw_eff, p.nbc, p.rate);
+        else
+            k_prune_punched<uint16_t><<<blocks, 256, lds, st>>>((const uint16_t *)w, mask, p.R, p.C, p.khw,
+                                                                p.bh_eff, p.bw_eff, p.nbc, p.rate);
+        return hipGetLastError();
     }
     const int col = p.reg == BSP_COL;
     const int ng_max = col ? p.bw_eff : p.bh_eff;

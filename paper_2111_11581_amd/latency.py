@@ -179,7 +179,7 @@ def measure(settings, reps: int = 10, rounds: int = 10, seed: int = 1234, device
         wd = (torch.randn(rows, cols, generator=gen, device=dev) * math.sqrt(2.0 / cols)).to(torch.bfloat16)
         x = torch.randn(s.batch, s.cin, s.h, s.w, generator=gen, device=dev).to(torch.bfloat16)
         y = torch.empty(s.batch, s.cout, s.ho, s.wo, dtype=torch.bfloat16, device=dev)
-        scheme = Scheme(rows, cols, s.bh, s.bw, s.regularity, s.rate)
+        scheme = Scheme(rows, cols, s.bh, s.bw, s.regularity, s.rate, s.kh * s.kw)
         conv = ConvShape(s.batch, s.cin, s.h, s.w, s.kh, s.kw, s.stride, s.stride, s.pad, s.pad)
         p = PackedLayer(scheme, BF16, wd, conv=conv)
         p.conv2d(x, y, s.batch, BF16)

@@ -25,7 +25,8 @@ class PackedLayer:
     def __init__(self, scheme, wdt: int, w: torch.Tensor, conv=None, mask: torch.Tensor | None = None,
                  stream=None):
         self.scheme = scheme if isinstance(scheme, Scheme) else Scheme(
-            scheme.rows, scheme.cols, scheme.bh, scheme.bw, scheme.regularity, scheme.rate)
+            scheme.rows, scheme.cols, scheme.bh, scheme.bw, scheme.regularity, scheme.rate,
+            getattr(scheme, "khw", 1))
         self.wdt = wdt
         self.conv = conv if (conv is None or isinstance(conv, ConvShape)) else ConvShape(*conv)
         dev = w.device

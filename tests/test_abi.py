@@ -43,10 +43,10 @@ def test_status_strings_and_version(bsp):
     assert bsp.bsp_version() == 100
 
 
-def _sizes_from_oracle(R, C, bh, bw, reg, rate):
+def _sizes_from_oracle(R, C, bh, bw, reg, rate, khw=1):
     from oracle import prune as OP
     w = np.random.default_rng(R + C).standard_normal((R, C))
-    m = OP.prune_mask(w, bh, bw, reg, rate)
+    m = OP.prune_mask(w, bh, bw, reg, rate, khw=khw)
     pk = OP.pack(w.astype(np.float32), m, bh, bw, reg, rate)
     return pk["values"].size, pk["indices"].size, pk["rowptr"].size
 
@@ -60,6 +60,28 @@ def test_packed_sizes_match_oracle_packing(bsp, R, C, bh, bw, reg, rate):
     nv, ni, nr, nb = bsp.bsp_packed_sizes(s, None, bsp.BF16)
     assert (nv, ni, nr) == _sizes_from_oracle(R, C, bh, bw, reg, rate)
     assert nb > 256
+
+
+@pytest.mark.parametrize("R,cin,khw,bh,bw,rate", [
+    (64, 64, 9, 16, 8, 2), (37, 20, 9, 8, 0, 3), (48, 12, 25, 0, 5, 4), (32, 32, 4, 4, 4, 2), (20, 7, 9, 3, 2, 9)])
+def test_packed_sizes_match_oracle_packing_block_punched(bsp, R, cin, khw, bh, bw, rate):
+    s = bsp.Scheme(R, cin * khw, bh, bw, bsp.PUNCHED, rate, khw)
+    nv, ni, nr, nb = bsp.bsp_packed_sizes(s, None, bsp.BF16)
+    assert (nv, ni, nr) == _sizes_from_oracle(R, cin * khw, bh, bw, bsp.PUNCHED, rate, khw)
+    k = int(np.sqrt(khw))
+    conv = bsp.ConvShape(1, cin, 12, 12, k, k, 1, 1, k // 2, k // 2)
+    assert bsp.bsp_packed_sizes(s, conv, bsp.BF16)[:3] == (nv, ni, nr)
+
+
+def test_block_punched_argument_errors(bsp):
+    L = bsp.lib()
+    out = [ctypes.c_int64() for _ in range(4)]
+    EINVAL = -1
+    bad = bsp.Scheme(64, 64 * 9 + 1, 16, 8, bsp.PUNCHED, 2, 9)      # columns not Cin * khw
+    assert L.bsp_packed_sizes(ctypes.byref(bad), None, 1, *[ctypes.byref(o) for o in out]) == EINVAL
+    s = bsp.Scheme(64, 64 * 9, 16, 8, bsp.PUNCHED, 2, 9)
+    conv = bsp.ConvShape(1, 144, 12, 12, 2, 2, 1, 1, 0, 0)           # 144 x 2 x 2 columns, khw 4 != 9
+    assert L.bsp_packed_sizes(ctypes.byref(s), ctypes.byref(conv), 1, *[ctypes.byref(o) for o in out]) == EINVAL
 
 
 def test_argument_errors_are_reported_before_any_launch(bsp):

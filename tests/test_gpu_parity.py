@@ -7,7 +7,8 @@ import numpy as np
 import pytest
 
 from oracle import prune as OP
-from synthetic import workload, draw, draw_layer, seed_for, ConvLayer, LinearLayer, ROW, COL, UNSTRUCTURED, DENSE
+from synthetic import (workload, draw, draw_layer, seed_for, ConvLayer, LinearLayer, ROW, COL, UNSTRUCTURED, DENSE,
+                       PUNCHED)
 from tests.helpers import DT, to_dev, from_dev, as_f64, rel_l2, oracle_mask, oracle_conv, oracle_linear, out_to_f64
 
 pytestmark = pytest.mark.gpu
@@ -82,6 +83,48 @@ def test_prune_and_pack_bit_exact(B, i):
     assert np.array_equal(back.view(np.uint8), expect.view(np.uint8))
 
 
+PUNCHED_MATS = [  # name, R, cin, khw, bh (filters), bw (channels), rate, dtype, dist
+    ("3x3 16x8 r2", 64, 64, 9, 16, 8, 2, "bf16", ("normal", 0, 0.05)),
+    ("3x3 ragged 8xwhole r3 f32", 37, 20, 9, 8, 0, 3, "f32", ("normal", 0, 1.0)),
+    ("c5 3x3 whole r4", 256, 256, 9, 0, 0, 4, "bf16", ("normal", 0, 0.03)),
+    ("5x5 whole x5 r4", 48, 12, 25, 0, 5, 4, "bf16", ("normal", 0, 0.1)),
+    ("7x7 4x1 r16", 16, 3, 49, 4, 1, 16, "bf16", ("normal", 0, 0.1)),
+    ("ties 3x3 16x4 r3", 48, 16, 9, 16, 4, 3, "bf16", ("ties",)),
+]
+
+
+@pytest.mark.parametrize("i", range(len(PUNCHED_MATS)), ids=[m[0] for m in PUNCHED_MATS])
+def test_punched_prune_and_pack_bit_exact(B, i):
+    name, R, cin, khw, bh, bw, rate, dtype, dist = PUNCHED_MATS[i]
+    C = cin * khw
+    w = _mat(60 + i, R, C, dtype, dist)
+    scheme = B.Scheme(R, C, bh, bw, PUNCHED, rate, khw)
+    layer = _layers().PackedLayer(scheme, DT[dtype], to_dev(w, dtype))
+    m_ref = oracle_mask(w, dtype, scheme)
+    m_gpu = layer.mask.cpu().numpy().reshape(R, C)
+    assert np.array_equal(m_gpu, m_ref), f"{name}: {int((m_gpu != m_ref).sum())} mask entries differ"
+    pk = OP.pack(w, m_ref, bh, bw, PUNCHED, rate)
+    vals = from_dev(layer.values[:layer.n_values], dtype)
+    assert np.array_equal(vals.view(np.uint8), np.ascontiguousarray(pk["values"]).view(np.uint8))
+    assert np.array_equal(layer.indices[:layer.n_indices].cpu().numpy(), pk["indices"])
+    assert np.array_equal(layer.rowptr[:layer.n_rowptr].cpu().numpy(), pk["rowptr"])
+    back = from_dev(layer.unpack(), dtype).reshape(R, C)
+    expect = np.where(m_ref == 1, w, np.zeros_like(w))
+    assert np.array_equal(back.view(np.uint8), expect.view(np.uint8))
+
+
+def test_pack_rejects_a_block_punched_mask_off_its_pattern(B):
+    import torch
+    R, cin, khw = 32, 16, 9
+    w = draw(seed_for(9, 51, 1), (R, cin * khw), ("normal", 0, 1), "bf16")
+    scheme = B.Scheme(R, cin * khw, 8, 4, PUNCHED, 3, khw)
+    m = oracle_mask(w, "bf16", scheme).reshape(R, cin, khw)
+    m[3, 5] = np.roll(m[3, 5], 1)            # one kernel with other locations
+    with pytest.raises(B.BspError) as e:
+        _layers().PackedLayer(scheme, B.BF16, to_dev(w, "bf16"), mask=torch.from_numpy(m.reshape(-1)).cuda())
+    assert e.value.status == -4
+
+
 def test_pack_rejects_a_mask_without_block_structure(B):
     import torch
     R, C = 64, 256
@@ -126,6 +169,13 @@ CONV_CASES = [
     _conv_case("3x3 row whole r16 relu", 1, 32, 10, 10, 64, 3, 1, 1, 0, 0, ROW, 16, relu=True),
     _conv_case("f32 3x3 row whole r4 bias", 1, 16, 12, 12, 40, 3, 1, 1, 0, 0, ROW, 4, dtype="f32", out="f32",
                bias=True),
+    # block-punched (Sec. 4.1.2): bh filters x bw input channels, kernel locations removed per block
+    _conv_case("3x3 punched 16x8 r3", 2, 64, 12, 12, 64, 3, 1, 1, 16, 8, PUNCHED, 3),
+    _conv_case("3x3 punched whole r4 s2", 2, 32, 15, 15, 48, 3, 2, 1, 0, 0, PUNCHED, 4),
+    _conv_case("5x5 punched 8x4 r5 relu bias", 1, 20, 11, 11, 24, 5, 1, 2, 8, 4, PUNCHED, 5, relu=True, bias=True),
+    _conv_case("3x3 punched 16x1 r9 ragged", 3, 24, 9, 13, 40, 3, 1, 1, 16, 1, PUNCHED, 9),
+    _conv_case("f32 3x3 punched 4x4 r2", 1, 16, 10, 10, 32, 3, 1, 1, 4, 4, PUNCHED, 2, dtype="f32", out="f32"),
+    _conv_case("1x1 punched 32x16 r2 keeps all", 2, 64, 14, 14, 96, 1, 1, 0, 32, 16, PUNCHED, 2),
 ]
 
 
@@ -265,6 +315,22 @@ def test_c5_sweep_layer_full_batch_sampled_images(B, name):
     got = out_to_f64(from_dev(y, "bf16"), "bf16")[[0, layer.n - 1]]
     err = rel_l2(got, ref)
     assert err <= TOL["bf16"], f"{name}: rel-L2 {err:.3e}"
+
+
+@pytest.mark.parametrize("bh,bw,rate", [(16, 16, 4), (0, 0, 8)])
+def test_punched_sweep_layer_full_batch_sampled_images(B, bh, bw, rate):
+    """Block-punched 3x3 256->256 conv at 56x56, batch 64 (the block-size sweep layer);
+    images 0 and 63 checked in full."""
+    layer = ConvLayer(f"punched {bh}x{bw} r{rate}", 64, 256, 56, 56, 256, 3, 3, 1, 1, 1, 1, bh, bw, PUNCHED,
+                      rate, "bf16", ("normal", 0.0, 1.0), ("normal", 0.0, (2.0 / 2304) ** 0.5))
+    d = draw_layer(layer, 5, 70 + rate)
+    L, y = run_conv(B, layer, d["x"], d["w"], "bf16", "bf16")
+    m = L.mask.cpu().numpy().reshape(layer.cout, -1)
+    assert np.array_equal(m, oracle_mask(d["w"], "bf16", layer.scheme))
+    ref = oracle_conv(d["x"], d["w"], m, "bf16", layer, images=[0, layer.n - 1])
+    got = out_to_f64(from_dev(y, "bf16"), "bf16")[[0, layer.n - 1]]
+    err = rel_l2(got, ref)
+    assert err <= TOL["bf16"], f"{layer.name}: rel-L2 {err:.3e}"
 
 
 def test_c1_full(B):
