@@ -25,7 +25,8 @@ import math
 import sys
 from dataclasses import asdict, dataclass
 
-REG_NAMES = {0: "row", 1: "col", 2: "unstructured", 3: "dense"}
+REG_NAMES = {0: "row", 1: "col", 2: "unstructured", 3: "dense", 4: "punched"}
+BLOCK_REGS = (0, 1, 4)   # regularities with a block size (the rule selects among them)
 
 
 @dataclass(frozen=True)
@@ -41,9 +42,9 @@ class Setting:
     stride: int
     pad: int
     batch: int
-    regularity: int   # 0 row, 1 column, 2 unstructured, 3 dense (package constants)
-    bh: int           # block height (0: whole matrix; 1 for unstructured)
-    bw: int           # block width (0: whole matrix; 1 for unstructured)
+    regularity: int   # 0 row, 1 column, 2 unstructured, 3 dense, 4 block-punched (package constants)
+    bh: int           # block height (0: whole matrix; 1 for unstructured; punched: filters)
+    bw: int           # block width (0: whole matrix; 1 for unstructured; punched: input channels)
     rate: int
 
     def key(self) -> str:
@@ -73,7 +74,10 @@ class Setting:
         return self.batch * self.cout * self.ho * self.wo * self.cin * self.kh * self.kw
 
     def area(self) -> int:
-        """Block area in weight elements (whole matrix: rows x cols)."""
+        """Block area in weight elements (whole matrix: rows x cols; a block-punched
+        block of bh filters x bw channels holds bh * bw kernels)."""
+        if self.regularity == 4:
+            return (self.bh or self.cout) * (self.bw or self.cin) * self.kh * self.kw
         rows, cols = self.cout, self.cin * self.kh * self.kw
         return (self.bh or rows) * (self.bw or cols)
 
@@ -146,9 +150,10 @@ def select_block_size(model: LatencyModel, layer: Setting, regularity: int, rate
 # ---- building the model on the GPU ----
 
 def sweep_settings(cin=256, cout=256, h=56, w=56, k=3, batch=64, blocks=(4, 8, 16, 32, 64, 0),
-                   rates=(2, 4, 8, 16), regularities=(0, 1), references=False):
+                   rates=(2, 4, 8, 16), regularities=BLOCK_REGS, references=False):
     """The block-size sweep of one conv layer: square blocks (0 = whole matrix) x
-    regularity x rate (defaults: 3x3 256->256 at 56x56, batch 64).  With
+    regularity x rate (defaults: 3x3 256->256 at 56x56, batch 64; row, column and
+    block-punched, whose blocks are filters x input channels).  With
     ``references``, also unstructured magnitude pruning at each rate and the dense
     layer (reference points; the selection rule does not use them)."""
     st = [Setting(cin, cout, h, w, k, k, 1, k // 2, batch, reg, b, b, r)
@@ -211,9 +216,9 @@ def report(model: LatencyModel, betas=(0.0, 0.1, 0.2, 0.5)) -> str:
         layers.setdefault(s.layer_key(), []).append(s)
     for lk in sorted(layers):
         st = layers[lk]
-        rates = sorted({s.rate for s in st if s.regularity in (0, 1)})
+        rates = sorted({s.rate for s in st if s.regularity in BLOCK_REGS})
         out.append(f"### {lk}\n")
-        for reg in (0, 1):
+        for reg in BLOCK_REGS:
             rs = [s for s in st if s.regularity == reg]
             if not rs:
                 continue
@@ -242,7 +247,7 @@ def report(model: LatencyModel, betas=(0.0, 0.1, 0.2, 0.5)) -> str:
         out.append("rule choice (smallest block within (1 + beta) of whole-matrix blocks, latency per dense MAC):\n")
         out.append("| regularity | rate | " + " | ".join(f"beta {b:g}" for b in betas) + " |")
         out.append("|---|---|" + "---|" * len(betas))
-        for reg in (0, 1):
+        for reg in BLOCK_REGS:
             for r in rates:
                 cells = []
                 for b in betas:
@@ -285,7 +290,7 @@ def _main(argv=None):
     m = LatencyModel.load(a.model)
     layers = {x.layer_key(): x for x in m.settings.values()}
     for lk, layer in sorted(layers.items()):
-        for reg in (0, 1):
+        for reg in BLOCK_REGS:
             for rate in sorted({x.rate for x in m.settings.values() if x.layer_key() == lk}):
                 try:
                     bh, bw = select_block_size(m, layer, reg, rate, a.beta)

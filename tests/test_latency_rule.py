@@ -90,14 +90,15 @@ def test_save_load_roundtrip(tmp_path):
 
 def test_sweep_settings_cover_the_block_size_sweep():
     st = sweep_settings()
-    # 6 block sizes (4..64 and whole) x 2 regularities x 4 rates, one 3x3 256->256 56x56 b64 layer
-    assert len(st) == 48 and len({s.key() for s in st}) == 48
+    # 6 block sizes (4..64 and whole) x 3 regularities (row, column, block-punched) x 4 rates,
+    # one 3x3 256->256 56x56 b64 layer
+    assert len(st) == 72 and len({s.key() for s in st}) == 72
     assert {s.bh for s in st} == {4, 8, 16, 32, 64, 0} and {s.rate for s in st} == {2, 4, 8, 16}
     assert all(s.ho == 56 and s.wo == 56 for s in st)
     assert st[0].macs() == 64 * 256 * 56 * 56 * 256 * 9
     # with the reference points: unstructured at each rate and the dense layer, all distinct
     sr = sweep_settings(references=True)
-    assert len(sr) == 53 and len({s.key() for s in sr}) == 53
+    assert len(sr) == 77 and len({s.key() for s in sr}) == 77
     assert sorted(s.rate for s in sr if s.regularity == 2) == [2, 4, 8, 16]
     assert [s.rate for s in sr if s.regularity == 3] == [1]
 
@@ -105,3 +106,10 @@ def test_sweep_settings_cover_the_block_size_sweep():
 def test_invalid_latency_rejected():
     with pytest.raises(ValueError):
         LatencyModel([(_layer(), 0.0)])
+
+
+def test_block_punched_blocks_are_filters_by_channels():
+    # a punched block of bh filters x bw channels holds bh * bw kernels of kh*kw weights
+    s = Setting(256, 128, 56, 56, 3, 3, 1, 1, 64, 4, 16, 8, 4)
+    assert s.area() == 16 * 8 * 9 and "punched 16x8 r4" in s.key()
+    assert Setting(256, 128, 56, 56, 3, 3, 1, 1, 64, 4, 0, 0, 4).area() == 128 * 256 * 9
