@@ -28,7 +28,11 @@ Readings where the paper is silent (each listed in the design notes):
 * a block size of 0 means the whole extent;
 * block-punched: blocks of bh filters x bw input channels; kept locations per
   block = ceil(kh*kw / rate); the score of a location sums over the block's
-  (filter, channel) pairs in ascending (filter, channel) order.
+  (filter, channel) pairs in ascending (filter, channel) order;
+* per-block kept counts (Sec. 4.1.1: the same or a different number per block;
+  Sec. 4.2: the reweighted method sets a rate per block) are given by the
+  caller as an array over the blocks in row-major order, replacing
+  ceil(extent / rate).
 
 Pins: tests/test_oracle_prune.py (brute-force subset enumeration, invariants,
 ties, ragged edges, scale invariance, hand-derived golden masks).
@@ -84,7 +88,17 @@ def top_k(scores: np.ndarray, k: int) -> np.ndarray:
     return np.sort(order[:k])
 
 
-def punched_mask(wg: np.ndarray, khw: int, bh: int, bw: int, rate: int) -> np.ndarray:
+def _count(counts, i: int, j: int, default: int) -> int:
+    """Kept groups of block (i, j): the caller's count, else the uniform rule."""
+    if counts is None:
+        return default
+    k = int(np.asarray(counts)[i, j])
+    if k < 0:
+        raise ValueError("kept counts must be >= 0")
+    return k
+
+
+def punched_mask(wg: np.ndarray, khw: int, bh: int, bw: int, rate: int, counts=None) -> np.ndarray:
     """Block-punched mask (Sec. 4.1.2, Eq. 4) of a GEMM-form fp64 conv weight
     (R filters x Cin*khw columns, column = c*khw + location).
 
@@ -99,38 +113,46 @@ def punched_mask(wg: np.ndarray, khw: int, bh: int, bw: int, rate: int) -> np.nd
         raise ValueError("columns must be Cin * khw")
     cin = C // khw
     w3 = wg.reshape(R, cin, khw)
-    k = kept_count(khw, rate)
     mask = np.zeros((R, cin, khw), dtype=np.uint8)
-    for r0, r1 in block_ranges(R, bh):
-        for c0, c1 in block_ranges(cin, bw):
+    for i, (r0, r1) in enumerate(block_ranges(R, bh)):
+        for j, (c0, c1) in enumerate(block_ranges(cin, bw)):
+            k = _count(counts, i, j, kept_count(khw, rate))
+            if k > khw:
+                raise ValueError("kept count exceeds the block's groups")
             groups = w3[r0:r1, c0:c1, :].reshape(-1, khw)    # rows: kernels (o, c) in order
             s = np.cumsum(groups * groups, axis=0)[-1]
             mask[r0:r1, c0:c1, top_k(s, k)] = 1
     return mask.reshape(R, C)
 
 
-def prune_mask(wg: np.ndarray, bh: int, bw: int, regularity: int, rate: int, khw: int = 1) -> np.ndarray:
+def prune_mask(wg: np.ndarray, bh: int, bw: int, regularity: int, rate: int, khw: int = 1,
+               counts=None) -> np.ndarray:
     """Mask (uint8, R x C) of the kept weights of a GEMM-form fp64 matrix
-    (khw: kernel locations per input channel, used by block-punched pruning)."""
+    (khw: kernel locations per input channel, used by block-punched pruning;
+    counts: optional kept groups per block, an (n_block_rows, n_block_cols)
+    array, for ROW, COL and PUNCHED)."""
     wg = np.asarray(wg, dtype=np.float64)
     R, C = wg.shape
     mask = np.zeros((R, C), dtype=np.uint8)
     if regularity == PUNCHED:
-        return punched_mask(wg, max(int(khw), 1), bh, bw, rate)
+        return punched_mask(wg, max(int(khw), 1), bh, bw, rate, counts)
     if regularity == DENSE:
         mask[:] = 1
         return mask
     if regularity == UNSTRUCTURED:
         return unstructured_mask(wg, rate)
-    for r0, r1 in block_ranges(R, bh):
-        for c0, c1 in block_ranges(C, bw):
+    for i, (r0, r1) in enumerate(block_ranges(R, bh)):
+        for j, (c0, c1) in enumerate(block_ranges(C, bw)):
             blk = wg[r0:r1, c0:c1]
             s = group_scores(blk, regularity)
+            ng = (c1 - c0) if regularity == COL else (r1 - r0)
+            k = _count(counts, i, j, kept_count(ng, rate))
+            if k > ng:
+                raise ValueError("kept count exceeds the block's groups")
+            keep = top_k(s, k)
             if regularity == COL:
-                keep = top_k(s, kept_count(c1 - c0, rate))
                 mask[r0:r1, c0 + keep] = 1
             else:
-                keep = top_k(s, kept_count(r1 - r0, rate))
                 mask[r0 + keep, c0:c1] = 1
     return mask
 
@@ -147,7 +169,8 @@ def unstructured_mask(wg: np.ndarray, rate: int) -> np.ndarray:
     return m.reshape(R, C)
 
 
-def mask_is_valid(mask: np.ndarray, bh: int, bw: int, regularity: int, rate: int, khw: int = 1) -> bool:
+def mask_is_valid(mask: np.ndarray, bh: int, bw: int, regularity: int, rate: int, khw: int = 1,
+                  counts=None) -> bool:
     """True iff the mask has the block structure of the scheme: every block
     keeps whole columns (COL) or whole rows (ROW), exactly ceil(extent/rate);
     block-punched: the same ceil(khw/rate) locations in every kernel of a block."""
@@ -160,30 +183,30 @@ def mask_is_valid(mask: np.ndarray, bh: int, bw: int, regularity: int, rate: int
         if C % khw:
             return False
         m3 = mask.reshape(R, C // khw, khw)
-        for r0, r1 in block_ranges(R, bh):
-            for c0, c1 in block_ranges(C // khw, bw):
+        for i, (r0, r1) in enumerate(block_ranges(R, bh)):
+            for j, (c0, c1) in enumerate(block_ranges(C // khw, bw)):
                 blk = m3[r0:r1, c0:c1, :]
                 if not np.all(blk == blk[0:1, 0:1, :]):
                     return False
-                if int(blk[0, 0].sum()) != kept_count(khw, rate):
+                if int(blk[0, 0].sum()) != _count(counts, i, j, kept_count(khw, rate)):
                     return False
         return True
     if regularity == DENSE:
         return bool(np.all(mask == 1))
     if regularity == UNSTRUCTURED:
         return int(mask.sum()) == kept_count(R * C, rate)
-    for r0, r1 in block_ranges(R, bh):
-        for c0, c1 in block_ranges(C, bw):
+    for i, (r0, r1) in enumerate(block_ranges(R, bh)):
+        for j, (c0, c1) in enumerate(block_ranges(C, bw)):
             blk = mask[r0:r1, c0:c1]
             if regularity == COL:
                 if not np.all(blk == blk[0:1, :]):
                     return False
-                if int(blk[0].sum()) != kept_count(c1 - c0, rate):
+                if int(blk[0].sum()) != _count(counts, i, j, kept_count(c1 - c0, rate)):
                     return False
             else:
                 if not np.all(blk == blk[:, 0:1]):
                     return False
-                if int(blk[:, 0].sum()) != kept_count(r1 - r0, rate):
+                if int(blk[:, 0].sum()) != _count(counts, i, j, kept_count(r1 - r0, rate)):
                     return False
     return True
 

@@ -336,3 +336,64 @@ def test_punched_pack_unpack_roundtrip_bitwise():
         assert np.all(np.diff(pk["rowptr"]) == L)
         back = P.unpack(pk, R, cin * khw, bh, bw, P.PUNCHED, wb)
         assert np.array_equal(back, np.where(m == 1, wb, 0).astype(wb.dtype))
+
+
+# ---------------------------------------------------- per-block kept counts ---
+# Sec. 4.1.1: a block may keep the same or a different number of rows / columns;
+# the counts (from the reweighted method of Sec. 4.2) are the caller's input.
+
+def _uniform_counts(R, C, bh, bw, reg, rate, khw=1):
+    rr = P.block_ranges(R, bh)
+    if reg == P.PUNCHED:
+        cc = P.block_ranges(C // khw, bw)
+        return np.full((len(rr), len(cc)), P.kept_count(khw, rate), dtype=np.int32)
+    cc = P.block_ranges(C, bw)
+    return np.array([[P.kept_count((c1 - c0) if reg == P.COL else (r1 - r0), rate) for c0, c1 in cc]
+                     for r0, r1 in rr], dtype=np.int32)
+
+
+@pytest.mark.parametrize("R,C,bh,bw,reg,rate,khw", [
+    (37, 53, 8, 16, P.COL, 3, 1), (37, 53, 8, 16, P.ROW, 3, 1), (64, 72, 16, 0, P.COL, 4, 1),
+    (20, 7 * 9, 6, 3, P.PUNCHED, 2, 9), (48, 96, 0, 32, P.ROW, 5, 1)])
+def test_counts_equal_to_the_uniform_rule_give_the_uniform_mask(R, C, bh, bw, reg, rate, khw):
+    w = np.random.default_rng(R * C).standard_normal((R, C))
+    cnt = _uniform_counts(R, C, bh, bw, reg, rate, khw)
+    assert np.array_equal(P.prune_mask(w, bh, bw, reg, rate, khw=khw, counts=cnt),
+                          P.prune_mask(w, bh, bw, reg, rate, khw=khw))
+
+
+@pytest.mark.parametrize("reg", [P.COL, P.ROW])
+def test_counts_brute_force_on_small_integer_blocks(reg):
+    rng = np.random.default_rng(3 + reg)
+    R, C, bh, bw = 6, 8, 3, 4
+    W = rng.integers(-3, 4, size=(R, C)).astype(np.float64)
+    cnt = np.array([[0, 3], [4, 1]], dtype=np.int32) if reg == P.COL else np.array([[2, 0], [3, 1]], np.int32)
+    m = P.prune_mask(W, bh, bw, reg, 2, counts=cnt)
+    assert P.mask_is_valid(m, bh, bw, reg, 2, counts=cnt)
+    for i, (r0, r1) in enumerate(P.block_ranges(R, bh)):
+        for j, (c0, c1) in enumerate(P.block_ranges(C, bw)):
+            blk = W[r0:r1, c0:c1]
+            s = (blk ** 2).sum(axis=0) if reg == P.COL else (blk ** 2).sum(axis=1)
+            k = int(cnt[i, j])
+            best = max(itertools.combinations(range(len(s)), k), key=lambda t: (sum(s[q] for q in t),
+                                                                                [-q for q in t]))
+            sub = m[r0:r1, c0:c1]
+            kept = tuple(np.nonzero(sub[0] if reg == P.COL else sub[:, 0])[0])
+            assert kept == best
+
+
+def test_counts_pack_lengths_and_edge_counts():
+    rng = np.random.default_rng(9)
+    R, C, bh, bw = 40, 96, 16, 32
+    w = rng.standard_normal((R, C)).astype(np.float32)
+    cnt = np.array([[0, 32, 5], [1, 2, 3], [7, 0, 0]], dtype=np.int32)   # ragged last block-row of 8 rows
+    m = P.prune_mask(w.astype(np.float64), bh, bw, P.COL, 4, counts=cnt)
+    assert P.mask_is_valid(m, bh, bw, P.COL, 4, counts=cnt)
+    assert not P.mask_is_valid(m, bh, bw, P.COL, 4)                    # not the uniform rule
+    assert m[0:16, 0:32].sum() == 0 and m[0:16, 32:64].all()           # 0 and all columns kept
+    pk = P.pack(w, m, bh, bw, P.COL, 4)
+    assert np.diff(pk["rowptr"]).tolist() == cnt.sum(axis=1).tolist()
+    back = P.unpack(pk, R, C, bh, bw, P.COL, w)
+    assert np.array_equal(back, np.where(m == 1, w, 0).astype(np.float32))
+    with pytest.raises(ValueError):
+        P.prune_mask(w.astype(np.float64), bh, bw, P.COL, 4, counts=np.full((3, 3), 33))
