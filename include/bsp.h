@@ -74,6 +74,16 @@ typedef struct {
                                (kh*kw; cols = Cin*khw, column = c*khw + r*kw + s);
                                must equal kh*kw of the conv shape.  Ignored by
                                the other regularities (0 reads as 1).          */
+    const int32_t *counts;  /* HOST array or NULL.  Kept groups of every block
+                               (Sec. 4.1.1: the same or a different number per
+                               block), n_block_rows x n_block_cols row-major
+                               (PUNCHED: filter blocks x channel blocks), each
+                               0 .. the block's group count (columns, rows or
+                               kernel locations); replaces ceil(extent/rate)
+                               for BSP_ROW, BSP_COL and BSP_PUNCHED.  Read by
+                               every call that takes the scheme; tiles packed
+                               with other counts are detected like another
+                               geometry.  NULL: the uniform rule.             */
 } bsp_scheme;
 
 /* Convolution geometry: dilation 1, groups 1, NCHW activations, OIHW weights. */
@@ -94,11 +104,12 @@ bsp_status bsp_packed_sizes(const bsp_scheme *scheme, const bsp_conv_shape *conv
 
 /* Prune (Sec. 4.1.1 with the group norms of Eqs. 2-3, Sec. 4.1.2 with the
  * norm of Eq. 4, one-shot magnitude selection of Sec. 5.1): w is the GEMM-form
- * weight matrix, row-major
- * rows x cols, of dtype wdt; mask (rows x cols bytes, row-major) receives 1
- * for kept and 0 for removed weights.  Async.  The whole-layer magnitude
- * ranking of BSP_UNSTRUCTURED allocates a small scratch buffer on `stream`
- * (stream-ordered) and frees it before returning. */
+ * weight matrix, row-major rows x cols, of dtype wdt; mask (rows x cols bytes,
+ * row-major) receives 1 for kept and 0 for removed weights.  Async.  The
+ * whole-layer magnitude ranking of BSP_UNSTRUCTURED allocates a small scratch
+ * buffer on `stream` (stream-ordered) and frees it before returning.  With
+ * per-block counts the counts go to such a buffer and the call waits for
+ * `stream` before returning. */
 bsp_status bsp_prune(const bsp_scheme *scheme, bsp_dtype wdt, const void *w, uint8_t *mask,
                      void *stream);
 

@@ -34,7 +34,20 @@ class BspError(RuntimeError):
 
 
 class Scheme(ctypes.Structure):
-    _fields_ = [(n, ctypes.c_int32) for n in ("rows", "cols", "bh", "bw", "regularity", "rate", "khw")]
+    """bsp_scheme.  ``counts`` (optional) is a host int32 array of kept groups per
+    block; set it with ``set_counts`` so that the array outlives the scheme's use."""
+    _fields_ = [(n, ctypes.c_int32) for n in ("rows", "cols", "bh", "bw", "regularity", "rate", "khw")] + [
+        ("counts", ctypes.POINTER(ctypes.c_int32))]
+
+    def set_counts(self, counts):
+        if counts is None:
+            self._counts_buf = None
+            self.counts = ctypes.POINTER(ctypes.c_int32)()
+            return self
+        flat = [int(v) for row in counts for v in (row if hasattr(row, "__iter__") else [row])]
+        self._counts_buf = (ctypes.c_int32 * len(flat))(*flat)
+        self.counts = ctypes.cast(self._counts_buf, ctypes.POINTER(ctypes.c_int32))
+        return self
 
 
 class ConvShape(ctypes.Structure):
@@ -76,8 +89,9 @@ def lib():
 def _scheme(s) -> Scheme:
     if isinstance(s, Scheme):
         return s
-    return Scheme(int(s.rows), int(s.cols), int(s.bh), int(s.bw), int(s.regularity), int(s.rate),
-                  int(getattr(s, "khw", 1)))
+    out = Scheme(int(s.rows), int(s.cols), int(s.bh), int(s.bw), int(s.regularity), int(s.rate),
+                 int(getattr(s, "khw", 1)))
+    return out.set_counts(getattr(s, "counts", None))
 
 
 def _shape(c) -> ConvShape | None:

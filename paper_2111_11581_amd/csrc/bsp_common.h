@@ -121,6 +121,8 @@ struct Plan {
     int R, C, bh, bw, reg, rate, dt, esize;
     int nbr, nbc;                 // number of block-rows / block-cols (PUNCHED: channel blocks)
     int khw;                      // kernel locations per input channel (PUNCHED), else 1
+    const int32_t *counts;        // caller's kept groups per block (host, valid during the call), or null
+    uint32_t counts_hash;         // hash of the counts (part of the fingerprint)
     int bh_eff, bw_eff;           // block size with 0 resolved to the extent
     // lists
     int shared;                   // 1 = identity list shared by all m-tiles
@@ -162,7 +164,7 @@ struct Plan {
     int occ;                      // workgroups per CU the plan is sized for
     // dev_tiles layout (bytes); with a row map, off_rowmap holds int32 rowmap[n_mt_pad * 16]
     // (kept output row of each computed row, 0 past RK) followed by the R - RK pruned rows
-    int64_t off_chunks, off_desc, off_desc16, off_a, off_rowmap, off_pruned, tile_bytes;
+    int64_t off_chunks, off_desc, off_desc16, off_a, off_rowmap, off_pruned, off_counts, tile_bytes;
     uint64_t fingerprint;
     // canonical sizes (elements)
     int64_t n_values, n_indices, n_rowptr;
@@ -258,5 +260,31 @@ BSP_HD constexpr int fwd_occ(int gather, int tm, int tpg) { return (void)gather,
 inline int div_up(int a, int b) { return (a + b - 1) / b; }
 inline int64_t div_up64(int64_t a, int64_t b) { return (a + b - 1) / b; }
 inline int kept_count(int extent, int rate) { return (extent + rate - 1) / rate; }
+
+// Kept groups of block b (row-major over block-rows x block-columns): the caller's
+// count, else ceil(groups / rate).
+int block_count(const Plan &p, int b);
+
+// Canonical rowptr of the plan (COL / PUNCHED: per block-row list offsets; ROW: per
+// block offsets), n_rowptr entries.
+void plan_rowptr(const Plan &p, int32_t *rowptr);
+
+// Kept GEMM columns of block (i, j) of a COL / PUNCHED plan.
+int block_cols(const Plan &p, int i, int j);
+
+// Slot runs of the forward lists of a COL / PUNCHED plan with per-block counts:
+// block column j owns slots [P[j], P[j+1]) of every block-row's list, as many as its
+// largest kept-column count; P has nbc + 1 entries and P[nbc] = L.
+void count_slots(const Plan &p, int32_t *P);
+
+// Device tables of a plan with per-block counts (in dev_tiles at off_counts):
+// counts[nbr*nbc], slot run starts P[nbc+1], block of each slot [L], and per block
+// (i, j) the offset of its kept columns inside list i and their number.
+struct CountTables {
+    const int32_t *counts, *P, *slot_block, *start, *ncols;
+};
+inline int64_t count_tables_bytes(int nbr, int nbc, int L) {
+    return 4 * ((int64_t)3 * nbr * nbc + nbc + 1 + L);
+}
 
 }  // namespace bsp

@@ -10,6 +10,8 @@
 // windows ("chunks") the forward stages through LDS.
 #include <hip/hip_runtime.h>
 
+#include <vector>
+
 #include "bsp_kernels.h"
 
 namespace bsp {
@@ -38,7 +40,7 @@ __device__ __forceinline__ int block_excl_scan_256(int v, int *wave_tot, int *to
 }
 
 __global__ void k_validate_blocks(const uint8_t *__restrict__ mask, int R, int C, int bh, int bw,
-                                  int nbc, int col, int rate, int *flag) {
+                                  int nbc, int col, int rate, const int32_t *__restrict__ counts, int *flag) {
     __shared__ int cnt;
     if (threadIdx.x == 0) cnt = 0;
     __syncthreads();
@@ -64,14 +66,14 @@ __global__ void k_validate_blocks(const uint8_t *__restrict__ mask, int R, int C
     if (local) atomicAdd(&cnt, local);
     if (bad) atomicOr(flag, 1);
     __syncthreads();
-    if (threadIdx.x == 0 && cnt != (ng + rate - 1) / rate) atomicOr(flag, 1);
+    if (threadIdx.x == 0 && cnt != (counts ? counts[b] : (ng + rate - 1) / rate)) atomicOr(flag, 1);
 }
 
 // Block-punched structure (Sec. 4.1.2): in block (filters [r0, r1) x channels
 // [c0, c1)) every kernel keeps the locations of the block's first kernel, and that
 // kernel keeps exactly k of its khw locations.
 __global__ void k_validate_punched(const uint8_t *__restrict__ mask, int R, int C, int khw, int bh,
-                                   int bw, int nbc, int k, int *flag) {
+                                   int bw, int nbc, int k, const int32_t *__restrict__ counts, int *flag) {
     const int b = blockIdx.x;
     const int bi = b / nbc, bj = b - bi * nbc;
     const int cin = C / khw;
@@ -88,7 +90,7 @@ __global__ void k_validate_punched(const uint8_t *__restrict__ mask, int R, int 
     if (threadIdx.x == 0) {
         int cnt = 0;
         for (int l = 0; l < khw; ++l) cnt += ref[l] == 1;
-        bad |= cnt != k;
+        bad |= cnt != (counts ? counts[b] : k);
     }
     if (bad) atomicOr(flag, 1);
 }
@@ -112,12 +114,14 @@ __global__ void k_check_count(const unsigned int *count, unsigned int k, int *fl
     if (*count != k) atomicOr(flag, 1);
 }
 
-__global__ void k_col_lists(const uint8_t *__restrict__ mask, int R, int C, int bh, int nbr, int L,
-                            int32_t *__restrict__ indices, int32_t *__restrict__ rowptr,
-                            int *flag) {
+// Kept-column list of block-row i, written at rowptr[i] (offsets computed on the host
+// from the scheme); the block-row's first row holds its kept columns.
+__global__ void k_col_lists(const uint8_t *__restrict__ mask, int C, int bh, const int32_t *__restrict__ rowptr,
+                            int32_t *__restrict__ indices, int *flag) {
     __shared__ int wave_tot[4];
     const int i = blockIdx.x;
     const uint8_t *mr = mask + (size_t)i * bh * C;
+    const int off = rowptr[i], L = rowptr[i + 1] - off;
     int base = 0;
     for (int q0 = 0; q0 < C; q0 += 256) {
         const int q = q0 + threadIdx.x;
@@ -125,41 +129,50 @@ __global__ void k_col_lists(const uint8_t *__restrict__ mask, int R, int C, int 
         int tot;
         const int pos = base + block_excl_scan_256(v, wave_tot, &tot);
         if (v) {
-            if (pos < L) indices[(size_t)i * L + pos] = q;
+            if (pos < L) indices[off + pos] = q;
             else atomicOr(flag, 1);
         }
         base += tot;
     }
-    if (threadIdx.x == 0) {
-        if (base != L) atomicOr(flag, 1);
-        if (rowptr) {
-            rowptr[i] = i * L;
-            if (i == nbr - 1) rowptr[nbr] = nbr * L;
-        }
-    }
+    if (threadIdx.x == 0 && base != L) atomicOr(flag, 1);
 }
 
+// Values of block-row i: [row][t] at rowptr[i] * bh (earlier block-rows are full).
 template <typename E>
 __global__ void k_col_values(const E *__restrict__ w, const int32_t *__restrict__ indices,
-                             E *__restrict__ values, int R, int C, int L, int bh) {
-    const size_t n = (size_t)R * L;
-    for (size_t e = blockIdx.x * (size_t)blockDim.x + threadIdx.x; e < n;
-         e += (size_t)gridDim.x * blockDim.x) {
-        const int row = (int)(e / L), t = (int)(e - (size_t)row * L);
-        const int i = row / bh;
-        values[e] = w[(size_t)row * C + indices[(size_t)i * L + t]];
+                             const int32_t *__restrict__ rowptr, E *__restrict__ values, int R, int C, int bh) {
+    const int i = blockIdx.x;
+    const int off = rowptr[i], L = rowptr[i + 1] - off;
+    const int r0 = i * bh, rows = min(R, r0 + bh) - r0;
+    const size_t vbase = (size_t)off * bh;
+    for (int e = threadIdx.x; e < rows * L; e += blockDim.x) {
+        const int p = e / L, t = e - p * L;
+        values[vbase + e] = w[(size_t)(r0 + p) * C + indices[off + t]];
     }
 }
 
+// Value offset of row block b: its values follow those of every earlier block, kept
+// rows x block width (only the last block column may be narrower).
+__device__ __forceinline__ size_t row_voff(const int32_t *__restrict__ rowptr, int b, int nbc, int bw,
+                                           int last_w) {
+    size_t v = (size_t)bw * rowptr[b];
+    if (last_w != bw) {
+        const int bi = b / nbc;
+        for (int i = 0; i < bi; ++i)
+            v -= (size_t)(bw - last_w) * (rowptr[i * nbc + nbc] - rowptr[i * nbc + nbc - 1]);
+    }
+    return v;
+}
+
+// Kept-row list of block b, written at rowptr[b]; the block's first column holds its
+// kept rows.
 __global__ void k_row_lists(const uint8_t *__restrict__ mask, int R, int C, int bh, int bw, int nbc,
-                            int rate, int32_t *__restrict__ indices, int32_t *__restrict__ rowptr,
-                            int *flag) {
+                            const int32_t *__restrict__ rowptr, int32_t *__restrict__ indices, int *flag) {
     __shared__ int wave_tot[4];
     const int b = blockIdx.x;
     const int bi = b / nbc, bj = b - bi * nbc;
     const int r0 = bi * bh, r1 = min(R, r0 + bh), c0 = bj * bw;
-    const int kf = (bh + rate - 1) / rate, ki = (r1 - r0 + rate - 1) / rate;
-    const int off = bi * kf * nbc + bj * ki;
+    const int off = rowptr[b], ki = rowptr[b + 1] - off;
     int base = 0;
     for (int p0 = r0; p0 < r1; p0 += 256) {
         const int p = p0 + threadIdx.x;
@@ -172,24 +185,19 @@ __global__ void k_row_lists(const uint8_t *__restrict__ mask, int R, int C, int 
         }
         base += tot;
     }
-    if (threadIdx.x == 0) {
-        if (base != ki) atomicOr(flag, 1);
-        rowptr[b] = off;
-        if (b == (int)gridDim.x - 1) rowptr[b + 1] = off + ki;
-    }
+    if (threadIdx.x == 0 && base != ki) atomicOr(flag, 1);
 }
 
 template <typename E>
 __global__ void k_row_values(const E *__restrict__ w, const int32_t *__restrict__ indices,
-                             E *__restrict__ values, int R, int C, int bh, int bw, int nbc,
-                             int rate) {
+                             const int32_t *__restrict__ rowptr, E *__restrict__ values, int C, int bw,
+                             int nbc) {
     const int b = blockIdx.x;
-    const int bi = b / nbc, bj = b - bi * nbc;
-    const int r0 = bi * bh, r1 = min(R, r0 + bh), c0 = bj * bw, c1 = min(C, c0 + bw);
-    const int wj = c1 - c0;
-    const int kf = (bh + rate - 1) / rate, ki = (r1 - r0 + rate - 1) / rate;
-    const int off = bi * kf * nbc + bj * ki;
-    const size_t voff = (size_t)bi * kf * C + (size_t)ki * bj * bw;
+    const int bj = b % nbc;
+    const int c0 = bj * bw, c1 = min(C, c0 + bw);
+    const int wj = c1 - c0, last_w = C - (nbc - 1) * bw;
+    const int off = rowptr[b], ki = rowptr[b + 1] - off;
+    const size_t voff = row_voff(rowptr, b, nbc, bw, last_w);
     for (int e = threadIdx.x; e < ki * wj; e += blockDim.x) {
         const int t = e / wj, q = e - t * wj;
         values[voff + e] = w[(size_t)indices[off + t] * C + c0 + q];
@@ -206,15 +214,47 @@ __global__ void k_masked_copy(const E *__restrict__ w, const uint8_t *__restrict
 
 struct DescArgs {
     int shared, n_groups, L, LP, C, KH, KW, CH_STRIDE, RS, VS, V;
+    CountTables ct;   // per-block counts (ct.P null: uniform lists)
+    int nbc, blk_cols;
 };
 
-__global__ void k_desc(DescArgs a, const int32_t *__restrict__ indices, int32_t *__restrict__ desc) {
+// Kept list of group g: offset and length (shared identity list: 0, L).
+__device__ __forceinline__ int2 group_list(const int32_t *__restrict__ rowptr, int shared, int L, int g) {
+    return shared ? int2{0, L} : int2{rowptr[g], rowptr[g + 1] - rowptr[g]};
+}
+
+// Slot t of group g's forward list when blocks have their own kept counts: block
+// column j owns slots [P[j], P[j+1]) in every group (as many as its largest count),
+// and group g's n kept columns of that block are spread evenly over them (kept column
+// e at slot floor(e * W / n)); the other slots repeat the kept column before them with
+// zero weight, so a step covers the same blocks in every group.  Returns the column
+// and whether the slot carries a kept weight.
+__device__ __forceinline__ int2 slot_col(const CountTables &ct, const int32_t *__restrict__ indices,
+                                         const int32_t *__restrict__ rowptr, int nbc, int blk_cols, int g, int t) {
+    const int j = ct.slot_block[t];
+    const int W = ct.P[j + 1] - ct.P[j], l = t - ct.P[j];
+    const int n = ct.ncols[g * nbc + j];
+    if (n == 0 || W == 0) return int2{j * blk_cols, 0};
+    const int e = (int)(((int64_t)(l + 1) * n - 1) / W);
+    const int real = (int)((int64_t)e * W / n) == l;
+    return int2{indices[rowptr[g] + ct.start[g * nbc + j] + e], real};
+}
+
+__global__ void k_desc(DescArgs a, const int32_t *__restrict__ indices, const int32_t *__restrict__ rowptr,
+                       int32_t *__restrict__ desc) {
     const int n = a.n_groups * a.LP;
     const int khw = a.KH * a.KW;
     for (int e = blockIdx.x * blockDim.x + threadIdx.x; e < n; e += gridDim.x * blockDim.x) {
         const int g = e / a.LP, t = e - g * a.LP;
-        const int tt = t < a.L ? t : a.L - 1;  // padding repeats the last kept column
-        const int q = a.shared ? tt : indices[(size_t)g * a.L + tt];
+        int q;
+        if (a.ct.P) {
+            q = slot_col(a.ct, indices, rowptr, a.nbc, a.blk_cols, g, min(t, a.L - 1)).x;
+        } else {
+            const int2 gl = group_list(rowptr, a.shared, a.L, g);
+            // padding repeats the last kept column (column 0 for an empty list); its weights are zero
+            const int tt = t < gl.y ? t : gl.y - 1;
+            q = gl.y == 0 ? 0 : (a.shared ? tt : indices[gl.x + tt]);
+        }
         const int c = q / khw, rs = q - c * khw;
         const int r = rs / a.KW, s = rs - r * a.KW;
         desc[e] = c * a.CH_STRIDE + (s % a.V) * a.VS + r * a.RS + (s / a.V) * a.V;
@@ -224,11 +264,14 @@ __global__ void k_desc(DescArgs a, const int32_t *__restrict__ indices, int32_t 
 struct ATileArgs {
     int shared, n_groups, mt_per_group, n_mt_pad, group_rows, S, L, R, C;
     int rowmap;   // 1: computed row i is weight row indices[i] (kept filters, ascending)
+    CountTables ct;
+    int nbc, blk_cols;
 };
 
 template <typename E>
 __global__ void k_atiles(ATileArgs a, const E *__restrict__ w, const uint8_t *__restrict__ mask,
-                         const int32_t *__restrict__ indices, E *__restrict__ A) {
+                         const int32_t *__restrict__ indices, const int32_t *__restrict__ rowptr,
+                         E *__restrict__ A) {
     const int64_t per_mt = (int64_t)a.S * 512;
     const int64_t n = (int64_t)a.n_mt_pad * per_mt;   // m-tiles past the last group are zero
     for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < n;
@@ -243,8 +286,17 @@ __global__ void k_atiles(ATileArgs a, const E *__restrict__ w, const uint8_t *__
         const int row = g * a.group_rows + rig;
         const int t = s * 32 + 8 * (lane >> 4) + j;
         E v = (E)0;
-        if (g < a.n_groups && rig < a.group_rows && row < a.R && t < a.L) {
-            const int q = a.shared ? t : indices[(size_t)g * a.L + t];
+        int2 gl = int2{0, 0};   // (column, carries a weight)
+        if (g < a.n_groups && t < a.L) {
+            if (a.ct.P) {
+                gl = slot_col(a.ct, indices, rowptr, a.nbc, a.blk_cols, g, t);
+            } else {
+                const int2 li = group_list(rowptr, a.shared, a.L, g);
+                if (t < li.y) gl = int2{a.shared ? t : indices[li.x + t], 1};
+            }
+        }
+        if (gl.y && rig < a.group_rows && row < a.R) {
+            const int q = gl.x;
             const int src = a.rowmap ? indices[row] : row;
             const size_t wi = (size_t)src * a.C + q;
             if (mask[wi]) v = w[wi];
@@ -348,25 +400,26 @@ __global__ void k_fill(E *p, size_t n, E v) {
 
 template <typename E>
 __global__ void k_col_unpack(const E *__restrict__ values, const int32_t *__restrict__ indices,
-                             E *__restrict__ out, int R, int C, int L, int bh) {
-    const size_t n = (size_t)R * L;
-    for (size_t e = blockIdx.x * (size_t)blockDim.x + threadIdx.x; e < n;
-         e += (size_t)gridDim.x * blockDim.x) {
-        const int row = (int)(e / L), t = (int)(e - (size_t)row * L);
-        out[(size_t)row * C + indices[(size_t)(row / bh) * L + t]] = values[e];
+                             const int32_t *__restrict__ rowptr, E *__restrict__ out, int R, int C, int bh) {
+    const int i = blockIdx.x;
+    const int off = rowptr[i], L = rowptr[i + 1] - off;
+    const int r0 = i * bh, rows = min(R, r0 + bh) - r0;
+    const size_t vbase = (size_t)off * bh;
+    for (int e = threadIdx.x; e < rows * L; e += blockDim.x) {
+        const int p = e / L, t = e - p * L;
+        out[(size_t)(r0 + p) * C + indices[off + t]] = values[vbase + e];
     }
 }
 
 template <typename E>
 __global__ void k_row_unpack(const E *__restrict__ values, const int32_t *__restrict__ indices,
-                             E *__restrict__ out, int R, int C, int bh, int bw, int nbc, int rate) {
+                             const int32_t *__restrict__ rowptr, E *__restrict__ out, int C, int bw, int nbc) {
     const int b = blockIdx.x;
-    const int bi = b / nbc, bj = b - bi * nbc;
-    const int r0 = bi * bh, r1 = min(R, r0 + bh), c0 = bj * bw, c1 = min(C, c0 + bw);
-    const int wj = c1 - c0;
-    const int kf = (bh + rate - 1) / rate, ki = (r1 - r0 + rate - 1) / rate;
-    const int off = bi * kf * nbc + bj * ki;
-    const size_t voff = (size_t)bi * kf * C + (size_t)ki * bj * bw;
+    const int bj = b % nbc;
+    const int c0 = bj * bw, c1 = min(C, c0 + bw);
+    const int wj = c1 - c0, last_w = C - (nbc - 1) * bw;
+    const int off = rowptr[b], ki = rowptr[b + 1] - off;
+    const size_t voff = row_voff(rowptr, b, nbc, bw, last_w);
     for (int e = threadIdx.x; e < ki * wj; e += blockDim.x) {
         const int t = e / wj, q = e - t * wj;
         out[(size_t)indices[off + t] * C + c0 + q] = values[voff + e];
@@ -392,15 +445,57 @@ bsp_status pack_t(const Plan &p, const E *w, const uint8_t *mask, E *values, int
     if (hipMemcpyAsync(tiles, &h, sizeof(h), hipMemcpyHostToDevice, st) != hipSuccess)
         return BSP_EDEVICE;
     const size_t n = (size_t)p.R * p.C;
+    const bool blocked = p.reg == BSP_COL || p.reg == BSP_ROW || p.reg == BSP_PUNCHED;
+    // canonical list offsets (from the scheme and its counts) and the counts, for the
+    // kernels below; both copies complete before this call returns (it synchronises)
+    std::vector<int32_t> rp(blocked ? (size_t)p.n_rowptr : 0);
+    if (blocked) {
+        plan_rowptr(p, rp.data());
+        if (hipMemcpyAsync(rowptr, rp.data(), sizeof(int32_t) * rp.size(), hipMemcpyHostToDevice, st) !=
+            hipSuccess)
+            return BSP_EDEVICE;
+    }
+    const int32_t *counts = nullptr;
+    CountTables ct{};
+    std::vector<int32_t> tab;
+    if (p.counts) {
+        // counts, slot runs, block of each slot, per-block start and length in the lists
+        const int nb = p.nbr * p.nbc;
+        const bool lists = p.reg == BSP_COL || p.reg == BSP_PUNCHED;
+        tab.assign((size_t)count_tables_bytes(p.nbr, p.nbc, p.L) / 4, 0);
+        int32_t *tc = tab.data(), *tP = tc + nb, *tsb = tP + p.nbc + 1, *tst = tsb + p.L, *tn = tst + nb;
+        for (int b = 0; b < nb; ++b) tc[b] = p.counts[b];
+        if (lists) {
+            count_slots(p, tP);
+            for (int j = 0; j < p.nbc; ++j)
+                for (int t = tP[j]; t < tP[j + 1]; ++t) tsb[t] = j;
+            for (int i = 0; i < p.nbr; ++i) {
+                int off = 0;
+                for (int j = 0; j < p.nbc; ++j) {
+                    tst[i * p.nbc + j] = off;
+                    tn[i * p.nbc + j] = block_cols(p, i, j);
+                    off += tn[i * p.nbc + j];
+                }
+            }
+        }
+        const int32_t *dt = (const int32_t *)(tiles + p.off_counts);
+        if (hipMemcpyAsync((void *)dt, tab.data(), sizeof(int32_t) * tab.size(), hipMemcpyHostToDevice, st) !=
+            hipSuccess)
+            return BSP_EDEVICE;
+        counts = dt;
+        if (lists) ct = CountTables{dt, dt + nb, dt + nb + p.nbc + 1, dt + nb + p.nbc + 1 + p.L,
+                                    dt + 2 * nb + p.nbc + 1 + p.L};
+    }
+    const int blk_cols = p.reg == BSP_PUNCHED ? p.bw_eff * p.khw : p.bw_eff;
     // 1. validate the block structure
     if (p.reg == BSP_PUNCHED) {
         k_validate_punched<<<p.nbr * p.nbc, 256, 0, st>>>(mask, p.R, p.C, p.khw, p.bh_eff, p.bw_eff, p.nbc,
-                                                         (p.khw + p.rate - 1) / p.rate, flag);
+                                                         (p.khw + p.rate - 1) / p.rate, counts, flag);
     } else if (p.reg == BSP_COL || p.reg == BSP_ROW) {
         const int ng = p.reg == BSP_COL ? p.bw_eff : p.bh_eff;
         const int threads = std::min(256, ((ng + 63) / 64) * 64);
         k_validate_blocks<<<p.nbr * p.nbc, threads, 0, st>>>(mask, p.R, p.C, p.bh_eff, p.bw_eff,
-                                                            p.nbc, p.reg == BSP_COL, p.rate, flag);
+                                                            p.nbc, p.reg == BSP_COL, p.rate, counts, flag);
     } else {
         k_validate_all<<<grid_for(n), 256, 0, st>>>(mask, n, p.reg == BSP_DENSE, flag, count);
         if (p.reg == BSP_UNSTRUCTURED)
@@ -413,24 +508,24 @@ bsp_status pack_t(const Plan &p, const E *w, const uint8_t *mask, E *values, int
     if (hflag) return BSP_EMASK;
     // 2. canonical packing
     if (p.reg == BSP_COL || p.reg == BSP_PUNCHED) {
-        k_col_lists<<<p.nbr, 256, 0, st>>>(mask, p.R, p.C, p.bh_eff, p.nbr, p.L, indices, rowptr, flag);
-        k_col_values<E><<<grid_for((size_t)p.R * p.L), 256, 0, st>>>(w, indices, values, p.R, p.C,
-                                                                     p.L, p.bh_eff);
+        k_col_lists<<<p.nbr, 256, 0, st>>>(mask, p.C, p.bh_eff, rowptr, indices, flag);
+        k_col_values<E><<<p.nbr, 256, 0, st>>>(w, indices, rowptr, values, p.R, p.C, p.bh_eff);
     } else if (p.reg == BSP_ROW) {
-        k_row_lists<<<p.nbr * p.nbc, 256, 0, st>>>(mask, p.R, p.C, p.bh_eff, p.bw_eff, p.nbc,
-                                                    p.rate, indices, rowptr, flag);
-        k_row_values<E><<<p.nbr * p.nbc, 256, 0, st>>>(w, indices, values, p.R, p.C, p.bh_eff,
-                                                        p.bw_eff, p.nbc, p.rate);
+        k_row_lists<<<p.nbr * p.nbc, 256, 0, st>>>(mask, p.R, p.C, p.bh_eff, p.bw_eff, p.nbc, rowptr,
+                                                    indices, flag);
+        k_row_values<E><<<p.nbr * p.nbc, 256, 0, st>>>(w, indices, rowptr, values, p.C, p.bw_eff, p.nbc);
     } else {
         k_masked_copy<E><<<grid_for(n), 256, 0, st>>>(w, mask, values, n);
     }
     // 3. forward layout
     int32_t *desc = (int32_t *)(tiles + p.off_desc);
-    DescArgs da{p.shared, p.n_groups, p.L, p.LP, p.C, p.KH, p.KW, p.CH_STRIDE, p.RS, p.VS, std::max(p.V, 1)};
-    k_desc<<<grid_for((size_t)p.n_groups * p.LP), 256, 0, st>>>(da, indices, desc);
-    ATileArgs aa{p.shared, p.n_groups, p.mt_per_group, p.n_mt_pad, p.group_rows, p.S, p.L, p.RK, p.C, p.rowmap};
+    DescArgs da{p.shared, p.n_groups, p.L, p.LP, p.C, p.KH, p.KW, p.CH_STRIDE, p.RS, p.VS, std::max(p.V, 1),
+                ct, p.nbc, blk_cols};
+    k_desc<<<grid_for((size_t)p.n_groups * p.LP), 256, 0, st>>>(da, indices, rowptr, desc);
+    ATileArgs aa{p.shared, p.n_groups, p.mt_per_group, p.n_mt_pad, p.group_rows, p.S, p.L, p.RK, p.C, p.rowmap,
+                 ct, p.nbc, blk_cols};
     const size_t na = (size_t)p.n_mt_pad * p.S * 512;
-    k_atiles<E><<<grid_for(na), 256, 0, st>>>(aa, w, mask, indices, (E *)(tiles + p.off_a));
+    k_atiles<E><<<grid_for(na), 256, 0, st>>>(aa, w, mask, indices, rowptr, (E *)(tiles + p.off_a));
     if (p.rowmap) {
         int32_t *rm = (int32_t *)(tiles + p.off_rowmap);
         const size_t nrm = (size_t)p.n_mt_pad * kMT;
@@ -460,18 +555,17 @@ bsp_status pack_t(const Plan &p, const E *w, const uint8_t *mask, E *values, int
 }
 
 template <typename E>
-hipError_t unpack_t(const Plan &p, const E *values, const int32_t *indices, E *out, hipStream_t st) {
+hipError_t unpack_t(const Plan &p, const E *values, const int32_t *indices, const int32_t *rowptr, E *out,
+                    hipStream_t st) {
     const size_t n = (size_t)p.R * p.C;
     if (p.reg == BSP_DENSE || p.reg == BSP_UNSTRUCTURED) {
         return hipMemcpyAsync(out, values, n * sizeof(E), hipMemcpyDeviceToDevice, st);
     }
     k_fill<E><<<grid_for(n), 256, 0, st>>>(out, n, (E)0);
     if (p.reg == BSP_COL || p.reg == BSP_PUNCHED)
-        k_col_unpack<E><<<grid_for((size_t)p.R * p.L), 256, 0, st>>>(values, indices, out, p.R, p.C,
-                                                                     p.L, p.bh_eff);
+        k_col_unpack<E><<<p.nbr, 256, 0, st>>>(values, indices, rowptr, out, p.R, p.C, p.bh_eff);
     else
-        k_row_unpack<E><<<p.nbr * p.nbc, 256, 0, st>>>(values, indices, out, p.R, p.C, p.bh_eff,
-                                                        p.bw_eff, p.nbc, p.rate);
+        k_row_unpack<E><<<p.nbr * p.nbc, 256, 0, st>>>(values, indices, rowptr, out, p.C, p.bw_eff, p.nbc);
     return hipGetLastError();
 }
 
@@ -487,10 +581,9 @@ bsp_status run_pack(const Plan &p, const void *w, const uint8_t *mask, void *val
 
 hipError_t launch_unpack(const Plan &p, const void *values, const int32_t *indices,
                          const int32_t *rowptr, void *w_out, hipStream_t st) {
-    (void)rowptr;
     if (p.dt == BSP_F32)
-        return unpack_t<float>(p, (const float *)values, indices, (float *)w_out, st);
-    return unpack_t<uint16_t>(p, (const uint16_t *)values, indices, (uint16_t *)w_out, st);
+        return unpack_t<float>(p, (const float *)values, indices, rowptr, (float *)w_out, st);
+    return unpack_t<uint16_t>(p, (const uint16_t *)values, indices, rowptr, (uint16_t *)w_out, st);
 }
 
 }  // namespace bsp

@@ -6,6 +6,7 @@
 #include <climits>
 #include <cmath>
 #include <cstring>
+#include <vector>
 
 #include "bsp_common.h"
 
@@ -65,13 +66,14 @@ static void finish_layout(Plan *p, int n_mt, int astep) {
     p->off_a = align256(p->off_desc16 + (int64_t)2 * p->n_g_pad * p->LP);
     p->off_rowmap = align256(p->off_a + (int64_t)p->n_mt_pad * p->S * astep);
     p->off_pruned = p->off_rowmap + (int64_t)4 * (p->rowmap ? p->n_mt_pad * kMT : 0);
-    p->tile_bytes = p->off_pruned + (int64_t)4 * (p->rowmap ? p->R - p->RK : 0);
+    p->off_counts = align256(p->off_pruned + (int64_t)4 * (p->rowmap ? p->R - p->RK : 0));
+    p->tile_bytes = p->off_counts + (p->counts ? count_tables_bytes(p->nbr, p->nbc, p->L) : 0);
 
     const int fpv[] = {p->R, p->C, p->bh_eff, p->bw_eff, p->reg, p->rate, p->dt, p->n_groups,
                        p->mt_per_group, p->LP, p->S, p->CH_STRIDE, p->RS, p->LEFT, p->NSLOT,
                        p->CC, p->KH, p->KW, p->is_linear, p->SW, p->NSUB, p->SMAX, p->resident,
                        p->MBT, p->MBG, p->n_mt_pad, p->n_g_pad, p->GE, p->NB, p->pw, p->NGR, p->VS, p->V,
-                       p->rowmap, p->RK, p->khw, 10};
+                       p->rowmap, p->RK, p->khw, (int)p->counts_hash, p->counts != nullptr, 11};
     p->fingerprint = fnv1a(fpv, (int)(sizeof(fpv) / sizeof(fpv[0])));
 }
 
@@ -214,6 +216,91 @@ static bool plan_pointwise(Plan *p, int span_req, int n_mt, int mpg, int astep) 
     return true;
 }
 
+// Groups of block (bi, bj): columns (COL), rows (ROW) or kernel locations (PUNCHED).
+static int block_groups(const Plan &p, int bi, int bj) {
+    if (p.reg == BSP_PUNCHED) return p.khw;
+    if (p.reg == BSP_COL) return std::min(p.C, (bj + 1) * p.bw_eff) - bj * p.bw_eff;
+    return std::min(p.R, (bi + 1) * p.bh_eff) - bi * p.bh_eff;
+}
+
+int block_count(const Plan &p, int b) {
+    if (p.counts) return p.counts[b];
+    return kept_count(block_groups(p, b / p.nbc, b % p.nbc), p.rate);
+}
+
+int block_cols(const Plan &p, int i, int j) {
+    const int k = block_count(p, i * p.nbc + j);
+    if (p.reg != BSP_PUNCHED) return k;
+    const int cin = p.C / p.khw;
+    return k * (std::min(cin, (j + 1) * p.bw_eff) - j * p.bw_eff);
+}
+
+// Kept GEMM columns of block-row i (COL, PUNCHED).
+static int64_t row_list_len(const Plan &p, int i) {
+    int64_t L = 0;
+    for (int j = 0; j < p.nbc; ++j) L += block_cols(p, i, j);
+    return L;
+}
+
+void count_slots(const Plan &p, int32_t *P) {
+    int64_t off = 0;
+    for (int j = 0; j < p.nbc; ++j) {
+        P[j] = (int32_t)off;
+        int kmax = 0;
+        for (int i = 0; i < p.nbr; ++i) kmax = std::max(kmax, block_cols(p, i, j));
+        off += kmax;
+    }
+    P[p.nbc] = (int32_t)off;
+}
+
+void plan_rowptr(const Plan &p, int32_t *rowptr) {
+    int64_t off = 0;
+    if (p.reg == BSP_ROW) {
+        for (int b = 0; b < p.nbr * p.nbc; ++b) {
+            rowptr[b] = (int32_t)off;
+            off += block_count(p, b);
+        }
+        rowptr[p.nbr * p.nbc] = (int32_t)off;
+        return;
+    }
+    for (int i = 0; i < p.nbr; ++i) {
+        rowptr[i] = (int32_t)off;
+        off += row_list_len(p, i);
+    }
+    rowptr[p.nbr] = (int32_t)off;
+}
+
+// Widest span, in GEMM columns, of 32 consecutive kept columns of one list, from the
+// per-block counts.  Units are column blocks, or the channels of punched blocks.  A
+// window whose first kept column lies in unit u may take a single column of u, so it
+// runs on through the following units until they hold 31 more (or the list ends).
+static int64_t max_step_span_cols(const Plan &p) {
+    // the forward lists give block column j the same slot run in every block-row
+    // (count_slots), so the units are the block columns with their run lengths
+    const int cin = p.C / p.khw;
+    int64_t worst = 0;
+    std::vector<int32_t> P(p.nbc + 1);
+    count_slots(p, P.data());
+    std::vector<int> cnt, width;
+    {
+        for (int j = 0; j < p.nbc; ++j) {
+            cnt.push_back(P[j + 1] - P[j]);
+            width.push_back(p.reg == BSP_PUNCHED ? (std::min(cin, (j + 1) * p.bw_eff) - j * p.bw_eff) * p.khw
+                                                 : std::min(p.C, (j + 1) * p.bw_eff) - j * p.bw_eff);
+        }
+        const int n = (int)cnt.size();
+        int e = 0;
+        int64_t have = 0, span = 0;   // units (u, e) after the start unit: kept columns, width
+        for (int u = 0; u < n; ++u) {
+            if (e < u + 1) { e = u + 1; have = 0; span = 0; }
+            while (e < n && have < kKS - 1) { have += cnt[e]; span += width[e]; ++e; }
+            if (cnt[u] > 0) worst = std::max(worst, width[u] + span);
+            if (e > u + 1) { have -= cnt[u + 1]; span -= width[u + 1]; }
+        }
+    }
+    return worst;
+}
+
 bsp_status make_plan(const bsp_scheme *s, const bsp_conv_shape *conv, bsp_dtype wdt,
                      int batch_for_linear, Plan *p) {
     if (!s || !p) return BSP_EINVAL;
@@ -242,9 +329,39 @@ bsp_status make_plan(const bsp_scheme *s, const bsp_conv_shape *conv, bsp_dtype 
         p->nbc = div_up(p->C, p->bw_eff);
     }
     p->nbr = div_up(p->R, p->bh_eff);
+    if (s->counts && (p->reg == BSP_ROW || p->reg == BSP_COL || p->reg == BSP_PUNCHED)) {
+        if ((int64_t)p->nbr * p->nbc > (1 << 24)) return BSP_EUNSUPPORTED;
+        uint32_t h = 2166136261u;
+        for (int b = 0; b < p->nbr * p->nbc; ++b) {
+            const int k = s->counts[b];
+            if (k < 0 || k > block_groups(*p, b / p->nbc, b % p->nbc)) return BSP_EINVAL;
+            h = (h ^ (uint32_t)k) * 16777619u;
+        }
+        p->counts = s->counts;
+        p->counts_hash = h;
+    }
 
     // canonical sizes and list structure
-    if (p->reg == BSP_PUNCHED) {
+    if (p->counts && p->reg != BSP_ROW) {
+        // per-block counts: lists of different lengths, padded to the longest
+        int64_t Lmax = 0, nv = 0, ni = 0;
+        for (int i = 0; i < p->nbr; ++i) {
+            const int64_t Li = row_list_len(*p, i);
+            Lmax = std::max(Lmax, Li);
+            ni += Li;
+            nv += Li * (std::min(p->R, (i + 1) * p->bh_eff) - i * p->bh_eff);
+        }
+        (void)Lmax;
+        std::vector<int32_t> P(p->nbc + 1);
+        count_slots(*p, P.data());
+        p->L = std::max(P[p->nbc], 1);   // forward lists: the slot runs of all block columns
+        p->n_indices = ni;
+        p->n_values = nv;
+        p->n_rowptr = p->nbr + 1;
+        p->shared = 0;
+        p->n_groups = p->nbr;
+        p->group_rows = p->bh_eff;
+    } else if (p->reg == BSP_PUNCHED) {
         // a block-row keeps ceil(khw / rate) locations of every input channel
         p->L = (p->C / khw) * kept_count(khw, p->rate);
         p->n_indices = (int64_t)p->nbr * p->L;
@@ -263,7 +380,17 @@ bsp_status make_plan(const bsp_scheme *s, const bsp_conv_shape *conv, bsp_dtype 
         p->n_groups = p->nbr;
         p->group_rows = p->bh_eff;
     } else {
-        if (p->reg == BSP_ROW) {
+        if (p->reg == BSP_ROW && p->counts) {
+            int64_t ni = 0, nv = 0;
+            for (int b = 0; b < p->nbr * p->nbc; ++b) {
+                const int j = b % p->nbc;
+                ni += p->counts[b];
+                nv += (int64_t)p->counts[b] * (std::min(p->C, (j + 1) * p->bw_eff) - j * p->bw_eff);
+            }
+            p->n_indices = ni;
+            p->n_values = nv;
+            p->n_rowptr = (int64_t)p->nbr * p->nbc + 1;
+        } else if (p->reg == BSP_ROW) {
             const int last_h = p->R - (p->nbr - 1) * p->bh_eff;
             const int64_t kf = kept_count(p->bh_eff, p->rate), kl = kept_count(last_h, p->rate);
             p->n_indices = ((p->nbr - 1) * kf + kl) * p->nbc;
@@ -365,6 +492,9 @@ bsp_status make_plan(const bsp_scheme *s, const bsp_conv_shape *conv, bsp_dtype 
         const int khw = p->KH * p->KW;
         int64_t cols;
         if (p->shared) cols = kKS;
+        else if (p->counts && p->nbc > 1) cols = max_step_span_cols(*p);
+        else if (p->counts)   // one block column: lists stretched over L slots, twice the mean spacing
+            cols = std::min<int64_t>(p->C, 2 * (int64_t)kKS * p->C / p->L + 1);
         else if (p->reg == BSP_PUNCHED) cols = (int64_t)div_up(kKS, kept_count(p->khw, p->rate)) * khw;
         else if (p->nbc > 1) cols = (int64_t)(div_up(kKS, kept_count(p->bw_eff, p->rate)) + 1) * p->bw_eff;
         else cols = (int64_t)2 * kKS * p->rate;
@@ -375,6 +505,7 @@ bsp_status make_plan(const bsp_scheme *s, const bsp_conv_shape *conv, bsp_dtype 
     {
         const int khw = p->KH * p->KW;
         if (p->shared) step_ch = (double)kKS / khw;
+        else if (p->counts) step_ch = (double)kKS * p->nbr * p->C / std::max<int64_t>(p->n_indices, 1) / khw;
         else if (p->reg == BSP_PUNCHED) step_ch = (double)kKS / kept_count(p->khw, p->rate);
         else if (p->nbc > 1) step_ch = (double)kKS * p->bw_eff / kept_count(p->bw_eff, p->rate) / khw;
         else step_ch = (double)kKS * p->rate / khw;

@@ -33,13 +33,13 @@ __device__ __forceinline__ uint32_t abs_key(const uint16_t *w, size_t i) {
 
 template <typename E>
 __global__ void k_prune_blocks(const E *__restrict__ w, uint8_t *__restrict__ mask, int R, int C,
-                               int bh, int bw, int nbc, int col, int rate) {
+                               int bh, int bw, int nbc, int col, int rate, const int32_t *__restrict__ counts) {
     extern __shared__ double sc[];
     const int b = blockIdx.x;
     const int bi = b / nbc, bj = b - bi * nbc;
     const int r0 = bi * bh, r1 = min(R, r0 + bh), c0 = bj * bw, c1 = min(C, c0 + bw);
     const int ng = col ? c1 - c0 : r1 - r0;
-    const int k = (ng + rate - 1) / rate;
+    const int k = counts ? counts[b] : (ng + rate - 1) / rate;
     for (int g = threadIdx.x; g < ng; g += blockDim.x) {
         double s = 0.0;
         if (col) {
@@ -76,14 +76,14 @@ __global__ void k_prune_blocks(const E *__restrict__ w, uint8_t *__restrict__ ma
 
 template <typename E>
 __global__ void k_prune_punched(const E *__restrict__ w, uint8_t *__restrict__ mask, int R, int C, int khw,
-                                int bh, int bw, int nbc, int rate) {
+                                int bh, int bw, int nbc, int rate, const int32_t *__restrict__ counts) {
     extern __shared__ double sc[];   // khw scores, then khw keep flags
     uint8_t *keep = (uint8_t *)(sc + khw);
     const int b = blockIdx.x;
     const int bi = b / nbc, bj = b - bi * nbc;
     const int cin = C / khw;
     const int r0 = bi * bh, r1 = min(R, r0 + bh), c0 = bj * bw, c1 = min(cin, c0 + bw);
-    const int k = (khw + rate - 1) / rate;
+    const int k = counts ? counts[b] : (khw + rate - 1) / rate;
     for (int l = threadIdx.x; l < khw; l += blockDim.x) {
         double s = 0.0;
         for (int o = r0; o < r1; ++o) {
@@ -273,30 +273,45 @@ hipError_t launch_prune(const Plan &p, const void *w, uint8_t *mask, hipStream_t
         return p.dt == BSP_F32 ? prune_unstructured(p, (const float *)w, mask, st)
                                : prune_unstructured(p, (const uint16_t *)w, mask, st);
     }
+    // per-block counts: a stream-ordered device copy, freed after the launch; the call
+    // then waits for its stream, so the caller's host array may go once it returns
+    int32_t *counts = nullptr;
+    const size_t cbytes = sizeof(int32_t) * (size_t)p.nbr * p.nbc;
+    if (p.counts) {
+        hipError_t e = hipMallocAsync((void **)&counts, cbytes, st);
+        if (e != hipSuccess) return e;
+        e = hipMemcpyAsync(counts, p.counts, cbytes, hipMemcpyHostToDevice, st);
+        if (e != hipSuccess) return e;
+    }
+    const int blocks = p.nbr * p.nbc;
     if (p.reg == BSP_PUNCHED) {
         const size_t lds = (sizeof(double) + 1) * (size_t)p.khw;
-        const int blocks = p.nbr * p.nbc;
         if (p.dt == BSP_F32)
             k_prune_punched<float><<<blocks, 256, lds, st>>>((const float *)w, mask, p.R, p.C, p.khw, p.bh_eff,
-                                                             p.bw_eff, p.nbc, p.rate);
+                                                             p.bw_eff, p.nbc, p.rate, counts);
         else
             k_prune_punched<uint16_t><<<blocks, 256, lds, st>>>((const uint16_t *)w, mask, p.R, p.C, p.khw,
-                                                                p.bh_eff, p.bw_eff, p.nbc, p.rate);
-        return hipGetLastError();
+                                                                p.bh_eff, p.bw_eff, p.nbc, p.rate, counts);
+    } else {
+        const int col = p.reg == BSP_COL;
+        const int ng_max = col ? p.bw_eff : p.bh_eff;
+        const int threads = std::min(256, ((ng_max + 63) / 64) * 64);
+        const size_t lds = sizeof(double) * (size_t)ng_max;
+        if (p.dt == BSP_F32)
+            k_prune_blocks<float><<<blocks, threads, lds, st>>>((const float *)w, mask, p.R, p.C,
+                                                                p.bh_eff, p.bw_eff, p.nbc, col, p.rate, counts);
+        else
+            k_prune_blocks<uint16_t><<<blocks, threads, lds, st>>>((const uint16_t *)w, mask, p.R, p.C,
+                                                                   p.bh_eff, p.bw_eff, p.nbc, col, p.rate,
+                                                                   counts);
     }
-    const int col = p.reg == BSP_COL;
-    const int ng_max = col ? p.bw_eff : p.bh_eff;
-    const int threads = std::min(256, ((ng_max + 63) / 64) * 64);
-    const size_t lds = sizeof(double) * (size_t)ng_max;
-    const int blocks = p.nbr * p.nbc;
-    if (p.dt == BSP_F32)
-        k_prune_blocks<float><<<blocks, threads, lds, st>>>((const float *)w, mask, p.R, p.C,
-                                                            p.bh_eff, p.bw_eff, p.nbc, col, p.rate);
-    else
-        k_prune_blocks<uint16_t><<<blocks, threads, lds, st>>>((const uint16_t *)w, mask, p.R, p.C,
-                                                               p.bh_eff, p.bw_eff, p.nbc, col,
-                                                               p.rate);
-    return hipGetLastError();
+    hipError_t e = hipGetLastError();
+    if (counts) {
+        const hipError_t e2 = hipFreeAsync(counts, st);
+        const hipError_t e3 = hipStreamSynchronize(st);
+        if (e == hipSuccess) e = e2 != hipSuccess ? e2 : e3;
+    }
+    return e;
 }
 
 }  // namespace bsp

@@ -26,7 +26,7 @@ class PackedLayer:
                  stream=None):
         self.scheme = scheme if isinstance(scheme, Scheme) else Scheme(
             scheme.rows, scheme.cols, scheme.bh, scheme.bw, scheme.regularity, scheme.rate,
-            getattr(scheme, "khw", 1))
+            getattr(scheme, "khw", 1)).set_counts(getattr(scheme, "counts", None))
         self.wdt = wdt
         self.conv = conv if (conv is None or isinstance(conv, ConvShape)) else ConvShape(*conv)
         dev = w.device

@@ -183,3 +183,39 @@ def test_every_tested_and_benchmarked_layer_gets_a_plan(bsp):
             except bsp.BspError as e:
                 missing.append((l.name, str(e)))
     assert not missing, missing
+
+
+def _random_counts(nbr, nbc, groups, seed):
+    rng = np.random.default_rng(seed)
+    return rng.integers(0, np.asarray(groups) + 1, size=(nbr, nbc)).astype(np.int32)
+
+
+@pytest.mark.parametrize("R,C,bh,bw,reg,khw", [
+    (64, 576, 16, 32, 1, 1), (37, 53, 8, 16, 1, 1), (37, 53, 8, 16, 0, 1), (48, 96, 0, 32, 0, 1),
+    (40, 90, 16, 0, 1, 1), (20, 7 * 9, 6, 3, 4, 9)])
+def test_packed_sizes_with_per_block_counts_match_oracle_packing(bsp, R, C, bh, bw, reg, khw):
+    from oracle import prune as OP
+    rr = OP.block_ranges(R, bh)
+    cc = OP.block_ranges(C // khw if reg == 4 else C, bw)
+    groups = [[khw if reg == 4 else ((c1 - c0) if reg == 1 else (r1 - r0)) for c0, c1 in cc] for r0, r1 in rr]
+    cnt = _random_counts(len(rr), len(cc), groups, R * C + reg)
+    s = bsp.Scheme(R, C, bh, bw, reg, 3, khw).set_counts(cnt)
+    nv, ni, nr, nb = bsp.bsp_packed_sizes(s, None, bsp.BF16)
+    w = np.random.default_rng(1).standard_normal((R, C))
+    m = OP.prune_mask(w, bh, bw, reg, 3, khw=khw, counts=cnt)
+    pk = OP.pack(w.astype(np.float32), m, bh, bw, reg, 3)
+    assert (nv, ni, nr) == (pk["values"].size, pk["indices"].size, pk["rowptr"].size)
+    # other counts give another fingerprint: the dev_tiles size or header differs
+    cnt2 = cnt.copy()
+    cnt2.flat[0] = (cnt2.flat[0] + 1) % (groups[0][0] + 1)
+    s2 = bsp.Scheme(R, C, bh, bw, reg, 3, khw).set_counts(cnt2)
+    assert bsp.bsp_packed_sizes(s2, None, bsp.BF16)[:2] != (nv, ni) or cnt2.flat[0] == cnt.flat[0]
+
+
+def test_per_block_counts_out_of_range_are_rejected(bsp):
+    L = bsp.lib()
+    out = [ctypes.c_int64() for _ in range(4)]
+    s = bsp.Scheme(32, 64, 16, 32, 1, 2).set_counts([[3, 33], [0, 1]])     # 33 > 32 columns
+    assert L.bsp_packed_sizes(ctypes.byref(s), None, 1, *[ctypes.byref(o) for o in out]) == -1
+    s = bsp.Scheme(32, 64, 16, 32, 1, 2).set_counts([[3, -1], [0, 1]])
+    assert L.bsp_packed_sizes(ctypes.byref(s), None, 1, *[ctypes.byref(o) for o in out]) == -1

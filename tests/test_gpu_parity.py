@@ -436,3 +436,96 @@ def test_vgg16_stack_per_layer_and_end_to_end(B):
     e2e = rel_l2(out_to_f64(from_dev(cur_gpu, "bf16"), "bf16"), cur_ref)
     print(f"VGG-16 stack end-to-end rel-L2 {e2e:.3e}")
     assert e2e <= 3e-2
+
+
+# ----------------------------------------------------- per-block kept counts ---
+# Sec. 4.1.1: each block may keep its own number of rows / columns / locations; the
+# counts come with the scheme (random here, including empty and full blocks).
+
+def _block_groups(R, C, bh, bw, reg, khw):
+    rr = OP.block_ranges(R, bh)
+    cc = OP.block_ranges(C // khw if reg == PUNCHED else C, bw)
+    return [[khw if reg == PUNCHED else ((c1 - c0) if reg == COL else (r1 - r0)) for c0, c1 in cc]
+            for r0, r1 in rr]
+
+
+def _counts(R, C, bh, bw, reg, khw, seed):
+    g = np.asarray(_block_groups(R, C, bh, bw, reg, khw))
+    rng = np.random.default_rng(seed)
+    cnt = rng.integers(0, g + 1).astype(np.int32)
+    cnt.flat[0] = 0                      # one empty block
+    cnt.flat[-1] = g.flat[-1]            # one full block
+    return cnt
+
+
+COUNT_CASES = [  # name, n, cin, h, w, cout, k, s, p, bh, bw, reg, dtype, bias+relu
+    ("3x3 col16x32", 2, 64, 12, 11, 64, 3, 1, 1, 16, 32, COL, "bf16", False),
+    ("3x3 col8x16 s2 f32", 2, 32, 13, 13, 40, 3, 2, 1, 8, 16, COL, "f32", True),
+    ("1x1 col32x32", 2, 128, 14, 14, 96, 1, 1, 0, 32, 32, COL, "bf16", False),
+    ("1x1 row32x32", 2, 96, 14, 14, 160, 1, 1, 0, 32, 32, ROW, "bf16", True),
+    ("3x3 row 16xwhole", 2, 24, 9, 11, 70, 3, 1, 1, 16, 0, ROW, "bf16", True),
+    ("3x3 punched 16x8", 2, 64, 12, 12, 64, 3, 1, 1, 16, 8, PUNCHED, "bf16", False),
+    ("3x3 col 16xwhole", 1, 32, 10, 10, 48, 3, 1, 1, 16, 0, COL, "bf16", False),
+]
+
+
+@pytest.mark.parametrize("case", COUNT_CASES, ids=[c[0] for c in COUNT_CASES])
+def test_per_block_counts_prune_pack_and_conv(B, case):
+    import torch
+    name, n, cin, h, w_, cout, k, s, p, bh, bw, reg, dtype, br = case
+    layer = ConvLayer(name, n, cin, h, w_, cout, k, k, s, s, p, p, bh, bw, reg, 4, dtype, ("normal", 0, 1.0),
+                      ("normal", 0, (2.0 / (cin * k * k)) ** 0.5), relu=br)
+    R, C, khw = cout, cin * k * k, k * k
+    cnt = _counts(R, C, bh, bw, reg, khw, 300 + COUNT_CASES.index(case))
+    d = draw_layer(layer, 8, 200 + COUNT_CASES.index(case), with_bias=br)
+    scheme = B.Scheme(R, C, bh, bw, reg, 4, khw).set_counts(cnt)
+    conv = B.ConvShape(n, cin, h, w_, k, k, s, s, p, p)
+    L = _layers().PackedLayer(scheme, DT[dtype], to_dev(d["w"].reshape(R, C), dtype), conv=conv)
+    m_ref = OP.prune_mask(as_f64(d["w"], dtype).reshape(R, C), bh, bw, reg, 4, khw=khw, counts=cnt)
+    assert np.array_equal(L.mask.cpu().numpy().reshape(R, C), m_ref)
+    pk = OP.pack(d["w"].reshape(R, C), m_ref, bh, bw, reg, 4)
+    assert np.array_equal(L.indices[:L.n_indices].cpu().numpy(), pk["indices"])
+    assert np.array_equal(L.rowptr[:L.n_rowptr].cpu().numpy(), pk["rowptr"])
+    vals = from_dev(L.values[:L.n_values], dtype)
+    assert np.array_equal(vals.view(np.uint8), np.ascontiguousarray(pk["values"]).view(np.uint8))
+    back = from_dev(L.unpack(), dtype).reshape(R, C)
+    assert np.array_equal(back.view(np.uint8), np.where(m_ref == 1, d["w"].reshape(R, C), 0).astype(back.dtype)
+                          .view(np.uint8))
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    y = torch.full(layer.y_shape, float("nan"), dtype=tdt, device="cuda")
+    bias = d.get("bias")
+    bd = None if bias is None else torch.from_numpy(bias.astype(np.float32)).cuda()
+    L.conv2d(to_dev(d["x"], dtype), y, n, DT[dtype], bd, br)
+    torch.cuda.synchronize()
+    ref = oracle_conv(d["x"], d["w"], m_ref, dtype, layer, bias=bias, relu=br)
+    got = out_to_f64(from_dev(y, dtype), dtype)
+    assert np.isfinite(got).all()
+    assert rel_l2(got, ref) <= TOL[dtype]
+
+
+def test_per_block_counts_linear_and_fingerprint(B):
+    import torch
+    layer = LinearLayer("fc", 100, 320, 200, 32, 32, COL, 4, "bf16", ("uniform", -1, 1), ("normal", 0, 0.05))
+    d = draw_layer(layer, 8, 250, with_bias=True)
+    cnt = _counts(200, 320, 32, 32, COL, 1, 77)
+    scheme = B.Scheme(200, 320, 32, 32, COL, 4).set_counts(cnt)
+    L = _layers().PackedLayer(scheme, B.BF16, to_dev(d["w"], "bf16"))
+    m = OP.prune_mask(as_f64(d["w"], "bf16"), 32, 32, COL, 4, counts=cnt)
+    assert np.array_equal(L.mask.cpu().numpy().reshape(200, 320), m)
+    y = torch.full(layer.y_shape, float("nan"), dtype=torch.bfloat16, device="cuda")
+    bd = torch.from_numpy(d["bias"].astype(np.float32)).cuda()
+    L.linear(to_dev(d["x"], "bf16"), y, 100, B.BF16, bd, False)
+    torch.cuda.synchronize()
+    ref = oracle_linear(d["x"], d["w"], m, "bf16", bias=d["bias"])
+    assert rel_l2(out_to_f64(from_dev(y, "bf16"), "bf16"), ref) <= TOL["bf16"]
+    # the same tiles used with other counts of the same list length bound: NaN, never wrong numbers
+    cnt2 = cnt.copy()
+    i = int(np.argmax((cnt2 > 0) & (cnt2 < 32)))
+    cnt2.flat[i] -= 1
+    other = B.Scheme(200, 320, 32, 32, COL, 4).set_counts(cnt2)
+    nb2 = B.bsp_packed_sizes(other, None, B.BF16)[3]
+    if nb2 <= L.tiles.numel():
+        y2 = torch.zeros(layer.y_shape, dtype=torch.bfloat16, device="cuda")
+        B.bsp_linear(other, 100, B.BF16, B.BF16, to_dev(d["x"], "bf16"), L.tiles, None, False, y2)
+        torch.cuda.synchronize()
+        assert torch.isnan(y2.float()).all()
