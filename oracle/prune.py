@@ -280,3 +280,50 @@ def gemm_form(w: np.ndarray) -> np.ndarray:
     """(Cout, Cin, kh, kw) -> (Cout, Cin*kh*kw) with column q = (c*kh + r)*kw + s."""
     w = np.asarray(w)
     return w.reshape(w.shape[0], -1)
+
+
+def bcs_encode(w_stored: np.ndarray, mask: np.ndarray) -> dict:
+    """Blocked Compressed Storage (Sec. 4.3) of a masked matrix, from its definition.
+
+    Like CSR, but the column indices of consecutive rows that keep the same columns
+    are stored once:
+      weights      the kept weights, row by row, ascending columns (CSR order);
+      row_offset   start of each row in ``weights`` (R + 1 entries);
+      occurrence   first row of each run of consecutive rows with identical kept
+                   columns, then R (runs + 1 entries);
+      compact_cols the kept columns of each run, run after run;
+      col_stride   start of each run's columns in ``compact_cols``, then its length
+                   (runs + 1 entries).
+    Kept means kept by the mask (a kept weight may be numerically zero).
+    """
+    w_stored = np.asarray(w_stored)
+    mask = np.asarray(mask, dtype=np.uint8)
+    R, C = mask.shape
+    cols = [np.nonzero(mask[r])[0] for r in range(R)]
+    weights = [w_stored[r, cols[r]] for r in range(R)]
+    row_offset = [0]
+    for r in range(R):
+        row_offset.append(row_offset[-1] + len(cols[r]))
+    occurrence, compact, stride = [], [], [0]
+    for r in range(R):
+        if r == 0 or not np.array_equal(cols[r], cols[r - 1]):
+            occurrence.append(r)
+            compact.extend(cols[r].tolist())
+            stride.append(len(compact))
+    occurrence.append(R)
+    return {"weights": np.concatenate(weights) if R else np.zeros(0, w_stored.dtype),
+            "row_offset": np.asarray(row_offset, np.int32), "occurrence": np.asarray(occurrence, np.int32),
+            "compact_cols": np.asarray(compact, np.int32), "col_stride": np.asarray(stride, np.int32)}
+
+
+def bcs_decode(bcs: dict, R: int, C: int, like: np.ndarray) -> np.ndarray:
+    """Dense matrix (stored dtype) of a BCS encoding: row r of run g takes the run's
+    columns and its weights from row_offset[r]."""
+    out = np.zeros((R, C), dtype=np.asarray(like).dtype)
+    occ, st, cc = bcs["occurrence"], bcs["col_stride"], bcs["compact_cols"]
+    for g in range(len(occ) - 1):
+        cols = cc[st[g]:st[g + 1]]
+        for r in range(occ[g], occ[g + 1]):
+            o = bcs["row_offset"][r]
+            out[r, cols] = bcs["weights"][o:o + len(cols)]
+    return out

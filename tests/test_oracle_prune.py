@@ -397,3 +397,38 @@ def test_counts_pack_lengths_and_edge_counts():
     assert np.array_equal(back, np.where(m == 1, w, 0).astype(np.float32))
     with pytest.raises(ValueError):
         P.prune_mask(w.astype(np.float64), bh, bw, P.COL, 4, counts=np.full((3, 3), 33))
+
+
+# ------------------------------------------------------------------- BCS ---
+def test_bcs_matches_the_paper_example_and_its_completion():
+    """Sec. 4.3 prints a fragment of a BCS example; the fixture completes it by hand."""
+    g = GOLD["bcs_sec43"]
+    W = np.array(g["W"], dtype=np.float32)
+    b = P.bcs_encode(W, (W != 0).astype(np.uint8))
+    for k, pref in g["paper_prefix"].items():
+        assert b[k][:len(pref)].tolist() == pref, k
+    for k in ("weights", "row_offset", "occurrence", "compact_cols", "col_stride"):
+        assert b[k].tolist() == g[k], k
+
+
+@pytest.mark.parametrize("bh,bw,reg,rate", [(16, 32, P.COL, 4), (8, 16, P.COL, 3), (0, 0, P.COL, 2), (4, 4, P.ROW, 2)])
+def test_bcs_is_csr_with_shared_column_runs(bh, bw, reg, rate):
+    rng = np.random.default_rng(bh + bw + reg)
+    R, C = 40, 96
+    w = rng.standard_normal((R, C)).astype(np.float32)
+    m = P.prune_mask(w.astype(np.float64), bh, bw, reg, rate)
+    b = P.bcs_encode(w, m)
+    # CSR equivalence: row offsets are CSR's indptr, runs expand to CSR's column indices
+    indptr = np.concatenate([[0], np.cumsum(m.sum(axis=1))])
+    assert np.array_equal(b["row_offset"], indptr)
+    rows_cols = []
+    for gi in range(len(b["occurrence"]) - 1):
+        cols = b["compact_cols"][b["col_stride"][gi]:b["col_stride"][gi + 1]]
+        rows_cols += [cols] * (b["occurrence"][gi + 1] - b["occurrence"][gi])
+    assert np.array_equal(np.concatenate(rows_cols), np.nonzero(m)[1])
+    assert np.array_equal(P.bcs_decode(b, R, C, w), np.where(m == 1, w, 0).astype(np.float32))
+    if reg == P.COL and bh:
+        # column blocks: every block-row is one run at most (more rows merge only if equal)
+        assert len(b["occurrence"]) - 1 <= len(P.block_ranges(R, bh))
+        # BCS weights are the canonical column packing's values
+        assert np.array_equal(b["weights"], P.pack(w, m, bh, bw, reg, rate)["values"])
