@@ -147,6 +147,23 @@ bsp_status bsp_unpack(const bsp_scheme *scheme, bsp_dtype wdt, const void *value
                       const int32_t *indices, const int32_t *rowptr, void *w_masked_out,
                       void *stream);
 
+/* Blocked Compressed Storage (BCS, Sec. 4.3) of a BSP_COL or BSP_PUNCHED
+ * packing (indices / rowptr from bsp_pack, same scheme): CSR whose column
+ * indices are stored once per run of consecutive rows that keep the same
+ * columns.  The BCS weights array is the canonical `values` array itself (the
+ * kept weights row by row, ascending columns).  Outputs (device, int32):
+ *   occurrence   first row of each run, then rows    (up to n_block_rows + 1)
+ *   compact_cols each run's kept columns, run by run (up to n_indices)
+ *   col_stride   start of each run in compact_cols, then its length
+ *                                                     (up to n_block_rows + 1)
+ *   row_offset   start of each row in values          (rows + 1)
+ *   n_runs       the number of runs (one int32)
+ * Runs never split a block-row; neighbouring block-rows with identical lists
+ * merge.  Other regularities return BSP_EUNSUPPORTED.  Async. */
+bsp_status bsp_to_bcs(const bsp_scheme *scheme, const int32_t *indices, const int32_t *rowptr,
+                      int32_t *occurrence, int32_t *compact_cols, int32_t *col_stride, int32_t *row_offset,
+                      int32_t *n_runs, void *stream);
+
 /* Forward of a pruned conv layer (the layer of Sec. 4.2 with pruned weights):
  *   y[n,o,oh,ow] = bias[o] + sum_{kept (c,r,s)} W[o,c,r,s] * x[n,c,oh*sh-ph+r,ow*sw-pw+s]
  * then ReLU if relu != 0.  x: NCHW of in_dt (must equal the packed dtype);

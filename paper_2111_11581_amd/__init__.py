@@ -16,7 +16,7 @@ import os
 __all__ = [
     "F32", "BF16", "ROW", "COL", "UNSTRUCTURED", "DENSE", "PUNCHED", "BspError", "Scheme", "ConvShape",
     "lib", "lib_path", "bsp_packed_sizes", "bsp_prune", "bsp_pack", "bsp_unpack", "bsp_conv2d",
-    "bsp_linear", "bsp_maxpool2x2", "bsp_status_string", "bsp_version",
+    "bsp_linear", "bsp_maxpool2x2", "bsp_status_string", "bsp_version", "bsp_to_bcs",
 ]
 
 F32, BF16 = 0, 1
@@ -80,7 +80,7 @@ def lib():
     L.bsp_status_string.restype = ctypes.c_char_p
     L.bsp_version.argtypes = []
     for f in ("bsp_packed_sizes", "bsp_prune", "bsp_pack", "bsp_unpack", "bsp_conv2d",
-              "bsp_linear", "bsp_maxpool2x2", "bsp_version"):
+              "bsp_linear", "bsp_maxpool2x2", "bsp_version", "bsp_to_bcs"):
         getattr(L, f).restype = I32
     _lib = L
     return L
@@ -177,6 +177,15 @@ def bsp_unpack(scheme, wdt: int, values, indices, rowptr, w_out, stream=None):
     _need("w_out", w_out, s.rows * s.cols * _esize(wdt))
     _check("bsp_unpack", lib().bsp_unpack(ctypes.byref(s), int(wdt), _p(values), _p(indices),
                                           _p(rowptr), _p(w_out), _stream(stream)))
+
+
+def bsp_to_bcs(scheme, indices, rowptr, occurrence, compact_cols, col_stride, row_offset, n_runs, stream=None):
+    s = _scheme(scheme)
+    _need("row_offset", row_offset, (s.rows + 1) * 4)
+    _need("n_runs", n_runs, 4)
+    _check("bsp_to_bcs", lib().bsp_to_bcs(ctypes.byref(s), _p(indices), _p(rowptr), _p(occurrence),
+                                          _p(compact_cols), _p(col_stride), _p(row_offset), _p(n_runs),
+                                          _stream(stream)))
 
 
 def bsp_conv2d(scheme, shape, in_dt: int, out_dt: int, x, dev_tiles, bias, relu: bool, y, stream=None):

@@ -89,6 +89,22 @@ bsp_status bsp_unpack(const bsp_scheme *scheme, bsp_dtype wdt, const void *value
                                                                                       : BSP_EDEVICE;
 }
 
+bsp_status bsp_to_bcs(const bsp_scheme *scheme, const int32_t *indices, const int32_t *rowptr,
+                      int32_t *occurrence, int32_t *compact_cols, int32_t *col_stride, int32_t *row_offset,
+                      int32_t *n_runs, void *stream) {
+    if (!scheme || !indices || !rowptr || !occurrence || !compact_cols || !col_stride || !row_offset || !n_runs)
+        return BSP_EINVAL;
+    Plan p;
+    bsp_status st = make_plan(scheme, nullptr, BSP_BF16, -1, &p);
+    if (st != BSP_OK) return st;
+    if (p.reg != BSP_COL && p.reg != BSP_PUNCHED) return BSP_EUNSUPPORTED;
+    if ((int64_t)p.R * p.C > INT32_MAX) return BSP_EUNSUPPORTED;
+    return launch_bcs(p, indices, rowptr, occurrence, compact_cols, col_stride, row_offset, n_runs, S(stream)) ==
+                   hipSuccess
+               ? BSP_OK
+               : BSP_EDEVICE;
+}
+
 bsp_status bsp_conv2d(const bsp_scheme *scheme, const bsp_conv_shape *shape, bsp_dtype in_dt,
                       bsp_dtype out_dt, const void *x, const void *dev_tiles, const float *bias,
                       int32_t relu, void *y, void *stream) {

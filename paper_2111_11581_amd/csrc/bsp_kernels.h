@@ -13,6 +13,8 @@ hipError_t launch_prune(const Plan &p, const void *w, uint8_t *mask, hipStream_t
 bsp_status run_pack(const Plan &p, const void *w, const uint8_t *mask, void *values,
                     int32_t *indices, int32_t *rowptr, uint8_t *tiles, hipStream_t st);
 
+hipError_t launch_bcs(const Plan &p, const int32_t *indices, const int32_t *rowptr, int32_t *occurrence,
+                      int32_t *compact, int32_t *col_stride, int32_t *row_offset, int32_t *n_runs, hipStream_t st);
 hipError_t launch_unpack(const Plan &p, const void *values, const int32_t *indices,
                          const int32_t *rowptr, void *w_out, hipStream_t st);
 

@@ -426,6 +426,55 @@ __global__ void k_row_unpack(const E *__restrict__ values, const int32_t *__rest
     }
 }
 
+// Blocked Compressed Storage (Sec. 4.3) from the canonical column packing: runs of
+// consecutive block-rows with identical kept-column lists share one copy of the list.
+// One workgroup walks the block-rows in order (prep-time work, no inter-workgroup
+// synchronisation): it compares each list with the previous one, appends the lists
+// that start a run, and writes every row's start in the values array.
+__global__ void k_bcs(const int32_t *__restrict__ indices, const int32_t *__restrict__ rowptr, int nbr, int bh,
+                      int R, int32_t *__restrict__ occurrence, int32_t *__restrict__ compact,
+                      int32_t *__restrict__ col_stride, int32_t *__restrict__ row_offset, int32_t *__restrict__ n_runs) {
+    __shared__ int s_same, s_runs, s_cpos;
+    if (threadIdx.x == 0) {
+        s_runs = 0;
+        s_cpos = 0;
+    }
+    __syncthreads();
+    for (int i = 0; i < nbr; ++i) {
+        const int off = rowptr[i], len = rowptr[i + 1] - off;
+        const int r0 = i * bh, r1 = min(R, r0 + bh);
+        for (int r = r0 + threadIdx.x; r < r1; r += blockDim.x) row_offset[r] = off * bh + (r - r0) * len;
+        if (threadIdx.x == 0) s_same = i > 0 && len == off - rowptr[i - 1];
+        __syncthreads();
+        if (s_same) {
+            const int prev = rowptr[i - 1];
+            for (int t = threadIdx.x; t < len; t += blockDim.x)
+                if (indices[off + t] != indices[prev + t]) s_same = 0;   // every writer stores 0
+        }
+        __syncthreads();
+        if (!s_same) {
+            const int run = s_runs, cpos = s_cpos;
+            for (int t = threadIdx.x; t < len; t += blockDim.x) compact[cpos + t] = indices[off + t];
+            if (threadIdx.x == 0) {
+                occurrence[run] = r0;
+                col_stride[run] = cpos;
+            }
+        }
+        __syncthreads();
+        if (threadIdx.x == 0 && !s_same) {
+            s_runs += 1;
+            s_cpos += len;
+        }
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) {
+        occurrence[s_runs] = R;
+        col_stride[s_runs] = s_cpos;
+        row_offset[R] = rowptr[nbr - 1] * bh + (R - (nbr - 1) * bh) * (rowptr[nbr] - rowptr[nbr - 1]);
+        *n_runs = s_runs;
+    }
+}
+
 inline int grid_for(size_t n) { return (int)std::max<size_t>(1, std::min<size_t>(8192, (n + 255) / 256)); }
 
 template <typename E>
@@ -577,6 +626,13 @@ bsp_status run_pack(const Plan &p, const void *w, const uint8_t *mask, void *val
         return pack_t<float>(p, (const float *)w, mask, (float *)values, indices, rowptr, tiles, st);
     return pack_t<uint16_t>(p, (const uint16_t *)w, mask, (uint16_t *)values, indices, rowptr,
                             tiles, st);
+}
+
+hipError_t launch_bcs(const Plan &p, const int32_t *indices, const int32_t *rowptr, int32_t *occurrence,
+                      int32_t *compact, int32_t *col_stride, int32_t *row_offset, int32_t *n_runs, hipStream_t st) {
+    k_bcs<<<1, 256, 0, st>>>(indices, rowptr, p.nbr, p.bh_eff, p.R, occurrence, compact, col_stride, row_offset,
+                             n_runs);
+    return hipGetLastError();
 }
 
 hipError_t launch_unpack(const Plan &p, const void *values, const int32_t *indices,

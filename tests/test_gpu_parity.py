@@ -529,3 +529,57 @@ def test_per_block_counts_linear_and_fingerprint(B):
         B.bsp_linear(other, 100, B.BF16, B.BF16, to_dev(d["x"], "bf16"), L.tiles, None, False, y2)
         torch.cuda.synchronize()
         assert torch.isnan(y2.float()).all()
+
+
+# ------------------------------------------------------------------- BCS ---
+def _gpu_bcs(B, L, scheme):
+    import torch
+    nbr = L.n_rowptr - 1
+    occ = torch.full((nbr + 1,), -1, dtype=torch.int32, device="cuda")
+    st = torch.full((nbr + 1,), -1, dtype=torch.int32, device="cuda")
+    cc = torch.full((max(L.n_indices, 1),), -1, dtype=torch.int32, device="cuda")
+    ro = torch.full((scheme.rows + 1,), -1, dtype=torch.int32, device="cuda")
+    nr = torch.zeros(1, dtype=torch.int32, device="cuda")
+    B.bsp_to_bcs(scheme, L.indices, L.rowptr, occ, cc, st, ro, nr)
+    torch.cuda.synchronize()
+    n = int(nr.item())
+    return {"occurrence": occ[:n + 1].cpu().numpy(), "col_stride": st[:n + 1].cpu().numpy(),
+            "compact_cols": cc[:int(st[n].item())].cpu().numpy(), "row_offset": ro.cpu().numpy()}
+
+
+@pytest.mark.parametrize("kind", ["col16x32", "col8x16 counts", "punched 16x8", "merged block-rows"])
+def test_bcs_encoding_matches_oracle(B, kind):
+    import torch
+    rng = np.random.default_rng(len(kind))
+    if kind == "punched 16x8":
+        R, cin, khw = 64, 24, 9
+        C = cin * khw
+        scheme = B.Scheme(R, C, 16, 8, PUNCHED, 3, khw)
+    else:
+        R, C = 70, 160
+        scheme = B.Scheme(R, C, 16, 32, COL, 4) if kind != "col8x16 counts" else B.Scheme(R, C, 8, 16, COL, 4)
+    w = draw(seed_for(9, 80 + len(kind), 1), (R, C), ("normal", 0, 1), "bf16")
+    mask = None
+    if kind == "col8x16 counts":
+        cnt = _counts(R, C, 8, 16, COL, 1, 5)
+        scheme.set_counts(cnt)
+        m = OP.prune_mask(as_f64(w, "bf16"), 8, 16, COL, 4, counts=cnt)
+    elif kind == "merged block-rows":
+        # block-rows 0-1 and 3-4 keep the same columns: BCS stores each list once
+        m = OP.prune_mask(as_f64(w, "bf16"), 16, 32, COL, 4)
+        m[16:32] = m[0]
+        m[64:70] = m[48]
+        mask = torch.from_numpy(m.reshape(-1)).cuda()
+    else:
+        m = oracle_mask(w, "bf16", scheme)
+    L = _layers().PackedLayer(scheme, B.BF16, to_dev(w, "bf16"), mask=mask)
+    assert np.array_equal(L.mask.cpu().numpy().reshape(R, C), m)
+    ref = OP.bcs_encode(w, m)
+    got = _gpu_bcs(B, L, scheme)
+    for k in ("occurrence", "col_stride", "compact_cols", "row_offset"):
+        assert np.array_equal(got[k], ref[k]), k
+    # the BCS weights array is the canonical values array
+    vals = from_dev(L.values[:L.n_values], "bf16")
+    assert np.array_equal(vals, ref["weights"])
+    if kind == "merged block-rows":
+        assert len(ref["occurrence"]) - 1 == 3
