@@ -29,6 +29,10 @@ Readings where the paper is silent (each listed in the design notes):
 * block-punched: blocks of bh filters x bw input channels; kept locations per
   block = ceil(kh*kw / rate); the score of a location sums over the block's
   (filter, channel) pairs in ascending (filter, channel) order;
+* simultaneous row and column pruning (Sec. 4.2: Eqs. 2 and 3 solved together):
+  every block keeps ceil(bh / rate) rows and ceil(bw / rate) columns, each set
+  chosen by its own group norm on the block's weights; the block keeps their
+  product (so the kept fraction is about 1 / rate^2);
 * per-block kept counts (Sec. 4.1.1: the same or a different number per block;
   Sec. 4.2: the reweighted method sets a rate per block) are given by the
   caller as an array over the blocks in row-major order, replacing
@@ -42,7 +46,7 @@ from __future__ import annotations
 
 import numpy as np
 
-ROW, COL, UNSTRUCTURED, DENSE, PUNCHED = 0, 1, 2, 3, 4
+ROW, COL, UNSTRUCTURED, DENSE, PUNCHED, ROWCOL = 0, 1, 2, 3, 4, 5
 
 
 def kept_count(extent: int, rate: int) -> int:
@@ -136,6 +140,16 @@ def prune_mask(wg: np.ndarray, bh: int, bw: int, regularity: int, rate: int, khw
     mask = np.zeros((R, C), dtype=np.uint8)
     if regularity == PUNCHED:
         return punched_mask(wg, max(int(khw), 1), bh, bw, rate, counts)
+    if regularity == ROWCOL:
+        if counts is not None:
+            raise ValueError("per-block counts are not defined for simultaneous row and column pruning")
+        for r0, r1 in block_ranges(R, bh):
+            for c0, c1 in block_ranges(C, bw):
+                blk = wg[r0:r1, c0:c1]
+                rows = top_k(group_scores(blk, ROW), kept_count(r1 - r0, rate))
+                cols = top_k(group_scores(blk, COL), kept_count(c1 - c0, rate))
+                mask[np.ix_(r0 + rows, c0 + cols)] = 1
+        return mask
     if regularity == DENSE:
         mask[:] = 1
         return mask
@@ -195,6 +209,16 @@ def mask_is_valid(mask: np.ndarray, bh: int, bw: int, regularity: int, rate: int
         return bool(np.all(mask == 1))
     if regularity == UNSTRUCTURED:
         return int(mask.sum()) == kept_count(R * C, rate)
+    if regularity == ROWCOL:
+        for r0, r1 in block_ranges(R, bh):
+            for c0, c1 in block_ranges(C, bw):
+                blk = mask[r0:r1, c0:c1]
+                rows, cols = blk.any(axis=1), blk.any(axis=0)
+                if not np.array_equal(blk, np.outer(rows, cols).astype(np.uint8)):
+                    return False
+                if rows.sum() != kept_count(r1 - r0, rate) or cols.sum() != kept_count(c1 - c0, rate):
+                    return False
+        return True
     for i, (r0, r1) in enumerate(block_ranges(R, bh)):
         for j, (c0, c1) in enumerate(block_ranges(C, bw)):
             blk = mask[r0:r1, c0:c1]
@@ -220,6 +244,8 @@ def pack(w_stored: np.ndarray, mask: np.ndarray, bh: int, bw: int, regularity: i
          W[i*bh + p, indices[rowptr[i] + t]].
     PUNCHED: as COL (a block-row keeps whole GEMM columns: the kept locations
          of each of its channel blocks).
+    ROWCOL: as COL over the columns any row of the block-row keeps; the values
+         of the rows a block removed are zero.
     ROW: for block (i, j) in row-major order, ``indices[rowptr[b]:rowptr[b+1]]``
          are its kept rows ascending; its values are rows of the block,
          ``[t][q_local]``, stored one block after the other.
@@ -233,12 +259,13 @@ def pack(w_stored: np.ndarray, mask: np.ndarray, bh: int, bw: int, regularity: i
         return {"indices": np.zeros(0, np.int32), "rowptr": np.zeros(0, np.int32),
                 "values": vals.reshape(-1).copy()}
     idx, ptr, vals = [], [0], []
-    if regularity in (COL, PUNCHED):
+    if regularity in (COL, PUNCHED, ROWCOL):
         for r0, r1 in block_ranges(R, bh):
-            kept = np.nonzero(mask[r0])[0].astype(np.int32)
+            kept = np.nonzero(mask[r0:r1].any(axis=0))[0].astype(np.int32)
             idx.append(kept)
             ptr.append(ptr[-1] + len(kept))
-            vals.append(w_stored[r0:r1][:, kept].reshape(-1))
+            sub = np.where(mask[r0:r1][:, kept] == 1, w_stored[r0:r1][:, kept], np.zeros_like(w_stored[:1, :1]))
+            vals.append(sub.reshape(-1))
     else:
         for r0, r1 in block_ranges(R, bh):
             for c0, c1 in block_ranges(C, bw):
@@ -258,7 +285,7 @@ def unpack(packed: dict, R: int, C: int, bh: int, bw: int, regularity: int, like
     if regularity in (DENSE, UNSTRUCTURED):
         return vals.reshape(R, C).copy()
     off = 0
-    if regularity in (COL, PUNCHED):
+    if regularity in (COL, PUNCHED, ROWCOL):
         for i, (r0, r1) in enumerate(block_ranges(R, bh)):
             kept = idx[ptr[i]:ptr[i + 1]]
             n = (r1 - r0) * len(kept)

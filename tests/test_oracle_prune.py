@@ -432,3 +432,38 @@ def test_bcs_is_csr_with_shared_column_runs(bh, bw, reg, rate):
         assert len(b["occurrence"]) - 1 <= len(P.block_ranges(R, bh))
         # BCS weights are the canonical column packing's values
         assert np.array_equal(b["weights"], P.pack(w, m, bh, bw, reg, rate)["values"])
+
+
+# ------------------------------------------ simultaneous row + column pruning ---
+def test_rowcol_golden_mask():
+    g = GOLD["matrix_4x8"]
+    m = P.prune_mask(np.array(g["W"], dtype=np.float64), 2, 4, P.ROWCOL, 2)
+    assert m.tolist() == g["rowcol_2x4_rate2"]["mask"]
+    assert P.mask_is_valid(m, 2, 4, P.ROWCOL, 2)
+
+
+@pytest.mark.parametrize("bh,bw,rate", [(4, 8, 2), (0, 16, 3), (5, 0, 4), (8, 8, 8)])
+def test_rowcol_reduces_to_column_and_row_blocks(bh, bw, rate):
+    """One-row blocks keep their row: column pruning; one-column blocks: row pruning."""
+    rng = np.random.default_rng(bh * 7 + bw + rate)
+    w = rng.standard_normal((24, 40))
+    assert np.array_equal(P.prune_mask(w, 1, bw, P.ROWCOL, rate), P.prune_mask(w, 1, bw, P.COL, rate))
+    assert np.array_equal(P.prune_mask(w, bh, 1, P.ROWCOL, rate), P.prune_mask(w, bh, 1, P.ROW, rate))
+    m = P.prune_mask(w, bh, bw, P.ROWCOL, rate)
+    assert P.mask_is_valid(m, bh, bw, P.ROWCOL, rate)
+    # the kept set is the product of the row choice and the column choice
+    assert np.array_equal(m, P.prune_mask(w, bh, bw, P.ROW, rate) & P.prune_mask(w, bh, bw, P.COL, rate))
+
+
+def test_rowcol_pack_roundtrip_and_invalid_mask():
+    rng = np.random.default_rng(21)
+    R, C, bh, bw = 37, 53, 8, 16
+    wb = f32_to_bf16_bits(rng.standard_normal((R, C)).astype(np.float32))
+    m = P.prune_mask(P.as_f64(wb, "bf16"), bh, bw, P.ROWCOL, 3)
+    pk = P.pack(wb, m, bh, bw, P.ROWCOL, 3)
+    back = P.unpack(pk, R, C, bh, bw, P.ROWCOL, wb)
+    assert np.array_equal(back, np.where(m == 1, wb, 0).astype(wb.dtype))
+    bad = m.copy()
+    r, c = np.argwhere(m == 1)[0]
+    bad[r, c] = 0                               # no longer a product of a row and a column set
+    assert not P.mask_is_valid(bad, bh, bw, P.ROWCOL, 3)
