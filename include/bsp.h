@@ -57,8 +57,13 @@ typedef enum {
     BSP_COL = 1,            /* whole columns removed inside each block (Eq. 3) */
     BSP_UNSTRUCTURED = 2,   /* magnitude top-k over the whole layer (Sec. 2.1.1) */
     BSP_DENSE = 3,          /* nothing removed                                 */
-    BSP_PUNCHED = 4         /* kernel locations removed per block of filters x
+    BSP_PUNCHED = 4,        /* kernel locations removed per block of filters x
                                input channels (Sec. 4.1.2, Eq. 4)              */
+    BSP_ROWCOL = 5          /* rows and columns removed in the same block
+                               (Eqs. 2 and 3 together, Sec. 4.2): a block keeps
+                               ceil(bh/rate) rows x ceil(bw/rate) columns;
+                               packed like BSP_COL with zeros for its removed
+                               rows; no per-block counts                       */
 } bsp_regularity;
 
 typedef struct {
@@ -94,7 +99,7 @@ typedef struct {
 /* Sizes (in elements, and bytes for dev_tiles) of the buffers bsp_pack fills.
  * Host-only, pure.  conv_or_null selects the conv layout (its n is ignored);
  * NULL means a linear layer.  The canonical arrays are
- *   COL, PUNCHED: values = nnz, indices = n_block_rows * kept_per_row,
+ *   COL, PUNCHED, ROWCOL: values = rows * kept_per_row, indices = n_block_rows * kept_per_row,
  *        rowptr = n_block_rows + 1 (PUNCHED keeps Cin*ceil(khw/rate) per row)
  *   ROW: values = nnz, indices = kept rows summed over blocks, rowptr = n_blocks + 1
  *   DENSE / UNSTRUCTURED: values = rows * cols, indices = rowptr = 0. */

@@ -95,6 +95,41 @@ __global__ void k_validate_punched(const uint8_t *__restrict__ mask, int R, int 
     if (bad) atomicOr(flag, 1);
 }
 
+// Row + column structure: inside a block the mask is the product of its kept rows
+// (rows with any kept entry) and kept columns, with ceil(extent / rate) of each.
+__global__ void k_validate_rowcol(const uint8_t *__restrict__ mask, int R, int C, int bh, int bw, int nbc, int rate,
+                                  int *flag) {
+    extern __shared__ uint8_t kf[];   // kept rows [bh], kept columns [bw]
+    __shared__ int nrk, nck;
+    const int b = blockIdx.x;
+    const int bi = b / nbc, bj = b - bi * nbc;
+    const int r0 = bi * bh, r1 = min(R, r0 + bh), c0 = bj * bw, c1 = min(C, c0 + bw);
+    const int nr = r1 - r0, nc = c1 - c0;
+    if (threadIdx.x == 0) nrk = nck = 0;
+    __syncthreads();
+    int bad = 0, lr = 0, lc = 0;
+    for (int g = threadIdx.x; g < nr + nc; g += blockDim.x) {
+        uint8_t any = 0;
+        if (g < nr)
+            for (int q = c0; q < c1; ++q) any |= mask[(size_t)(r0 + g) * C + q];
+        else
+            for (int p = r0; p < r1; ++p) any |= mask[(size_t)p * C + c0 + (g - nr)];
+        bad |= any > 1;
+        kf[g < nr ? g : bh + (g - nr)] = any;
+        if (g < nr) lr += any == 1;
+        else lc += any == 1;
+    }
+    if (lr) atomicAdd(&nrk, lr);
+    if (lc) atomicAdd(&nck, lc);
+    __syncthreads();
+    for (int e = threadIdx.x; e < nr * nc; e += blockDim.x) {
+        const int p = e / nc, q = e - p * nc;
+        bad |= mask[(size_t)(r0 + p) * C + c0 + q] != (kf[p] & kf[bh + q]);
+    }
+    if (threadIdx.x == 0) bad |= nrk != (nr + rate - 1) / rate || nck != (nc + rate - 1) / rate;
+    if (bad) atomicOr(flag, 1);
+}
+
 __global__ void k_validate_all(const uint8_t *__restrict__ mask, size_t n, int need_ones,
                                int *flag, unsigned int *count) {
     int bad = 0;
@@ -116,16 +151,19 @@ __global__ void k_check_count(const unsigned int *count, unsigned int k, int *fl
 
 // Kept-column list of block-row i, written at rowptr[i] (offsets computed on the host
 // from the scheme); the block-row's first row holds its kept columns.
-__global__ void k_col_lists(const uint8_t *__restrict__ mask, int C, int bh, const int32_t *__restrict__ rowptr,
-                            int32_t *__restrict__ indices, int *flag) {
+__global__ void k_col_lists(const uint8_t *__restrict__ mask, int R, int C, int bh, int any_row,
+                            const int32_t *__restrict__ rowptr, int32_t *__restrict__ indices, int *flag) {
     __shared__ int wave_tot[4];
     const int i = blockIdx.x;
     const uint8_t *mr = mask + (size_t)i * bh * C;
+    const int rows = any_row ? min(R - i * bh, bh) : 1;   // row + column blocks: a column is kept by any row
     const int off = rowptr[i], L = rowptr[i + 1] - off;
     int base = 0;
     for (int q0 = 0; q0 < C; q0 += 256) {
         const int q = q0 + threadIdx.x;
-        const int v = q < C ? mr[q] : 0;
+        int v = 0;
+        if (q < C)
+            for (int r = 0; r < rows && !v; ++r) v = mr[(size_t)r * C + q];
         int tot;
         const int pos = base + block_excl_scan_256(v, wave_tot, &tot);
         if (v) {
@@ -139,15 +177,17 @@ __global__ void k_col_lists(const uint8_t *__restrict__ mask, int C, int bh, con
 
 // Values of block-row i: [row][t] at rowptr[i] * bh (earlier block-rows are full).
 template <typename E>
-__global__ void k_col_values(const E *__restrict__ w, const int32_t *__restrict__ indices,
-                             const int32_t *__restrict__ rowptr, E *__restrict__ values, int R, int C, int bh) {
+__global__ void k_col_values(const E *__restrict__ w, const uint8_t *__restrict__ mask,
+                             const int32_t *__restrict__ indices, const int32_t *__restrict__ rowptr,
+                             E *__restrict__ values, int R, int C, int bh) {
     const int i = blockIdx.x;
     const int off = rowptr[i], L = rowptr[i + 1] - off;
     const int r0 = i * bh, rows = min(R, r0 + bh) - r0;
     const size_t vbase = (size_t)off * bh;
     for (int e = threadIdx.x; e < rows * L; e += blockDim.x) {
         const int p = e / L, t = e - p * L;
-        values[vbase + e] = w[(size_t)(r0 + p) * C + indices[off + t]];
+        const size_t wi = (size_t)(r0 + p) * C + indices[off + t];
+        values[vbase + e] = mask[wi] ? w[wi] : (E)0;   // zero in the rows a row + column block removed
     }
 }
 
@@ -494,7 +534,7 @@ bsp_status pack_t(const Plan &p, const E *w, const uint8_t *mask, E *values, int
     if (hipMemcpyAsync(tiles, &h, sizeof(h), hipMemcpyHostToDevice, st) != hipSuccess)
         return BSP_EDEVICE;
     const size_t n = (size_t)p.R * p.C;
-    const bool blocked = p.reg == BSP_COL || p.reg == BSP_ROW || p.reg == BSP_PUNCHED;
+    const bool blocked = p.reg != BSP_DENSE && p.reg != BSP_UNSTRUCTURED;
     // canonical list offsets (from the scheme and its counts) and the counts, for the
     // kernels below; both copies complete before this call returns (it synchronises)
     std::vector<int32_t> rp(blocked ? (size_t)p.n_rowptr : 0);
@@ -537,7 +577,10 @@ bsp_status pack_t(const Plan &p, const E *w, const uint8_t *mask, E *values, int
     }
     const int blk_cols = p.reg == BSP_PUNCHED ? p.bw_eff * p.khw : p.bw_eff;
     // 1. validate the block structure
-    if (p.reg == BSP_PUNCHED) {
+    if (p.reg == BSP_ROWCOL) {
+        k_validate_rowcol<<<p.nbr * p.nbc, 256, p.bh_eff + p.bw_eff, st>>>(mask, p.R, p.C, p.bh_eff, p.bw_eff,
+                                                                          p.nbc, p.rate, flag);
+    } else if (p.reg == BSP_PUNCHED) {
         k_validate_punched<<<p.nbr * p.nbc, 256, 0, st>>>(mask, p.R, p.C, p.khw, p.bh_eff, p.bw_eff, p.nbc,
                                                          (p.khw + p.rate - 1) / p.rate, counts, flag);
     } else if (p.reg == BSP_COL || p.reg == BSP_ROW) {
@@ -556,9 +599,9 @@ bsp_status pack_t(const Plan &p, const E *w, const uint8_t *mask, E *values, int
         return BSP_EDEVICE;
     if (hflag) return BSP_EMASK;
     // 2. canonical packing
-    if (p.reg == BSP_COL || p.reg == BSP_PUNCHED) {
-        k_col_lists<<<p.nbr, 256, 0, st>>>(mask, p.C, p.bh_eff, rowptr, indices, flag);
-        k_col_values<E><<<p.nbr, 256, 0, st>>>(w, indices, rowptr, values, p.R, p.C, p.bh_eff);
+    if (p.reg == BSP_COL || p.reg == BSP_PUNCHED || p.reg == BSP_ROWCOL) {
+        k_col_lists<<<p.nbr, 256, 0, st>>>(mask, p.R, p.C, p.bh_eff, p.reg == BSP_ROWCOL, rowptr, indices, flag);
+        k_col_values<E><<<p.nbr, 256, 0, st>>>(w, mask, indices, rowptr, values, p.R, p.C, p.bh_eff);
     } else if (p.reg == BSP_ROW) {
         k_row_lists<<<p.nbr * p.nbc, 256, 0, st>>>(mask, p.R, p.C, p.bh_eff, p.bw_eff, p.nbc, rowptr,
                                                     indices, flag);
@@ -611,7 +654,7 @@ hipError_t unpack_t(const Plan &p, const E *values, const int32_t *indices, cons
         return hipMemcpyAsync(out, values, n * sizeof(E), hipMemcpyDeviceToDevice, st);
     }
     k_fill<E><<<grid_for(n), 256, 0, st>>>(out, n, (E)0);
-    if (p.reg == BSP_COL || p.reg == BSP_PUNCHED)
+    if (p.reg == BSP_COL || p.reg == BSP_PUNCHED || p.reg == BSP_ROWCOL)
         k_col_unpack<E><<<p.nbr, 256, 0, st>>>(values, indices, rowptr, out, p.R, p.C, p.bh_eff);
     else
         k_row_unpack<E><<<p.nbr * p.nbc, 256, 0, st>>>(values, indices, rowptr, out, p.C, p.bw_eff, p.nbc);

@@ -219,7 +219,7 @@ static bool plan_pointwise(Plan *p, int span_req, int n_mt, int mpg, int astep) 
 // Groups of block (bi, bj): columns (COL), rows (ROW) or kernel locations (PUNCHED).
 static int block_groups(const Plan &p, int bi, int bj) {
     if (p.reg == BSP_PUNCHED) return p.khw;
-    if (p.reg == BSP_COL) return std::min(p.C, (bj + 1) * p.bw_eff) - bj * p.bw_eff;
+    if (p.reg == BSP_COL || p.reg == BSP_ROWCOL) return std::min(p.C, (bj + 1) * p.bw_eff) - bj * p.bw_eff;
     return std::min(p.R, (bi + 1) * p.bh_eff) - bi * p.bh_eff;
 }
 
@@ -306,7 +306,8 @@ bsp_status make_plan(const bsp_scheme *s, const bsp_conv_shape *conv, bsp_dtype 
     if (!s || !p) return BSP_EINVAL;
     std::memset(p, 0, sizeof(*p));
     if (s->rows <= 0 || s->cols <= 0 || s->bh < 0 || s->bw < 0 || s->rate < 1) return BSP_EINVAL;
-    if (s->regularity < BSP_ROW || s->regularity > BSP_PUNCHED) return BSP_EINVAL;
+    if (s->regularity < BSP_ROW || s->regularity > BSP_ROWCOL) return BSP_EINVAL;
+    if (s->regularity == BSP_ROWCOL && s->counts) return BSP_EUNSUPPORTED;
     if (wdt != BSP_F32 && wdt != BSP_BF16) return BSP_EINVAL;
     const int khw = s->regularity == BSP_PUNCHED ? std::max(s->khw, 1) : 1;
     if (s->regularity == BSP_PUNCHED && (s->khw < 0 || s->cols % khw != 0)) return BSP_EINVAL;
@@ -370,7 +371,7 @@ bsp_status make_plan(const bsp_scheme *s, const bsp_conv_shape *conv, bsp_dtype 
         p->shared = 0;
         p->n_groups = p->nbr;
         p->group_rows = p->bh_eff;
-    } else if (p->reg == BSP_COL) {
+    } else if (p->reg == BSP_COL || p->reg == BSP_ROWCOL) {
         const int last_w = p->C - (p->nbc - 1) * p->bw_eff;
         p->L = (p->nbc - 1) * kept_count(p->bw_eff, p->rate) + kept_count(last_w, p->rate);
         p->n_indices = (int64_t)p->nbr * p->L;

@@ -115,6 +115,55 @@ __global__ void k_prune_punched(const E *__restrict__ w, uint8_t *__restrict__ m
     }
 }
 
+// Simultaneous row and column pruning: the block's row scores (Eq. 2) and column
+// scores (Eq. 3), each summed in ascending order, ranked separately; the block keeps
+// the product of the kept rows and the kept columns.
+template <typename E>
+__global__ void k_prune_rowcol(const E *__restrict__ w, uint8_t *__restrict__ mask, int R, int C, int bh, int bw,
+                               int nbc, int rate) {
+    extern __shared__ double sc[];   // row scores [bh], column scores [bw], then keep flags
+    const int b = blockIdx.x;
+    const int bi = b / nbc, bj = b - bi * nbc;
+    const int r0 = bi * bh, r1 = min(R, r0 + bh), c0 = bj * bw, c1 = min(C, c0 + bw);
+    const int nr = r1 - r0, nc = c1 - c0;
+    double *rs = sc, *cs = sc + bh;
+    uint8_t *kr = (uint8_t *)(sc + bh + bw), *kc = kr + bh;
+    for (int g = threadIdx.x; g < nr + nc; g += blockDim.x) {
+        double s = 0.0;
+        if (g < nr) {
+            const size_t row = (size_t)(r0 + g) * C;
+            for (int q = c0; q < c1; ++q) {
+                const double v = ld_f64(w, row + q);
+                s = fma(v, v, s);
+            }
+            rs[g] = s;
+        } else {
+            for (int p = r0; p < r1; ++p) {
+                const double v = ld_f64(w, (size_t)p * C + c0 + (g - nr));
+                s = fma(v, v, s);
+            }
+            cs[g - nr] = s;
+        }
+    }
+    __syncthreads();
+    const int kr_n = (nr + rate - 1) / rate, kc_n = (nc + rate - 1) / rate;
+    for (int g = threadIdx.x; g < nr + nc; g += blockDim.x) {
+        const bool isr = g < nr;
+        const double *sv = isr ? rs : cs;
+        const int n = isr ? nr : nc, x = isr ? g : g - nr;
+        const double s = sv[x];
+        int rank = 0;
+        for (int h = 0; h < n; ++h) rank += (sv[h] > s) || (sv[h] == s && h < x);
+        if (isr) kr[x] = rank < kr_n;
+        else kc[x] = rank < kc_n;
+    }
+    __syncthreads();
+    for (int e = threadIdx.x; e < nr * nc; e += blockDim.x) {
+        const int p = e / nc, q = e - p * nc;
+        mask[(size_t)(r0 + p) * C + c0 + q] = kr[p] & kc[q];
+    }
+}
+
 __global__ void k_fill_u8(uint8_t *p, size_t n, uint8_t v) {
     for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n;
          i += (size_t)gridDim.x * blockDim.x)
@@ -284,7 +333,15 @@ hipError_t launch_prune(const Plan &p, const void *w, uint8_t *mask, hipStream_t
         if (e != hipSuccess) return e;
     }
     const int blocks = p.nbr * p.nbc;
-    if (p.reg == BSP_PUNCHED) {
+    if (p.reg == BSP_ROWCOL) {
+        const size_t lds = (sizeof(double) + 1) * (size_t)(p.bh_eff + p.bw_eff);
+        if (p.dt == BSP_F32)
+            k_prune_rowcol<float><<<blocks, 256, lds, st>>>((const float *)w, mask, p.R, p.C, p.bh_eff, p.bw_eff,
+                                                            p.nbc, p.rate);
+        else
+            k_prune_rowcol<uint16_t><<<blocks, 256, lds, st>>>((const uint16_t *)w, mask, p.R, p.C, p.bh_eff,
+                                                               p.bw_eff, p.nbc, p.rate);
+    } else if (p.reg == BSP_PUNCHED) {
         const size_t lds = (sizeof(double) + 1) * (size_t)p.khw;
         if (p.dt == BSP_F32)
             k_prune_punched<float><<<blocks, 256, lds, st>>>((const float *)w, mask, p.R, p.C, p.khw, p.bh_eff,

@@ -15,8 +15,9 @@ from __future__ import annotations
 import math
 from dataclasses import dataclass, field
 
-ROW, COL, UNSTRUCTURED, DENSE, PUNCHED = 0, 1, 2, 3, 4
-REG_NAMES = {ROW: "row", COL: "col", UNSTRUCTURED: "unstructured", DENSE: "dense", PUNCHED: "punched"}
+ROW, COL, UNSTRUCTURED, DENSE, PUNCHED, ROWCOL = 0, 1, 2, 3, 4, 5
+REG_NAMES = {ROW: "row", COL: "col", UNSTRUCTURED: "unstructured", DENSE: "dense", PUNCHED: "punched",
+             ROWCOL: "row+col"}
 
 
 @dataclass(frozen=True)

@@ -8,7 +8,7 @@ import pytest
 
 from oracle import prune as OP
 from synthetic import (workload, draw, draw_layer, seed_for, ConvLayer, LinearLayer, ROW, COL, UNSTRUCTURED, DENSE,
-                       PUNCHED)
+                       PUNCHED, ROWCOL)
 from tests.helpers import DT, to_dev, from_dev, as_f64, rel_l2, oracle_mask, oracle_conv, oracle_linear, out_to_f64
 
 pytestmark = pytest.mark.gpu
@@ -50,6 +50,10 @@ MATS = [  # name, R, C, bh, bw, reg, rate, dtype, dist
     ("ties col", 48, 96, 16, 32, COL, 4, "bf16", ("ties",)),
     ("ties row", 96, 48, 32, 16, ROW, 4, "f32", ("ties",)),
     ("ties unstructured", 64, 64, 1, 1, UNSTRUCTURED, 5, "bf16", ("ties",)),
+    ("rowcol 16x32 r2", 64, 576, 16, 32, ROWCOL, 2, "bf16", ("normal", 0, 0.05)),
+    ("rowcol ragged 8x16 r3 f32", 37, 53, 8, 16, ROWCOL, 3, "f32", ("normal", 0, 1.0)),
+    ("rowcol whole r4", 96, 300, 0, 0, ROWCOL, 4, "bf16", ("normal", 0, 0.05)),
+    ("ties rowcol", 48, 96, 16, 32, ROWCOL, 4, "bf16", ("ties",)),
 ]
 
 
@@ -75,7 +79,7 @@ def test_prune_and_pack_bit_exact(B, i):
     pk = OP.pack(w, m_ref, bh, bw, reg, rate)
     vals = from_dev(layer.values[:layer.n_values], dtype)
     assert np.array_equal(vals.view(np.uint8), np.ascontiguousarray(pk["values"]).view(np.uint8))
-    if reg in (ROW, COL):
+    if reg in (ROW, COL, ROWCOL):
         assert np.array_equal(layer.indices[:layer.n_indices].cpu().numpy(), pk["indices"])
         assert np.array_equal(layer.rowptr[:layer.n_rowptr].cpu().numpy(), pk["rowptr"])
     back = from_dev(layer.unpack(), dtype).reshape(R, C)
@@ -176,6 +180,10 @@ CONV_CASES = [
     _conv_case("3x3 punched 16x1 r9 ragged", 3, 24, 9, 13, 40, 3, 1, 1, 16, 1, PUNCHED, 9),
     _conv_case("f32 3x3 punched 4x4 r2", 1, 16, 10, 10, 32, 3, 1, 1, 4, 4, PUNCHED, 2, dtype="f32", out="f32"),
     _conv_case("1x1 punched 32x16 r2 keeps all", 2, 64, 14, 14, 96, 1, 1, 0, 32, 16, PUNCHED, 2),
+    # rows and columns removed in the same block (Eqs. 2-3 together)
+    _conv_case("3x3 rowcol 16x32 r2 bias relu", 2, 64, 12, 12, 64, 3, 1, 1, 16, 32, ROWCOL, 2, relu=True, bias=True),
+    _conv_case("1x1 rowcol 32x32 r2 s2", 2, 64, 14, 14, 96, 1, 2, 0, 32, 32, ROWCOL, 2),
+    _conv_case("f32 3x3 rowcol 8x8 r2", 1, 16, 10, 10, 32, 3, 1, 1, 8, 8, ROWCOL, 2, dtype="f32", out="f32"),
 ]
 
 
@@ -372,7 +380,7 @@ def test_c4_fc_layer_sampled_columns(B):
 @pytest.mark.parametrize("batch,reg,bh,bw,rate,out_dt,relu", [
     (37, COL, 32, 32, 10, "bf16", False), (100, ROW, 32, 32, 2, "f32", True),
     (64, DENSE, 0, 0, 1, "bf16", True), (130, COL, 16, 64, 4, "bf16", False),
-    (100, ROW, 0, 0, 4, "bf16", True), (70, ROW, 32, 0, 2, "f32", False)])
+    (100, ROW, 0, 0, 4, "bf16", True), (70, ROW, 32, 0, 2, "f32", False), (90, ROWCOL, 32, 32, 2, "bf16", True)])
 def test_linear_small(B, batch, reg, bh, bw, rate, out_dt, relu):
     layer = LinearLayer("fc", batch, 320, 200, bh, bw, reg, rate, "bf16", ("uniform", -1, 1),
                         ("normal", 0, 0.05), relu=relu)
