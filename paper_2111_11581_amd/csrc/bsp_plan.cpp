@@ -140,7 +140,8 @@ static bool plan_pointwise(Plan *p, int span_req, int n_mt, int mpg, int astep) 
                     const int64_t fixed = d_res + (resident ? align256(a_all) : 0);
                     for (int nb = 2; nb <= 3; ++nb) {
                         for (int occ = 1; occ <= occ_v; ++occ) {
-                            const int64_t budget = (160 * 1024) / occ - 1280;   // minus static LDS
+                            // minus static LDS (bias, and the row map of row-mapped layers)
+                            const int64_t budget = (160 * 1024) / occ - 1280 - (p->rowmap ? 1024 : 0);
                             const int64_t free_b = budget - fixed - nb * align256(astage) - nb * 256;
                             if (free_b <= 0) continue;
                             // patches are whole 1 KB copy slots of four waves (256 granules)

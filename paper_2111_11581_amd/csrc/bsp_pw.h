@@ -42,6 +42,7 @@ __global__ __launch_bounds__(kThreads, pw_occ((int)sizeof(E), MODE, TM)) void k_
     constexpr int GE = 16 / (int)sizeof(E);  // elements per granule
     extern __shared__ __attribute__((aligned(256))) unsigned char lds[];
     __shared__ float s_bias[kMaxMBRows];
+    __shared__ int s_orow[MAP ? kMaxMBRows : 1];   // output row of each row of the m-block (row map)
 
     // workgroup -> (range of pixel tiles, m-block); each XCD (workgroup id % 8) gets
     // a contiguous range of logical ids, the m-blocks of a tile range adjacent
@@ -206,18 +207,13 @@ __global__ __launch_bounds__(kThreads, pw_occ((int)sizeof(E), MODE, TM)) void k_
         const int p0 = oh * a.Wo + 4 * gi;
         const int nvalid = pix_ok ? max(0, min(4, a.Wo - 4 * gi)) : 0;
         const float qnan = __builtin_nanf("");
-        // row map (kept filter of each computed row): loaded, and waited for, before the
-        // first store, since the kernel counts its outstanding stores by hand
+        // row map (kept filter of each computed row), staged in LDS at the start
         int omap[TM][4] = {};
         if constexpr (MAP) {
 #pragma unroll
-            for (int t2 = 0; t2 < TM; ++t2) {
-                const int gm = mt_first + m_loc0 + t2;
-                const int mt_in = gm - (gm / a.mt_per_group) * a.mt_per_group;
+            for (int t2 = 0; t2 < TM; ++t2)
 #pragma unroll
-                for (int i = 0; i < 4; ++i) omap[t2][i] = a.rowmap[mt_in * kMT + 4 * kg + i];
-            }
-            wait_vm_all();
+                for (int i = 0; i < 4; ++i) omap[t2][i] = s_orow[(m_loc0 + t2) * kMT + 4 * kg + i];
         }
         int n = 0;
 #pragma unroll
@@ -280,12 +276,14 @@ __global__ __launch_bounds__(kThreads, pw_occ((int)sizeof(E), MODE, TM)) void k_
     };
 
     // ---- work items (tile, chunk), NB buffers, copies NB - 1 items ahead ----
-    if (a.bias)
+    if (a.bias || MAP)
         for (int r = tid; r < a.MBT * kMT; r += kThreads) {
             const int gm = mt_first + r / kMT;
             const int gidx = gm / a.mt_per_group;
             const int orow = gidx * a.group_rows + (gm - gidx * a.mt_per_group) * kMT + r % kMT;
-            s_bias[r] = orow < a.R ? a.bias[MAP ? a.rowmap[orow] : orow] : 0.f;
+            const int out = MAP ? (orow < a.R ? a.rowmap[orow] : 0) : orow;
+            if constexpr (MAP) s_orow[r] = out;
+            if (a.bias) s_bias[r] = orow < a.R ? a.bias[out] : 0.f;
         }
     const int NB = a.NB;
     const int nchx = max(nch, 1);

@@ -164,6 +164,25 @@ def sweep_settings(cin=256, cout=256, h=56, w=56, k=3, batch=64, blocks=(4, 8, 1
     return st
 
 
+def network_settings(layers, blocks=(4, 8, 16, 32, 64, 0), rates=(4,)):
+    """Settings of a network's conv layers (distinct shapes): every block size at each
+    rate, column and row blocks for every layer and block-punched blocks for K x K
+    kernels (K > 1), plus the whole-matrix reference of each regularity.  ``layers``
+    holds (cin, cout, h, w, k, stride, batch) tuples."""
+    seen, st = set(), []
+    for cin, cout, h, w, k, stride, batch in layers:
+        key = (cin, cout, h, w, k, stride, batch)
+        if key in seen:
+            continue
+        seen.add(key)
+        regs = (0, 1, 4) if k > 1 else (0, 1)
+        for reg in regs:
+            for b in blocks:
+                for r in rates:
+                    st.append(Setting(cin, cout, h, w, k, k, stride, k // 2, batch, reg, b, b, r))
+    return st
+
+
 def measure(settings, reps: int = 10, rounds: int = 10, seed: int = 1234, device=None) -> LatencyModel:
     """Times the library's forward call for each setting (bf16): a graph of ``reps``
     back-to-back launches of the layer (the test model of ten layers of one setting,
@@ -171,7 +190,7 @@ def measure(settings, reps: int = 10, rounds: int = 10, seed: int = 1234, device
     Weights and activations are seeded normal draws made on the device (He-normal
     weights): the latency depends on the shapes and the kept structure only."""
     import torch
-    from . import BF16, ConvShape, Scheme, bsp_version
+    from . import BF16, BspError, ConvShape, Scheme, bsp_version
     from .layers import PackedLayer
 
     dev = torch.device(device or "cuda:0")
@@ -186,7 +205,11 @@ def measure(settings, reps: int = 10, rounds: int = 10, seed: int = 1234, device
         y = torch.empty(s.batch, s.cout, s.ho, s.wo, dtype=torch.bfloat16, device=dev)
         scheme = Scheme(rows, cols, s.bh, s.bw, s.regularity, s.rate, s.kh * s.kw)
         conv = ConvShape(s.batch, s.cin, s.h, s.w, s.kh, s.kw, s.stride, s.stride, s.pad, s.pad)
-        p = PackedLayer(scheme, BF16, wd, conv=conv)
+        try:
+            p = PackedLayer(scheme, BF16, wd, conv=conv)
+        except BspError as e:   # a setting the library does not run is left out of the model
+            print(f"skipped {s.key()}: {e}", flush=True)
+            continue
         p.conv2d(x, y, s.batch, BF16)
         torch.cuda.synchronize(dev)
         g = torch.cuda.CUDAGraph()
@@ -270,6 +293,8 @@ def _main(argv=None):
     b.add_argument("--cin", type=int, default=256)
     b.add_argument("--hw", type=int, default=56)
     b.add_argument("--batch", type=int, default=64)
+    b.add_argument("--resnet50", action="store_true",
+                   help="the distinct ResNet-50 v1.5 conv shapes at 224x224 (rate 4) instead of the sweep layer")
     s = sub.add_parser("select", help="block size per regularity and rate from a saved model")
     s.add_argument("--model", required=True)
     s.add_argument("--beta", type=float, default=0.2)
@@ -281,7 +306,12 @@ def _main(argv=None):
         print(report(LatencyModel.load(a.model), tuple(a.betas)))
         return 0
     if a.cmd == "build":
-        st = sweep_settings(cin=a.cin, cout=a.cin, h=a.hw, w=a.hw, batch=a.batch, references=True)
+        if a.resnet50:
+            from synthetic import workload   # layer shapes only
+            st = network_settings([(l.cin, l.cout, l.h, l.w, l.kh, l.sh, a.batch) for l in workload(3)
+                                   if l.kind == "conv" and not (l.kh == 7)])
+        else:
+            st = sweep_settings(cin=a.cin, cout=a.cin, h=a.hw, w=a.hw, batch=a.batch, references=True)
         m = measure(st)
         m.save(a.out)
         for k in sorted(m.ms):

@@ -113,3 +113,16 @@ def test_block_punched_blocks_are_filters_by_channels():
     s = Setting(256, 128, 56, 56, 3, 3, 1, 1, 64, 4, 16, 8, 4)
     assert s.area() == 16 * 8 * 9 and "punched 16x8 r4" in s.key()
     assert Setting(256, 128, 56, 56, 3, 3, 1, 1, 64, 4, 0, 0, 4).area() == 128 * 256 * 9
+
+
+def test_network_settings_cover_every_distinct_layer():
+    from paper_2111_11581_amd.latency import network_settings
+    layers = [(64, 64, 56, 56, 1, 1, 64), (64, 64, 56, 56, 3, 1, 64), (64, 64, 56, 56, 1, 1, 64),
+              (256, 512, 56, 56, 1, 2, 64)]
+    st = network_settings(layers, blocks=(8, 0), rates=(4,))
+    # 1x1: row and column; 3x3 also block-punched; repeated shapes once
+    assert len(st) == 2 * 2 + 3 * 2 + 2 * 2
+    assert {s.layer_key() for s in st} == {"1x1/1 64->64 56x56 b64", "3x3/1 64->64 56x56 b64",
+                                          "1x1/2 256->512 56x56 b64"}
+    assert all(s.pad == s.kh // 2 for s in st)
+    assert {s.regularity for s in st if s.kh == 3} == {0, 1, 4}
