@@ -54,7 +54,7 @@ def _sizes_from_oracle(R, C, bh, bw, reg, rate, khw=1):
 @pytest.mark.parametrize("R,C,bh,bw,reg,rate", [
     (64, 576, 16, 16, 1, 4), (64, 576, 8, 16, 1, 8), (256, 64, 32, 32, 0, 2), (37, 53, 8, 16, 1, 3),
     (37, 53, 8, 16, 0, 3), (40, 40, 0, 0, 1, 4), (40, 40, 0, 0, 0, 4), (96, 100, 32, 32, 1, 10),
-    (64, 147, 0, 0, 3, 1), (30, 20, 1, 1, 2, 4)])
+    (64, 147, 0, 0, 3, 1), (30, 20, 1, 1, 2, 4), (64, 576, 16, 32, 5, 2), (37, 53, 8, 16, 5, 3)])
 def test_packed_sizes_match_oracle_packing(bsp, R, C, bh, bw, reg, rate):
     s = bsp.Scheme(R, C, bh, bw, reg, rate)
     nv, ni, nr, nb = bsp.bsp_packed_sizes(s, None, bsp.BF16)

@@ -187,3 +187,60 @@ def test_unmodified_prune_copy_passes_the_pins(tmp_path):
 def test_planted_prune_mistake_is_caught(tmp_path, name):
     old, new = PRUNE_MUTATIONS[name]
     assert not _prune_pins_pass(_load_prune(tmp_path, name, old, new))
+
+
+# ----------------- block-punched, row + column, per-block counts, BCS ---
+# The planted copy replaces the oracle module seen by the pins of
+# tests/test_oracle_prune.py (hand-worked examples, the paper's BCS fragment,
+# brute force, reductions to column / row pruning); at least one must fail.
+EXT_MUTATIONS = {
+    "punched_location_axis_transposed": ("w3 = wg.reshape(R, cin, khw)",
+                                         "w3 = wg.reshape(R, khw, cin).transpose(0, 2, 1)"),
+    "punched_count_from_channels": ("k = _count(counts, i, j, kept_count(khw, rate))",
+                                    "k = _count(counts, i, j, kept_count(c1 - c0, rate))"),
+    "rowcol_rows_by_reversed_scores": (
+        "rows = top_k(group_scores(blk, ROW), kept_count(r1 - r0, rate))",
+        "rows = top_k(group_scores(blk, ROW)[::-1], kept_count(r1 - r0, rate))"),
+    "counts_ignored": ("    if counts is None:\n        return default", "    return default"),
+    "bcs_runs_never_merge": ("if r == 0 or not np.array_equal(cols[r], cols[r - 1]):", "if True:"),
+    "bcs_stride_holds_run_starts": ("            stride.append(len(compact))",
+                                    "            stride.append(len(compact) - len(cols[r]))"),
+}
+
+
+def _ext_pins_pass(P):
+    import tests.test_oracle_prune as T
+    saved = T.P
+    T.P = P
+    checks = [
+        lambda: [T.test_punched_golden_masks(c) for c in ("whole_block_rate2", "filter_blocks_rate2",
+                                                             "channel_blocks_rate4")],
+        lambda: [T.test_punched_brute_force_on_small_integer_blocks(s) for s in range(3)],
+        lambda: T.test_punched_with_one_channel_blocks_is_column_pruning(2, 2, 9),
+        T.test_rowcol_golden_mask,
+        lambda: T.test_rowcol_reduces_to_column_and_row_blocks(4, 8, 2),
+        lambda: [T.test_counts_brute_force_on_small_integer_blocks(r) for r in (T.P.COL, T.P.ROW)],
+        T.test_counts_pack_lengths_and_edge_counts,
+        T.test_bcs_matches_the_paper_example_and_its_completion,
+        lambda: T.test_bcs_is_csr_with_shared_column_runs(16, 32, T.P.COL, 4),
+    ]
+    try:
+        for c in checks:
+            try:
+                c()
+            except Exception:
+                return False
+        return True
+    finally:
+        T.P = saved
+
+
+def test_extended_pins_pass_on_the_oracle():
+    from oracle import prune as P
+    assert _ext_pins_pass(P)
+
+
+@pytest.mark.parametrize("name", sorted(EXT_MUTATIONS))
+def test_planted_mistake_in_extended_schemes_is_caught(tmp_path, name):
+    old, new = EXT_MUTATIONS[name]
+    assert not _ext_pins_pass(_load_prune(tmp_path, name, old, new))
