@@ -33,6 +33,14 @@ Readings where the paper is silent (each listed in the design notes):
   every block keeps ceil(bh / rate) rows and ceil(bw / rate) columns, each set
   chosen by its own group norm on the block's weights; the block keeps their
   product (so the kept fraction is about 1 / rate^2);
+* pattern-based pruning of 3x3 kernels (Sec. 2.1 and Sec. 5.2.3, the comparison
+  point of block-punched pruning): every kept kernel keeps 4 weights in one of
+  a library of P patterns (the P most frequent top-4 location sets of the
+  layer's kernels, ties to the smaller location bit mask); a kernel takes the
+  library pattern with the largest kept squared norm (ties to the earlier
+  pattern); connectivity pruning keeps the ceil(n_kernels * 9 / (4 * rate))
+  kernels with the largest kept norm (ties to the lower kernel index o*Cin+c),
+  all of them when rate <= 9/4;
 * per-block kept counts (Sec. 4.1.1: the same or a different number per block;
   Sec. 4.2: the reweighted method sets a rate per block) are given by the
   caller as an array over the blocks in row-major order, replacing
@@ -46,7 +54,7 @@ from __future__ import annotations
 
 import numpy as np
 
-ROW, COL, UNSTRUCTURED, DENSE, PUNCHED, ROWCOL = 0, 1, 2, 3, 4, 5
+ROW, COL, UNSTRUCTURED, DENSE, PUNCHED, ROWCOL, PATTERN = 0, 1, 2, 3, 4, 5, 6
 
 
 def kept_count(extent: int, rate: int) -> int:
@@ -129,6 +137,37 @@ def punched_mask(wg: np.ndarray, khw: int, bh: int, bw: int, rate: int, counts=N
     return mask.reshape(R, C)
 
 
+def pattern_kept_kernels(n_kernels: int, rate: int, khw: int = 9) -> int:
+    """Kernels kept by connectivity pruning: ceil(n * khw / (4 * rate)), at most n."""
+    return min(n_kernels, (n_kernels * khw + 4 * rate - 1) // (4 * rate))
+
+
+def pattern_mask(wg: np.ndarray, khw: int, n_patterns: int, rate: int) -> np.ndarray:
+    """Pattern-based mask of a GEMM-form fp64 conv weight (R x Cin*khw), 4 kept
+    weights per kept kernel (Sec. 2.1), library and connectivity as in the header."""
+    wg = np.asarray(wg, dtype=np.float64)
+    R, C = wg.shape
+    cin = C // khw
+    sq = (wg * wg).reshape(R * cin, khw)                  # kernel k = o * Cin + c
+    own = [int(sum(1 << int(l) for l in top_k(sq[k], 4))) for k in range(R * cin)]
+    counts = {}
+    for code in own:
+        counts[code] = counts.get(code, 0) + 1
+    library = sorted(counts, key=lambda code: (-counts[code], code))[:n_patterns]
+    locs = [[l for l in range(khw) if (code >> l) & 1] for code in library]
+    best_pat = np.zeros(R * cin, dtype=np.int64)
+    best = np.zeros(R * cin)
+    for k in range(R * cin):
+        vals = [sum(sq[k, l] for l in ls) for ls in locs]   # ascending location order
+        best_pat[k] = int(np.argmax(vals))                 # first maximum: the earlier pattern
+        best[k] = vals[best_pat[k]]
+    keep = top_k(best, pattern_kept_kernels(R * cin, rate, khw))
+    mask = np.zeros((R * cin, khw), dtype=np.uint8)
+    for k in keep:
+        mask[k, locs[best_pat[k]]] = 1
+    return mask.reshape(R, C)
+
+
 def prune_mask(wg: np.ndarray, bh: int, bw: int, regularity: int, rate: int, khw: int = 1,
                counts=None) -> np.ndarray:
     """Mask (uint8, R x C) of the kept weights of a GEMM-form fp64 matrix
@@ -140,6 +179,8 @@ def prune_mask(wg: np.ndarray, bh: int, bw: int, regularity: int, rate: int, khw
     mask = np.zeros((R, C), dtype=np.uint8)
     if regularity == PUNCHED:
         return punched_mask(wg, max(int(khw), 1), bh, bw, rate, counts)
+    if regularity == PATTERN:   # bh: library size (0: 8)
+        return pattern_mask(wg, int(khw), int(bh) or 8, rate)
     if regularity == ROWCOL:
         if counts is not None:
             raise ValueError("per-block counts are not defined for simultaneous row and column pruning")
@@ -209,6 +250,11 @@ def mask_is_valid(mask: np.ndarray, bh: int, bw: int, regularity: int, rate: int
         return bool(np.all(mask == 1))
     if regularity == UNSTRUCTURED:
         return int(mask.sum()) == kept_count(R * C, rate)
+    if regularity == PATTERN:
+        per = mask.reshape(-1, khw).sum(axis=1)
+        codes = {tuple(r) for r in mask.reshape(-1, khw) if r.sum()}
+        return bool(np.all((per == 0) | (per == 4)) and (per == 4).sum() == pattern_kept_kernels(len(per), rate, khw)
+                    and len(codes) <= (bh or 8))
     if regularity == ROWCOL:
         for r0, r1 in block_ranges(R, bh):
             for c0, c1 in block_ranges(C, bw):
@@ -254,7 +300,7 @@ def pack(w_stored: np.ndarray, mask: np.ndarray, bh: int, bw: int, regularity: i
     w_stored = np.asarray(w_stored)
     mask = np.asarray(mask, dtype=np.uint8)
     R, C = mask.shape
-    if regularity in (DENSE, UNSTRUCTURED):
+    if regularity in (DENSE, UNSTRUCTURED, PATTERN):
         vals = np.where(mask == 1, w_stored, np.zeros_like(w_stored))
         return {"indices": np.zeros(0, np.int32), "rowptr": np.zeros(0, np.int32),
                 "values": vals.reshape(-1).copy()}
@@ -282,7 +328,7 @@ def unpack(packed: dict, R: int, C: int, bh: int, bw: int, regularity: int, like
     """Inverse of ``pack``: the masked dense matrix in the stored dtype."""
     out = np.zeros((R, C), dtype=np.asarray(like).dtype)
     vals, idx, ptr = packed["values"], packed["indices"], packed["rowptr"]
-    if regularity in (DENSE, UNSTRUCTURED):
+    if regularity in (DENSE, UNSTRUCTURED, PATTERN):
         return vals.reshape(R, C).copy()
     off = 0
     if regularity in (COL, PUNCHED, ROWCOL):

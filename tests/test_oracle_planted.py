@@ -205,6 +205,12 @@ EXT_MUTATIONS = {
     "bcs_runs_never_merge": ("if r == 0 or not np.array_equal(cols[r], cols[r - 1]):", "if True:"),
     "bcs_stride_holds_run_starts": ("            stride.append(len(compact))",
                                     "            stride.append(len(compact) - len(cols[r]))"),
+    "pattern_library_least_frequent": ("library = sorted(counts, key=lambda code: (-counts[code], code))[:n_patterns]",
+                                       "library = sorted(counts, key=lambda code: (counts[code], code))[:n_patterns]"),
+    "pattern_connectivity_floors": ("return min(n_kernels, (n_kernels * khw + 4 * rate - 1) // (4 * rate))",
+                                    "return min(n_kernels, (n_kernels * khw) // (4 * rate))"),
+    "pattern_keeps_weakest_kernels": ("    keep = top_k(best, pattern_kept_kernels(R * cin, rate, khw))",
+                                      "    keep = top_k(-best, pattern_kept_kernels(R * cin, rate, khw))"),
 }
 
 
@@ -223,6 +229,9 @@ def _ext_pins_pass(P):
         T.test_counts_pack_lengths_and_edge_counts,
         T.test_bcs_matches_the_paper_example_and_its_completion,
         lambda: T.test_bcs_is_csr_with_shared_column_runs(16, 32, T.P.COL, 4),
+        lambda: T.test_pattern_with_every_pattern_allowed_keeps_each_kernels_best_four(False),
+        T.test_pattern_library_is_the_most_frequent_sets_and_kernels_take_their_best_pattern,
+        lambda: [T.test_pattern_connectivity_keeps_the_strongest_kernels(r) for r in (3, 4, 8)],
     ]
     try:
         for c in checks:

@@ -467,3 +467,59 @@ def test_rowcol_pack_roundtrip_and_invalid_mask():
     r, c = np.argwhere(m == 1)[0]
     bad[r, c] = 0                               # no longer a product of a row and a column set
     assert not P.mask_is_valid(bad, bh, bw, P.ROWCOL, 3)
+
+
+# ---------------------------------------------------- pattern-based (3x3) ---
+# Sec. 2.1 / Sec. 5.2.3: 4 weights per kernel in one of a library of patterns, and
+# connectivity pruning of whole kernels beyond 9/4.
+
+@pytest.mark.parametrize("integer", [False, True])
+def test_pattern_with_every_pattern_allowed_keeps_each_kernels_best_four(integer):
+    rng = np.random.default_rng(31)
+    w = (rng.integers(-4, 5, size=(6, 5, 9)).astype(np.float64) if integer    # exact sums, many ties
+         else rng.standard_normal((6, 5, 9)))
+    m = P.prune_mask(w.reshape(6, -1), 126, 0, P.PATTERN, 2, khw=9).reshape(30, 9)
+    for k, kern in enumerate(w.reshape(30, 9)):
+        s = kern ** 2
+        best = max(itertools.combinations(range(9), 4), key=lambda t: (sum(s[i] for i in t), [-i for i in t]))
+        got = tuple(np.nonzero(m[k])[0])
+        if integer:   # ties: any maximising set of the library may be taken
+            assert len(got) == 4 and sum(s[i] for i in got) == sum(s[i] for i in best)
+        else:
+            assert got == best
+
+
+def test_pattern_library_is_the_most_frequent_sets_and_kernels_take_their_best_pattern():
+    A, Bs, Cs = (0, 1, 2, 4), (4, 5, 7, 8), (1, 3, 4, 6)
+    kern = []
+    for n, pat in ((10, A), (6, Bs), (3, Cs)):
+        for i in range(n):
+            k = np.full(9, 0.1 + 0.01 * i)
+            k[list(pat)] = 2.0 + 0.1 * i
+            kern.append(k)
+    w = np.array(kern)                                                   # 19 kernels: 19 filters x 1 channel
+    m = P.prune_mask(w, 2, 0, P.PATTERN, 2, khw=9)
+    codes = {tuple(np.nonzero(r)[0]) for r in m}
+    assert codes <= {A, Bs}                                              # library = the two most frequent
+    for r, k in zip(m, kern):                                            # each kernel: its best library pattern
+        best = max((A, Bs), key=lambda t: sum(k[i] ** 2 for i in t))
+        assert tuple(np.nonzero(r)[0]) == best
+
+
+@pytest.mark.parametrize("rate", [2, 3, 4, 8, 16])
+def test_pattern_connectivity_keeps_the_strongest_kernels(rate):
+    rng = np.random.default_rng(rate)
+    R, cin = 12, 10
+    w = rng.standard_normal((R, cin * 9))
+    m = P.prune_mask(w, 8, 0, P.PATTERN, rate, khw=9)
+    assert P.mask_is_valid(m, 8, 0, P.PATTERN, rate, khw=9)
+    per = m.reshape(-1, 9).sum(axis=1)
+    n_keep = P.pattern_kept_kernels(R * cin, rate)
+    assert (per == 4).sum() == n_keep and set(per.tolist()) <= {0, 4}
+    assert n_keep == min(R * cin, math.ceil(R * cin * 9 / (4 * rate)))
+    kept_norm = ((w.reshape(-1, 9) ** 2) * m.reshape(-1, 9)).sum(axis=1)
+    # every dropped kernel's best library pattern is no stronger than any kept kernel's
+    lib = {tuple(np.nonzero(r)[0]) for r in m.reshape(-1, 9) if r.sum()}
+    best = np.array([max(sum(k[i] ** 2 for i in t) for t in lib) for k in w.reshape(-1, 9)])
+    if n_keep < R * cin:
+        assert best[per == 0].max() <= kept_norm[per == 4].min() + 1e-12
