@@ -59,11 +59,18 @@ typedef enum {
     BSP_DENSE = 3,          /* nothing removed                                 */
     BSP_PUNCHED = 4,        /* kernel locations removed per block of filters x
                                input channels (Sec. 4.1.2, Eq. 4)              */
-    BSP_ROWCOL = 5          /* rows and columns removed in the same block
+    BSP_ROWCOL = 5,         /* rows and columns removed in the same block
                                (Eqs. 2 and 3 together, Sec. 4.2): a block keeps
                                ceil(bh/rate) rows x ceil(bw/rate) columns;
                                packed like BSP_COL with zeros for its removed
                                rows; no per-block counts                       */
+    BSP_PATTERN = 6         /* pattern-based pruning of 3x3 kernels (Sec. 2.1,
+                               the comparison point of Sec. 5.2.3): 4 weights
+                               per kept kernel in one of a library of bh
+                               patterns (0 -> 8; the most frequent top-4 sets),
+                               connectivity pruning keeps ceil(kernels*9 /
+                               (4*rate)) kernels; khw must be 9; packed and run
+                               like BSP_UNSTRUCTURED                           */
 } bsp_regularity;
 
 typedef struct {

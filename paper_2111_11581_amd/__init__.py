@@ -14,13 +14,13 @@ import ctypes
 import os
 
 __all__ = [
-    "F32", "BF16", "ROW", "COL", "UNSTRUCTURED", "DENSE", "PUNCHED", "ROWCOL", "BspError", "Scheme", "ConvShape",
+    "F32", "BF16", "ROW", "COL", "UNSTRUCTURED", "DENSE", "PUNCHED", "ROWCOL", "PATTERN", "BspError", "Scheme", "ConvShape",
     "lib", "lib_path", "bsp_packed_sizes", "bsp_prune", "bsp_pack", "bsp_unpack", "bsp_conv2d",
     "bsp_linear", "bsp_maxpool2x2", "bsp_status_string", "bsp_version", "bsp_to_bcs",
 ]
 
 F32, BF16 = 0, 1
-ROW, COL, UNSTRUCTURED, DENSE, PUNCHED, ROWCOL = 0, 1, 2, 3, 4, 5
+ROW, COL, UNSTRUCTURED, DENSE, PUNCHED, ROWCOL, PATTERN = 0, 1, 2, 3, 4, 5, 6
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _LIB_PATH = os.path.join(_HERE, "_build", "libbsp.so")

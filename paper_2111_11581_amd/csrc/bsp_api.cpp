@@ -74,7 +74,7 @@ bsp_status bsp_pack(const bsp_scheme *scheme, bsp_dtype wdt, const void *w, cons
     bsp_status st = make_plan(scheme, conv, wdt, 0, &p);
     if (st != BSP_OK) return st;
     if ((st = check_scheme_for_prune(p)) != BSP_OK) return st;
-    if (p.reg != BSP_DENSE && p.reg != BSP_UNSTRUCTURED && (!indices || !rowptr)) return BSP_EINVAL;
+    if (p.reg != BSP_DENSE && p.reg != BSP_UNSTRUCTURED && p.reg != BSP_PATTERN && (!indices || !rowptr)) return BSP_EINVAL;
     if (p.S > kMaxSteps) return BSP_EUNSUPPORTED;
     return run_pack(p, w, mask, values, indices, rowptr, (uint8_t *)dev_tiles, S(stream));
 }
@@ -85,7 +85,7 @@ bsp_status bsp_unpack(const bsp_scheme *scheme, bsp_dtype wdt, const void *value
     Plan p;
     bsp_status st = make_plan(scheme, nullptr, wdt, -1, &p);
     if (st != BSP_OK) return st;
-    if (p.reg != BSP_DENSE && p.reg != BSP_UNSTRUCTURED && (!indices || !rowptr)) return BSP_EINVAL;
+    if (p.reg != BSP_DENSE && p.reg != BSP_UNSTRUCTURED && p.reg != BSP_PATTERN && (!indices || !rowptr)) return BSP_EINVAL;
     return launch_unpack(p, values, indices, rowptr, w_out, S(stream)) == hipSuccess ? BSP_OK
                                                                                       : BSP_EDEVICE;
 }

@@ -261,6 +261,12 @@ inline int div_up(int a, int b) { return (a + b - 1) / b; }
 inline int64_t div_up64(int64_t a, int64_t b) { return (a + b - 1) / b; }
 inline int kept_count(int extent, int rate) { return (extent + rate - 1) / rate; }
 
+// Kernels kept by the connectivity pruning of pattern-based pruning (3x3 kernels,
+// 4 weights each): ceil(n * 9 / (4 * rate)), at most n.
+inline int pattern_kept(int n, int rate) {
+    return (int)std::min<int64_t>(n, ((int64_t)n * 9 + 4 * rate - 1) / (4 * (int64_t)rate));
+}
+
 // Kept groups of block b (row-major over block-rows x block-columns): the caller's
 // count, else ceil(groups / rate).
 int block_count(const Plan &p, int b);

@@ -145,6 +145,15 @@ __global__ void k_validate_all(const uint8_t *__restrict__ mask, size_t n, int n
     if (c) atomicAdd(count, c);
 }
 
+// Pattern-based masks: every 3x3 kernel keeps 0 or 4 weights.
+__global__ void k_validate_kernels4(const uint8_t *__restrict__ mask, int n_kernels, int *flag) {
+    for (int k = blockIdx.x * blockDim.x + threadIdx.x; k < n_kernels; k += gridDim.x * blockDim.x) {
+        int c = 0;
+        for (int l = 0; l < 9; ++l) c += mask[(size_t)k * 9 + l];
+        if (c != 0 && c != 4) atomicOr(flag, 1);
+    }
+}
+
 __global__ void k_check_count(const unsigned int *count, unsigned int k, int *flag) {
     if (*count != k) atomicOr(flag, 1);
 }
@@ -534,7 +543,7 @@ bsp_status pack_t(const Plan &p, const E *w, const uint8_t *mask, E *values, int
     if (hipMemcpyAsync(tiles, &h, sizeof(h), hipMemcpyHostToDevice, st) != hipSuccess)
         return BSP_EDEVICE;
     const size_t n = (size_t)p.R * p.C;
-    const bool blocked = p.reg != BSP_DENSE && p.reg != BSP_UNSTRUCTURED;
+    const bool blocked = p.reg != BSP_DENSE && p.reg != BSP_UNSTRUCTURED && p.reg != BSP_PATTERN;
     // canonical list offsets (from the scheme and its counts) and the counts, for the
     // kernels below; both copies complete before this call returns (it synchronises)
     std::vector<int32_t> rp(blocked ? (size_t)p.n_rowptr : 0);
@@ -592,6 +601,11 @@ bsp_status pack_t(const Plan &p, const E *w, const uint8_t *mask, E *values, int
         k_validate_all<<<grid_for(n), 256, 0, st>>>(mask, n, p.reg == BSP_DENSE, flag, count);
         if (p.reg == BSP_UNSTRUCTURED)
             k_check_count<<<1, 1, 0, st>>>(count, (unsigned int)((n + p.rate - 1) / p.rate), flag);
+        if (p.reg == BSP_PATTERN) {
+            const int nk = (int)(n / 9);
+            k_validate_kernels4<<<grid_for(nk), 256, 0, st>>>(mask, nk, flag);
+            k_check_count<<<1, 1, 0, st>>>(count, 4u * (unsigned int)pattern_kept(nk, p.rate), flag);
+        }
     }
     int hflag = 0;
     if (hipMemcpyAsync(&hflag, flag, sizeof(int), hipMemcpyDeviceToHost, st) != hipSuccess ||
@@ -650,7 +664,7 @@ template <typename E>
 hipError_t unpack_t(const Plan &p, const E *values, const int32_t *indices, const int32_t *rowptr, E *out,
                     hipStream_t st) {
     const size_t n = (size_t)p.R * p.C;
-    if (p.reg == BSP_DENSE || p.reg == BSP_UNSTRUCTURED) {
+    if (p.reg == BSP_DENSE || p.reg == BSP_UNSTRUCTURED || p.reg == BSP_PATTERN) {
         return hipMemcpyAsync(out, values, n * sizeof(E), hipMemcpyDeviceToDevice, st);
     }
     k_fill<E><<<grid_for(n), 256, 0, st>>>(out, n, (E)0);

@@ -307,7 +307,9 @@ bsp_status make_plan(const bsp_scheme *s, const bsp_conv_shape *conv, bsp_dtype 
     if (!s || !p) return BSP_EINVAL;
     std::memset(p, 0, sizeof(*p));
     if (s->rows <= 0 || s->cols <= 0 || s->bh < 0 || s->bw < 0 || s->rate < 1) return BSP_EINVAL;
-    if (s->regularity < BSP_ROW || s->regularity > BSP_ROWCOL) return BSP_EINVAL;
+    if (s->regularity < BSP_ROW || s->regularity > BSP_PATTERN) return BSP_EINVAL;
+    if (s->regularity == BSP_PATTERN && (s->khw != 9 || s->cols % 9 != 0 || s->bh > 126 || s->counts))
+        return BSP_EINVAL;
     if (s->regularity == BSP_ROWCOL && s->counts) return BSP_EUNSUPPORTED;
     if (wdt != BSP_F32 && wdt != BSP_BF16) return BSP_EINVAL;
     const int khw = s->regularity == BSP_PUNCHED ? std::max(s->khw, 1) : 1;
@@ -331,6 +333,12 @@ bsp_status make_plan(const bsp_scheme *s, const bsp_conv_shape *conv, bsp_dtype 
         p->nbc = div_up(p->C, p->bw_eff);
     }
     p->nbr = div_up(p->R, p->bh_eff);
+    if (p->reg == BSP_PATTERN) {   // no blocks; bh is the library size
+        p->khw = 9;
+        p->bh_eff = s->bh ? s->bh : 8;
+        p->bw_eff = p->C;
+        p->nbr = p->nbc = 1;
+    }
     if (s->counts && (p->reg == BSP_ROW || p->reg == BSP_COL || p->reg == BSP_PUNCHED)) {
         if ((int64_t)p->nbr * p->nbc > (1 << 24)) return BSP_EUNSUPPORTED;
         uint32_t h = 2166136261u;

@@ -16,6 +16,8 @@
 // block.
 #include <hip/hip_runtime.h>
 
+#include <hipcub/hipcub.hpp>
+
 #include "bsp_kernels.h"
 
 namespace bsp {
@@ -162,6 +164,127 @@ __global__ void k_prune_rowcol(const E *__restrict__ w, uint8_t *__restrict__ ma
         const int p = e / nc, q = e - p * nc;
         mask[(size_t)(r0 + p) * C + c0 + q] = kr[p] & kc[q];
     }
+}
+
+__global__ void k_fill_u8(uint8_t *p, size_t n, uint8_t v);
+
+// ---- pattern-based pruning of 3x3 kernels (Sec. 2.1, Sec. 5.2.3) ------------------
+// A kernel k = o * Cin + c holds w[o][c * khw + l].  Each kernel's own top-4 location
+// set (squares, ties to the lower location) is counted in a histogram of bit masks;
+// the library is the n_lib most frequent masks (ties to the smaller mask); every
+// kernel takes the library pattern with the largest kept squared norm, summed in
+// ascending location order (ties to the earlier pattern); connectivity keeps the
+// kernels with the largest such norm (a stable descending sort: ties to the lower
+// kernel index).
+template <typename E>
+__global__ void k_pattern_own(const E *__restrict__ w, int n_kernels, int khw, unsigned int *__restrict__ hist) {
+    for (int k = blockIdx.x * blockDim.x + threadIdx.x; k < n_kernels; k += gridDim.x * blockDim.x) {
+        double sq[9];
+        for (int l = 0; l < 9; ++l) {
+            const double v = ld_f64(w, (size_t)k * khw + l);
+            sq[l] = v * v;
+        }
+        int code = 0;
+        for (int l = 0; l < 9; ++l) {
+            int rank = 0;
+            for (int h = 0; h < 9; ++h) rank += (sq[h] > sq[l]) || (sq[h] == sq[l] && h < l);
+            if (rank < 4) code |= 1 << l;
+        }
+        atomicAdd(&hist[code], 1u);
+    }
+}
+
+__global__ void k_pattern_library(const unsigned int *__restrict__ hist, int n_lib, int *__restrict__ lib) {
+    __shared__ unsigned int h[512];
+    const int c = threadIdx.x;   // 512 threads, one per 9-bit mask
+    h[c] = hist[c];
+    if (c < n_lib) lib[c] = -1;
+    __syncthreads();
+    const unsigned int n = h[c];
+    if (n == 0) return;
+    int rank = 0;
+    for (int d = 0; d < 512; ++d) rank += (h[d] > n) || (h[d] == n && d < c);
+    if (rank < n_lib) lib[rank] = c;
+}
+
+template <typename E>
+__global__ void k_pattern_assign(const E *__restrict__ w, int n_kernels, int khw, const int *__restrict__ lib,
+                                 int n_lib, double *__restrict__ score, int *__restrict__ idx,
+                                 int *__restrict__ pat) {
+    for (int k = blockIdx.x * blockDim.x + threadIdx.x; k < n_kernels; k += gridDim.x * blockDim.x) {
+        double sq[9];
+        for (int l = 0; l < 9; ++l) {
+            const double v = ld_f64(w, (size_t)k * khw + l);
+            sq[l] = v * v;
+        }
+        double best = -1.0;
+        int bp = 0;
+        for (int j = 0; j < n_lib; ++j) {
+            const int code = lib[j];
+            if (code < 0) break;   // fewer distinct masks than library entries
+            double s = 0.0;
+            for (int l = 0; l < 9; ++l)
+                if ((code >> l) & 1) s += sq[l];
+            if (s > best) {
+                best = s;
+                bp = j;
+            }
+        }
+        score[k] = best;
+        idx[k] = k;
+        pat[k] = bp;
+    }
+}
+
+__global__ void k_pattern_mask(const int *__restrict__ order, int n_keep, int n_kernels, const int *__restrict__ lib,
+                               const int *__restrict__ pat, int khw, uint8_t *__restrict__ mask) {
+    // order[0 .. n_keep) are the kept kernels; each thread writes one kept kernel's row
+    // of 9 bytes, the mask having been cleared before
+    for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n_keep; i += gridDim.x * blockDim.x) {
+        const int k = order[i];
+        const int code = lib[pat[k]];
+        for (int l = 0; l < 9; ++l) mask[(size_t)k * khw + l] = (code >> l) & 1;
+    }
+    (void)n_kernels;
+}
+
+template <typename E>
+static hipError_t prune_pattern(const Plan &p, const E *w, uint8_t *mask, hipStream_t st) {
+    const int n = p.R * (p.C / p.khw);
+    const int n_lib = p.bh_eff;   // library size (planner: bh, 0 -> 8)
+    const int n_keep = pattern_kept(n, p.rate);
+    size_t cub_bytes = 0;
+    hipError_t e = hipcub::DeviceRadixSort::SortPairsDescending(nullptr, cub_bytes, (const uint64_t *)nullptr,
+                                                                (uint64_t *)nullptr, (const int *)nullptr,
+                                                                (int *)nullptr, n, 0, 64, st);
+    if (e != hipSuccess) return e;
+    // scratch: histogram, library, scores, sorted keys, indices, sorted indices, patterns, sort temp
+    const size_t off_lib = 512 * 4, off_sc = 4096, off_keys = off_sc + 8 * (size_t)n,
+                 off_idx = off_keys + 8 * (size_t)n, off_idx2 = off_idx + 4 * (size_t)n,
+                 off_pat = off_idx2 + 4 * (size_t)n, off_tmp = (off_pat + 4 * (size_t)n + 255) / 256 * 256;
+    char *scr = nullptr;
+    e = hipMallocAsync((void **)&scr, off_tmp + cub_bytes, st);
+    if (e != hipSuccess) return e;
+    unsigned int *hist = (unsigned int *)scr;
+    int *lib = (int *)(scr + off_lib);
+    double *score = (double *)(scr + off_sc);
+    uint64_t *keys2 = (uint64_t *)(scr + off_keys);
+    int *idx = (int *)(scr + off_idx), *idx2 = (int *)(scr + off_idx2), *pat = (int *)(scr + off_pat);
+    const int blocks = (int)std::min<int64_t>(4096, (n + 255) / 256);
+    k_fill_u8<<<4, 256, 0, st>>>((uint8_t *)hist, 512 * 4, 0);
+    k_fill_u8<<<(int)std::min<size_t>(8192, ((size_t)p.R * p.C + 255) / 256), 256, 0, st>>>(mask, (size_t)p.R * p.C, 0);
+    k_pattern_own<E><<<blocks, 256, 0, st>>>(w, n, p.khw, hist);
+    k_pattern_library<<<1, 512, 0, st>>>(hist, n_lib, lib);
+    k_pattern_assign<E><<<blocks, 256, 0, st>>>(w, n, p.khw, lib, n_lib, score, idx, pat);
+    // non-negative doubles sort like their bit patterns; the sort is stable
+    e = hipcub::DeviceRadixSort::SortPairsDescending(scr + off_tmp, cub_bytes, (const uint64_t *)score, keys2, idx,
+                                                      idx2, n, 0, 64, st);
+    if (e == hipSuccess) {
+        k_pattern_mask<<<blocks, 256, 0, st>>>(idx2, n_keep, n, lib, pat, p.khw, mask);
+        e = hipGetLastError();
+    }
+    const hipError_t e2 = hipFreeAsync(scr, st);
+    return e != hipSuccess ? e : e2;
 }
 
 __global__ void k_fill_u8(uint8_t *p, size_t n, uint8_t v) {
@@ -321,6 +444,10 @@ hipError_t launch_prune(const Plan &p, const void *w, uint8_t *mask, hipStream_t
     if (p.reg == BSP_UNSTRUCTURED) {
         return p.dt == BSP_F32 ? prune_unstructured(p, (const float *)w, mask, st)
                                : prune_unstructured(p, (const uint16_t *)w, mask, st);
+    }
+    if (p.reg == BSP_PATTERN) {
+        return p.dt == BSP_F32 ? prune_pattern(p, (const float *)w, mask, st)
+                               : prune_pattern(p, (const uint16_t *)w, mask, st);
     }
     // per-block counts: a stream-ordered device copy, freed after the launch; the call
     // then waits for its stream, so the caller's host array may go once it returns

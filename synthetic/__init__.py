@@ -12,5 +12,5 @@ from .gen import (  # noqa: F401
 )
 from .workloads import (  # noqa: F401
     Scheme, ConvLayer, LinearLayer, workload, WORKLOADS,
-    ROW, COL, UNSTRUCTURED, DENSE, PUNCHED, ROWCOL,
+    ROW, COL, UNSTRUCTURED, DENSE, PUNCHED, ROWCOL, PATTERN,
 )

@@ -15,9 +15,9 @@ from __future__ import annotations
 import math
 from dataclasses import dataclass, field
 
-ROW, COL, UNSTRUCTURED, DENSE, PUNCHED, ROWCOL = 0, 1, 2, 3, 4, 5
+ROW, COL, UNSTRUCTURED, DENSE, PUNCHED, ROWCOL, PATTERN = 0, 1, 2, 3, 4, 5, 6
 REG_NAMES = {ROW: "row", COL: "col", UNSTRUCTURED: "unstructured", DENSE: "dense", PUNCHED: "punched",
-             ROWCOL: "row+col"}
+             ROWCOL: "row+col", PATTERN: "pattern"}
 
 
 @dataclass(frozen=True)

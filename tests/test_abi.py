@@ -212,6 +212,16 @@ def test_packed_sizes_with_per_block_counts_match_oracle_packing(bsp, R, C, bh, 
     assert bsp.bsp_packed_sizes(s2, None, bsp.BF16)[:2] != (nv, ni) or cnt2.flat[0] == cnt.flat[0]
 
 
+def test_pattern_scheme_sizes_and_errors(bsp):
+    s = bsp.Scheme(64, 64 * 9, 8, 0, bsp.PATTERN, 4, 9)
+    nv, ni, nr, nb = bsp.bsp_packed_sizes(s, None, bsp.BF16)
+    assert (nv, ni, nr) == _sizes_from_oracle(64, 64 * 9, 8, 0, bsp.PATTERN, 4, 9)
+    L = bsp.lib()
+    out = [ctypes.c_int64() for _ in range(4)]
+    for bad in (bsp.Scheme(64, 64 * 9, 8, 0, bsp.PATTERN, 4, 4), bsp.Scheme(64, 64 * 9, 127, 0, bsp.PATTERN, 4, 9)):
+        assert L.bsp_packed_sizes(ctypes.byref(bad), None, 1, *[ctypes.byref(o) for o in out]) == -1
+
+
 def test_per_block_counts_out_of_range_are_rejected(bsp):
     L = bsp.lib()
     out = [ctypes.c_int64() for _ in range(4)]

@@ -8,7 +8,7 @@ import pytest
 
 from oracle import prune as OP
 from synthetic import (workload, draw, draw_layer, seed_for, ConvLayer, LinearLayer, ROW, COL, UNSTRUCTURED, DENSE,
-                       PUNCHED, ROWCOL)
+                       PUNCHED, ROWCOL, PATTERN)
 from tests.helpers import DT, to_dev, from_dev, as_f64, rel_l2, oracle_mask, oracle_conv, oracle_linear, out_to_f64
 
 pytestmark = pytest.mark.gpu
@@ -591,3 +591,47 @@ def test_bcs_encoding_matches_oracle(B, kind):
     assert np.array_equal(vals, ref["weights"])
     if kind == "merged block-rows":
         assert len(ref["occurrence"]) - 1 == 3
+
+
+# --------------------------------------------------- pattern-based (3x3) ---
+PATTERN_MATS = [  # name, R, cin, n_patterns, rate, dtype, dist
+    ("64x64 8 patterns r4", 64, 64, 8, 4, "bf16", ("normal", 0, 0.05)),
+    ("37x20 16 patterns r2 f32", 37, 20, 16, 2, "f32", ("normal", 0, 1.0)),
+    ("256x256 8 patterns r8", 256, 256, 8, 8, "bf16", ("normal", 0, 0.03)),
+    ("ties 48x16 4 patterns r3", 48, 16, 4, 3, "bf16", ("ties",)),
+]
+
+
+@pytest.mark.parametrize("i", range(len(PATTERN_MATS)), ids=[m[0] for m in PATTERN_MATS])
+def test_pattern_prune_and_pack_bit_exact(B, i):
+    name, R, cin, npat, rate, dtype, dist = PATTERN_MATS[i]
+    C = cin * 9
+    w = _mat(70 + i, R, C, dtype, dist)
+    scheme = B.Scheme(R, C, npat, 0, PATTERN, rate, 9)
+    layer = _layers().PackedLayer(scheme, DT[dtype], to_dev(w, dtype))
+    m_ref = oracle_mask(w, dtype, scheme)
+    m_gpu = layer.mask.cpu().numpy().reshape(R, C)
+    assert np.array_equal(m_gpu, m_ref), f"{name}: {int((m_gpu != m_ref).sum())} mask entries differ"
+    assert OP.mask_is_valid(m_gpu, npat, 0, PATTERN, rate, khw=9)
+    back = from_dev(layer.unpack(), dtype).reshape(R, C)
+    assert np.array_equal(back.view(np.uint8), np.where(m_ref == 1, w, np.zeros_like(w)).view(np.uint8))
+
+
+def test_pattern_conv_matches_oracle_and_pack_rejects_a_three_weight_kernel(B):
+    import torch
+    layer = ConvLayer("pattern", 2, 32, 12, 12, 48, 3, 3, 1, 1, 1, 1, 8, 0, PATTERN, 4, "bf16", ("normal", 0, 1.0),
+                      ("normal", 0, (2.0 / 288) ** 0.5), relu=True)
+    d = draw_layer(layer, 8, 300, with_bias=True)
+    L, y = run_conv(B, layer, d["x"], d["w"], "bf16", "bf16", d["bias"], True)
+    m = L.mask.cpu().numpy().reshape(48, -1)
+    assert np.array_equal(m, oracle_mask(d["w"], "bf16", layer.scheme))
+    ref = oracle_conv(d["x"], d["w"], m, "bf16", layer, bias=d["bias"], relu=True)
+    assert rel_l2(out_to_f64(from_dev(y, "bf16"), "bf16"), ref) <= TOL["bf16"]
+    bad = m.copy().reshape(-1, 9)
+    k = int(np.argmax(bad.sum(axis=1)))
+    bad[k, np.nonzero(bad[k])[0][0]] = 0
+    with pytest.raises(B.BspError) as e:
+        _layers().PackedLayer(layer.scheme, B.BF16, to_dev(d["w"].reshape(48, -1), "bf16"),
+                              conv=B.ConvShape(2, 32, 12, 12, 3, 3, 1, 1, 1, 1),
+                              mask=torch.from_numpy(bad.reshape(-1)).cuda())
+    assert e.value.status == -4
