@@ -25,7 +25,7 @@ import math
 import sys
 from dataclasses import asdict, dataclass
 
-REG_NAMES = {0: "row", 1: "col", 2: "unstructured", 3: "dense", 4: "punched"}
+REG_NAMES = {0: "row", 1: "col", 2: "unstructured", 3: "dense", 4: "punched", 6: "pattern"}
 BLOCK_REGS = (0, 1, 4)   # regularities with a block size (the rule selects among them)
 
 
@@ -52,6 +52,8 @@ class Setting:
             b = "-"
         elif self.regularity == 2:
             b = "1x1"
+        elif self.regularity == 6:
+            b = f"{self.bh}p"
         else:
             b = "whole" if self.bh == 0 and self.bw == 0 else f"{self.bh}x{self.bw}"
         return (f"{self.kh}x{self.kw}/{self.stride} {self.cin}->{self.cout} {self.h}x{self.w} b{self.batch} "
@@ -160,6 +162,8 @@ def sweep_settings(cin=256, cout=256, h=56, w=56, k=3, batch=64, blocks=(4, 8, 1
           for b in blocks for reg in regularities for r in rates]
     if references:
         st += [Setting(cin, cout, h, w, k, k, 1, k // 2, batch, 2, 1, 1, r) for r in rates]
+        if k == 3:   # pattern-based pruning (8 patterns), the 3x3 comparison point of Sec. 5.2.3
+            st += [Setting(cin, cout, h, w, k, k, 1, k // 2, batch, 6, 8, 0, r) for r in rates]
         st.append(Setting(cin, cout, h, w, k, k, 1, k // 2, batch, 3, 0, 0, 1))
     return st
 
@@ -262,10 +266,11 @@ def report(model: LatencyModel, betas=(0.0, 0.1, 0.2, 0.5)) -> str:
                 name = "whole" if b == (0, 0) else f"{b[0]}x{b[1]}"
                 out.append(f"| {name} | " + " | ".join(cells) + " |")
             out.append("")
-        refs = [s for s in st if s.regularity in (2, 3)]
+        refs = [s for s in st if s.regularity in (2, 3, 6)]
         if refs:
+            names = {2: "unstructured", 3: "dense", 6: "pattern (8 patterns)"}
             out.append("reference points: " + ", ".join(
-                f"{'dense' if s.regularity == 3 else f'unstructured {s.rate}x'} {model.latency(s) * 1e3:.1f} us"
+                f"{names[s.regularity]}{'' if s.regularity == 3 else f' {s.rate}x'} {model.latency(s) * 1e3:.1f} us"
                 for s in sorted(refs, key=lambda s: (s.regularity, s.rate))) + "\n")
         out.append("rule choice (smallest block within (1 + beta) of whole-matrix blocks, latency per dense MAC):\n")
         out.append("| regularity | rate | " + " | ".join(f"beta {b:g}" for b in betas) + " |")

@@ -98,7 +98,8 @@ def test_sweep_settings_cover_the_block_size_sweep():
     assert st[0].macs() == 64 * 256 * 56 * 56 * 256 * 9
     # with the reference points: unstructured at each rate and the dense layer, all distinct
     sr = sweep_settings(references=True)
-    assert len(sr) == 77 and len({s.key() for s in sr}) == 77
+    assert len(sr) == 81 and len({s.key() for s in sr}) == 81
+    assert sorted(s.rate for s in sr if s.regularity == 6) == [2, 4, 8, 16]
     assert sorted(s.rate for s in sr if s.regularity == 2) == [2, 4, 8, 16]
     assert [s.rate for s in sr if s.regularity == 3] == [1]
 
