@@ -109,7 +109,7 @@ typedef struct {
  *   COL, PUNCHED, ROWCOL: values = rows * kept_per_row, indices = n_block_rows * kept_per_row,
  *        rowptr = n_block_rows + 1 (PUNCHED keeps Cin*ceil(khw/rate) per row)
  *   ROW: values = nnz, indices = kept rows summed over blocks, rowptr = n_blocks + 1
- *   DENSE / UNSTRUCTURED: values = rows * cols, indices = rowptr = 0. */
+ *   DENSE / UNSTRUCTURED / PATTERN: values = rows * cols, indices = rowptr = 0. */
 bsp_status bsp_packed_sizes(const bsp_scheme *scheme, const bsp_conv_shape *conv_or_null,
                             bsp_dtype wdt, int64_t *n_values, int64_t *n_indices,
                             int64_t *n_rowptr, int64_t *dev_tile_bytes);
@@ -118,8 +118,8 @@ bsp_status bsp_packed_sizes(const bsp_scheme *scheme, const bsp_conv_shape *conv
  * norm of Eq. 4, one-shot magnitude selection of Sec. 5.1): w is the GEMM-form
  * weight matrix, row-major rows x cols, of dtype wdt; mask (rows x cols bytes,
  * row-major) receives 1 for kept and 0 for removed weights.  Async.  The
- * whole-layer magnitude ranking of BSP_UNSTRUCTURED allocates a small scratch
- * buffer on `stream` (stream-ordered) and frees it before returning.  With
+ * whole-layer rankings of BSP_UNSTRUCTURED and BSP_PATTERN allocate a scratch
+ * buffer on `stream` (stream-ordered) and free it before returning.  With
  * per-block counts the counts go to such a buffer and the call waits for
  * `stream` before returning. */
 bsp_status bsp_prune(const bsp_scheme *scheme, bsp_dtype wdt, const void *w, uint8_t *mask,
@@ -138,7 +138,7 @@ bsp_status bsp_prune(const bsp_scheme *scheme, bsp_dtype wdt, const void *w, uin
  *     ROW: for block b = i*n_block_cols + j, indices[rowptr[b] .. rowptr[b+1])
  *          are its kept rows ascending; its values are those rows restricted
  *          to the block's columns, [t][q_local], blocks stored in order b.
- *     DENSE / UNSTRUCTURED: values = W * mask (rows x cols); indices and
+ *     DENSE / UNSTRUCTURED / PATTERN: values = W * mask (rows x cols); indices and
  *          rowptr are not written (may be NULL).
  *   dev_tiles: the kernels' private layout (pre-decoded gather offsets for
  *     the given conv geometry, MFMA-ordered weight tiles, channel-chunk
