@@ -186,7 +186,8 @@ static bool plan_pointwise(Plan *p, int span_req, int n_mt, int mpg, int astep) 
                             // buffers win where the model alone cannot tell; these enter as
                             // factors on the modelled time.
                             const double prior = (occ == 2 ? 1.0 : 1.3) * (nsub == 2 ? 1.0 : 1.15) *
-                                                 (TM == 4 || p->esize == 4 ? 1.0 : 1.15) * (nb == 2 ? 1.0 : 1.3);
+                                                 (TM == 4 || p->esize == 4 || p->SW == 2 ? 1.0 : 1.15) *
+                                                 (nb == 2 ? 1.0 : (p->SW == 2 ? 2.0 : 1.3));
                             const double cyc = (std::max(std::max(t_hbm, t_l2), std::max(std::max(t_lds, t_mfma), t_lat)) +
                                                 (KS > 1 ? 1500.0 : 0.0)) * prior;
                             if (cyc < best * (1 - 1e-9)) {
