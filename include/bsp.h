@@ -153,8 +153,9 @@ bsp_status bsp_pack(const bsp_scheme *scheme, bsp_dtype wdt, const void *w, cons
                     void *values, int32_t *indices, int32_t *rowptr, void *dev_tiles,
                     const bsp_conv_shape *conv_or_null, void *stream);
 
-/* Inverse of the canonical packing: w_masked_out (rows x cols, dtype) =
- * W * mask, bit-exact.  Async.  For tests and checkpoints. */
+/* Inverse of the canonical packing (the compact storage of Sec. 4.3 read
+ * back): w_masked_out (rows x cols, dtype) = W * mask, bit-exact.  Async.
+ * For tests and checkpoints. */
 bsp_status bsp_unpack(const bsp_scheme *scheme, bsp_dtype wdt, const void *values,
                       const int32_t *indices, const int32_t *rowptr, void *w_masked_out,
                       void *stream);
@@ -187,7 +188,9 @@ bsp_status bsp_conv2d(const bsp_scheme *scheme, const bsp_conv_shape *shape, bsp
                       bsp_dtype out_dt, const void *x, const void *dev_tiles,
                       const float *bias_or_null, int32_t relu, void *y, void *stream);
 
-/* Forward of a pruned FC layer on feature-major activations:
+/* Forward of a pruned FC layer on feature-major activations (an FC layer's
+ * weight matrix is its own GEMM form, pruned in blocks as in Sec. 4.1.1; the
+ * layer computation with weights W_i and bias b_i of Sec. 4.2):
  *   y[o][b] = bias[o] + sum_{kept k} W[o][k] * x[k][b], then ReLU if relu.
  * x: [cols][batch], y: [rows][batch].  dev_tiles packed with conv_or_null =
  * NULL.  Async. */
@@ -196,7 +199,9 @@ bsp_status bsp_linear(const bsp_scheme *scheme, int32_t batch, bsp_dtype in_dt, 
                       int32_t relu, void *y, void *stream);
 
 /* 2x2 max pooling, stride 2 (floor), NCHW, same dtype in and out: the glue
- * between VGG-16 stages.  y is [n][c][h/2][w/2].  Async. */
+ * between VGG-16 stages (not part of the pruning method).  y is
+ * [n][c][h/2][w/2]; each output is the largest of its four inputs, copied
+ * bit-exactly; a NaN in a window makes the output NaN.  Async. */
 bsp_status bsp_maxpool2x2(bsp_dtype dt, int32_t n, int32_t c, int32_t h, int32_t w,
                           const void *x, void *y, void *stream);
 

@@ -194,6 +194,7 @@ def bsp_conv2d(scheme, shape, in_dt: int, out_dt: int, x, dev_tiles, bias, relu:
     wo = (sh.w + 2 * sh.pad_w - sh.kw) // sh.stride_w + 1
     _need("x", x, sh.n * sh.cin * sh.h * sh.w * _esize(in_dt))
     _need("y", y, sh.n * s.rows * ho * wo * _esize(out_dt))
+    _need("dev_tiles", dev_tiles, bsp_packed_sizes(s, sh, in_dt)[3])
     if bias is not None:
         _need("bias", bias, s.rows * 4)
     _check("bsp_conv2d", lib().bsp_conv2d(ctypes.byref(s), ctypes.byref(sh), int(in_dt), int(out_dt),
@@ -206,6 +207,7 @@ def bsp_linear(scheme, batch: int, in_dt: int, out_dt: int, x, dev_tiles, bias, 
     s = _scheme(scheme)
     _need("x", x, s.cols * batch * _esize(in_dt))
     _need("y", y, s.rows * batch * _esize(out_dt))
+    _need("dev_tiles", dev_tiles, bsp_packed_sizes(s, None, in_dt)[3])
     if bias is not None:
         _need("bias", bias, s.rows * 4)
     _check("bsp_linear", lib().bsp_linear(ctypes.byref(s), int(batch), int(in_dt), int(out_dt), _p(x),

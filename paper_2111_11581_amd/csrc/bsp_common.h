@@ -243,6 +243,7 @@ struct PwArgs {
     FastDiv div_Ho;               // group row -> (image, row in image)
     FastDiv div_nmb;              // workgroup -> (pixel tile, m-block)
     const int32_t *rowmap;        // output row of each computed row (row-mapped kernels only)
+    int Rout;                     // output channels (R is the number of computed rows)
 };
 
 // Workgroups per CU the pointwise kernel's register budget allows (its launch

@@ -35,16 +35,23 @@ static fwd_fn pick(int dt, int mode, int TM, int TPG, int KS, bool map) {
 // Output rows of the filters that whole-width row pruning removed: every element is
 // the epilogue of a zero sum (bias, ReLU, rounding), as the forward kernels would write
 // it.  A workgroup walks planes (image, pruned row) of `plane` contiguous elements;
-// 16-byte stores where the plane allows them.
+// 16-byte stores where the plane allows them.  Tiles packed for another plan (header
+// check): the list of pruned rows is not read; rows R - n_pruned .. R - 1 get NaN,
+// the forward kernel fills the others with NaN, so the whole output is NaN.
 template <typename E>
-__global__ void k_fill_pruned(E *__restrict__ y, const int32_t *__restrict__ pruned, const float *__restrict__ bias,
-                              int relu, int n_pruned, int64_t n_planes, int64_t plane, int64_t img_stride,
-                              int64_t ch_stride) {
+__global__ void k_fill_pruned(E *__restrict__ y, const uint8_t *__restrict__ tiles, int64_t off_pruned, uint32_t fp_lo,
+                              uint32_t fp_hi, const float *__restrict__ bias, int relu, int R, int n_pruned,
+                              int64_t n_planes, int64_t plane, int64_t img_stride, int64_t ch_stride) {
     constexpr int VE = 16 / (int)sizeof(E);
+    const TileHeader *hdr = (const TileHeader *)tiles;
+    const bool ok = hdr->magic == kMagic && hdr->fp_lo == fp_lo && hdr->fp_hi == fp_hi;
+    const int32_t *pruned = (const int32_t *)(tiles + off_pruned);
     for (int64_t pi = blockIdx.x; pi < n_planes; pi += gridDim.x) {
         const int64_t img = pi / n_pruned;
-        const int o = pruned[pi - img * n_pruned];
-        const float v = fwd::epi(0.f, bias ? bias[o] : 0.f, relu);
+        const int j = (int)(pi - img * n_pruned);
+        const int o = ok ? pruned[j] : R - n_pruned + j;
+        if (o < 0 || o >= R) continue;   // not a row of the output
+        const float v = ok ? fwd::epi(0.f, bias ? bias[o] : 0.f, relu) : __builtin_nanf("");
         E ev;
         if constexpr (sizeof(E) == 2) ev = fwd::f32_to_bf16_rne(v);
         else ev = v;
@@ -68,13 +75,13 @@ static hipError_t launch_fill_pruned(const Plan &p, int64_t n_img, int64_t plane
     const int64_t n_planes = n_img * n_pruned;
     if (!p.rowmap || n_planes <= 0 || plane <= 0) return hipSuccess;
     const int grid = (int)std::min<int64_t>(n_planes, 16384);
-    const int32_t *pr = (const int32_t *)(tiles + p.off_pruned);
+    const uint32_t lo = (uint32_t)p.fingerprint, hi = (uint32_t)(p.fingerprint >> 32);
     if (out_bf16)
-        k_fill_pruned<uint16_t><<<grid, 256, 0, st>>>((uint16_t *)y, pr, bias, relu, n_pruned, n_planes, plane,
-                                                      img_stride, ch_stride);
+        k_fill_pruned<uint16_t><<<grid, 256, 0, st>>>((uint16_t *)y, tiles, p.off_pruned, lo, hi, bias, relu, p.R,
+                                                      n_pruned, n_planes, plane, img_stride, ch_stride);
     else
-        k_fill_pruned<float><<<grid, 256, 0, st>>>((float *)y, pr, bias, relu, n_pruned, n_planes, plane,
-                                                   img_stride, ch_stride);
+        k_fill_pruned<float><<<grid, 256, 0, st>>>((float *)y, tiles, p.off_pruned, lo, hi, bias, relu, p.R,
+                                                   n_pruned, n_planes, plane, img_stride, ch_stride);
     return hipGetLastError();
 }
 
@@ -97,6 +104,7 @@ static hipError_t launch_pw(const Plan &p, int n, const void *x, const uint8_t *
     a.relu = relu;
     a.out_bf16 = out_bf16;
     a.R = p.RK;
+    a.Rout = p.R;
     a.rowmap = p.rowmap ? (const int32_t *)(tiles + p.off_rowmap) : nullptr;
     a.SW = p.SW;
     int64_t images;

@@ -776,16 +776,19 @@ __global__ __launch_bounds__(kFwdThreads, 1) void k_fwd(ConvArgs a) {
         const bool plain = ok && !a.bias && !a.relu;
         // row map (kept filter of each computed row): loaded, and waited for, before the
         // first store, since the kernel counts its outstanding stores by hand
+        // (tiles of another plan: no map is read and the rows below stay in range)
         int omap[TM][4] = {};
         if constexpr (MAP) {
+            if (ok) {
 #pragma unroll
-            for (int t = 0; t < TM; ++t) {
-                const int gm = mt_first + m_loc0 + t;
-                const int mt_in = gm - (gm / a.mt_per_group) * a.mt_per_group;
+                for (int t = 0; t < TM; ++t) {
+                    const int gm = mt_first + m_loc0 + t;
+                    const int mt_in = gm - (gm / a.mt_per_group) * a.mt_per_group;
 #pragma unroll
-                for (int i = 0; i < 4; ++i) omap[t][i] = a.rowmap[mt_in * kMT + 4 * kg + i];
+                    for (int i = 0; i < 4; ++i) omap[t][i] = a.rowmap[mt_in * kMT + 4 * kg + i];
+                }
+                wait_vm_all();
             }
-            wait_vm_all();
         }
         int n = 0;
 #pragma unroll
@@ -797,7 +800,7 @@ __global__ __launch_bounds__(kFwdThreads, 1) void k_fwd(ConvArgs a) {
                 const int rig = mt_in * kMT + 4 * kg + i;              // row inside the list group
                 const int row = gidx * a.group_rows + rig;
                 const bool row_ok = rig < a.group_rows && row < a.R;
-                const int orow = MAP ? omap[t][i] : row;
+                const int orow = MAP ? (ok ? min(max(omap[t][i], 0), a.Rout - 1) : min(row, a.Rout - 1)) : row;
                 float o[4];
                 if (plain) {
 #pragma unroll
@@ -889,7 +892,8 @@ __global__ __launch_bounds__(kFwdThreads, 1) void k_fwd(ConvArgs a) {
             const int gm = mt_first + r / kMT;
             const int gidx = gm / a.mt_per_group;
             const int row = gidx * a.group_rows + (gm - gidx * a.mt_per_group) * kMT + r % kMT;
-            s_bias[r] = row < a.R ? a.bias[MAP ? a.rowmap[row] : row] : 0.f;
+            const int orow = MAP ? (ok ? min(max(a.rowmap[row], 0), a.Rout - 1) : min(row, a.Rout - 1)) : row;
+            s_bias[r] = row < a.R ? a.bias[orow] : 0.f;
         }
     }
     __syncthreads();

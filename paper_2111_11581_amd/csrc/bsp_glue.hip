@@ -21,13 +21,14 @@ __global__ void k_maxpool2x2(const E *__restrict__ x, E *__restrict__ y, int nc,
         const int r = (int)(i - plane * ho * wo);
         const int oh = r / wo, ow = r - oh * wo;
         const E *p = x + (plane * h + 2 * oh) * w + 2 * ow;
-        // max of the four values; the winner is copied bit-exactly
+        // max of the four values, the winner copied bit-exactly; a NaN wins over
+        // every number and the first NaN in window order is kept (NaN propagates)
         E best = p[0];
         float bv = ld(&p[0]);
         const E *cand[3] = {p + 1, p + w, p + w + 1};
         for (int k = 0; k < 3; ++k) {
             const float v = ld(cand[k]);
-            if (v > bv) {
+            if (bv == bv && !(v <= bv)) {
                 bv = v;
                 best = *cand[k];
             }

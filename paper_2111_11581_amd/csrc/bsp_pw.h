@@ -281,9 +281,11 @@ __global__ __launch_bounds__(kThreads, pw_occ((int)sizeof(E), MODE, TM)) void k_
             const int gm = mt_first + r / kMT;
             const int gidx = gm / a.mt_per_group;
             const int orow = gidx * a.group_rows + (gm - gidx * a.mt_per_group) * kMT + r % kMT;
-            const int out = MAP ? (orow < a.R ? a.rowmap[orow] : 0) : orow;
+            // tiles of another plan (!ok): no map is read; output rows stay in range
+            const int out = MAP ? (orow < a.R && ok ? min(max(a.rowmap[orow], 0), a.Rout - 1) : min(orow, a.Rout - 1))
+                                : orow;
             if constexpr (MAP) s_orow[r] = out;
-            if (a.bias) s_bias[r] = orow < a.R ? a.bias[out] : 0.f;
+            if (a.bias) s_bias[r] = orow < a.R ? a.bias[out] : 0.f;   // out < Rout: in the bias array
         }
     const int NB = a.NB;
     const int nchx = max(nch, 1);

@@ -136,3 +136,43 @@ def test_whole_matrix_row_pruning_leaves_bias_on_pruned_filters(oracle_direct):
     y = oracle_direct.conv2d(x, w * m, b, (1, 1), (1, 1))
     for o in pruned:
         assert np.all(y[:, o] == b[o])
+
+
+# ------------------------------------------------------------- maxpool glue ---
+def _f(v):
+    return float(v) if not isinstance(v, str) else float(v.replace("inf", "inf"))
+
+
+def _maxpool_brute(x):
+    """2x2 / stride 2 / floor max pooling by plain loops; NaN propagates."""
+    N, C, H, W = x.shape
+    out = np.empty((N, C, H // 2, W // 2))
+    for n in range(N):
+        for c in range(C):
+            for i in range(H // 2):
+                for j in range(W // 2):
+                    vals = [float(x[n, c, 2 * i + a, 2 * j + b]) for a in (0, 1) for b in (0, 1)]
+                    out[n, c, i, j] = float("nan") if any(v != v for v in vals) else max(vals)
+    return out
+
+
+def test_maxpool_golden_example():
+    from oracle import glue
+    g = GOLD["maxpool_2x2"]
+    x = np.vectorize(_f)(np.array(g["x"], dtype=object)).astype(np.float64)
+    want = np.vectorize(_f)(np.array(g["y"], dtype=object)).astype(np.float64)
+    got = glue.maxpool2x2(x)
+    assert got.shape == want.shape == (1, 2, 2, 2)
+    assert np.array_equal(got, want, equal_nan=True)
+
+
+@pytest.mark.parametrize("shape", [(2, 3, 4, 4), (1, 2, 5, 7), (3, 1, 9, 2), (1, 1, 1, 6)])
+def test_maxpool_matches_brute_force_with_nonfinite_values(shape):
+    from oracle import glue
+    rng = np.random.default_rng(sum(shape))
+    x = rng.integers(-3, 4, size=shape).astype(np.float64)       # many ties
+    flat = x.reshape(-1)
+    idx = rng.permutation(flat.size)
+    flat[idx[: max(1, flat.size // 10)]] = -np.inf
+    flat[idx[max(1, flat.size // 10): max(2, flat.size // 7)]] = np.nan
+    assert np.array_equal(glue.maxpool2x2(x), _maxpool_brute(x), equal_nan=True)

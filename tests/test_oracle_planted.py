@@ -124,6 +124,9 @@ PRUNE_MUTATIONS = {
                           "return max(1, int(extent) // int(rate))"),
     "abs_instead_of_square": ("sq = block * block", "sq = np.abs(block)"),
     "keeps_smallest": ("order = np.argsort(-scores, kind=\"stable\")", "order = np.argsort(scores, kind=\"stable\")"),
+    "ragged_block_anchored_at_the_end": (
+        "return [(s, min(s + b, extent)) for s in range(0, extent, b)]",
+        "return [(max(0, e - b), e) for e in range(int(extent), 0, -b)][::-1]"),
 }
 
 
@@ -154,6 +157,12 @@ def _prune_pins_pass(P) -> bool:
     if P.prune_mask(W, 2, 4, P.COL, 2).tolist() != g["col_2x4_rate2"]["mask"]:
         return False
     if P.prune_mask(W, 2, 4, P.ROW, 2).tolist() != g["row_2x4_rate2"]["mask"]:
+        return False
+    gr = GOLD["ragged_5x7"]
+    Wr = np.array(gr["W"], dtype=np.float64)
+    if P.prune_mask(Wr, 2, 3, P.COL, 2).tolist() != gr["col_2x3_rate2"]["mask"]:
+        return False
+    if P.prune_mask(Wr, 2, 3, P.ROW, 2).tolist() != gr["row_2x3_rate2"]["mask"]:
         return False
     rng = np.random.default_rng(11)
     for trial in range(40):
@@ -253,3 +262,106 @@ def test_extended_pins_pass_on_the_oracle():
 def test_planted_mistake_in_extended_schemes_is_caught(tmp_path, name):
     old, new = EXT_MUTATIONS[name]
     assert not _ext_pins_pass(_load_prune(tmp_path, name, old, new))
+
+
+# ------------------------------------------------- parity gates themselves ---
+# The forward parity tests gate every output three ways (tests/helpers.check_output):
+# global rel-L2, rel-L2 per (image, output channel) plane, and an element-wise
+# rounding bound.  A stand-in for the kernel that accumulates in fp32 and rounds to
+# bf16 must pass all three; the same stand-in with one kept column of one output row
+# left out passes the global norm but must fail the other two.
+
+def _fp32_conv_bf16(x_bits, w_bits, mask, layer):
+    """fp32-accumulating conv (torch on the CPU) of the bf16 inputs, rounded to bf16."""
+    from tests.helpers import as_f64
+    x = torch.from_numpy(as_f64(x_bits, "bf16").astype(np.float32))
+    wm = (as_f64(w_bits, "bf16").reshape(layer.cout, -1) * mask).reshape(layer.w_shape).astype(np.float32)
+    y = torch.nn.functional.conv2d(x, torch.from_numpy(wm), stride=(layer.sh, layer.sw),
+                                   padding=(layer.ph, layer.pw))
+    return y.to(torch.bfloat16).to(torch.float64).numpy()
+
+
+def test_one_dropped_kept_column_fails_the_plane_and_element_gates(oracle_direct):
+    from synthetic import ConvLayer, COL, draw_layer
+    from tests.helpers import gate_conv, oracle_conv, oracle_mask, rel_l2
+    layer = ConvLayer("3x3 256@14 col16x32 r4", 1, 256, 14, 14, 256, 3, 3, 1, 1, 1, 1, 16, 32, COL, 4, "bf16",
+                      ("normal", 0, 1.0), ("normal", 0, (2.0 / 2304) ** 0.5))
+    d = draw_layer(layer, 9, 0)
+    m = oracle_mask(d["w"], "bf16", layer.scheme)
+    good = _fp32_conv_bf16(d["x"], d["w"], m, layer)
+    gate_conv(good, d["x"], d["w"], m, "bf16", "bf16", layer)
+    # output row 77 loses a kept column of median weight magnitude
+    m2 = m.reshape(layer.cout, -1).copy()
+    o = 77
+    kept = np.nonzero(m2[o])[0]
+    wo = np.abs(as_f64_bits(d["w"]).reshape(layer.cout, -1)[o, kept])
+    q = kept[np.argsort(wo)[len(kept) // 2]]
+    m2[o, q] = 0
+    bad = _fp32_conv_bf16(d["x"], d["w"], m2, layer)
+    ref = oracle_conv(d["x"], d["w"], m, "bf16", layer)
+    assert rel_l2(bad, ref) <= 5e-3        # the global norm alone lets it through
+    with pytest.raises(AssertionError, match="plane rel-L2|error bound"):
+        gate_conv(bad, d["x"], d["w"], m, "bf16", "bf16", layer)
+
+
+def as_f64_bits(w_bits):
+    from tests.helpers import as_f64
+    return as_f64(w_bits, "bf16")
+
+
+# --------------------------------------------------------------- maxpool ---
+GLUE_MUTATIONS = {
+    "window_one_row_down": ("x[:, :, 2 * i + 1, 2 * j], x[:, :, 2 * i + 1, 2 * j + 1]",
+                            "x[:, :, 2 * i + 2 - (2 * i + 2 >= H), 2 * j], x[:, :, 2 * i + 1, 2 * j + 1]"),
+    "nan_ignored": ("out[:, :, i, j] = np.maximum(np.maximum(", "out[:, :, i, j] = np.fmax(np.fmax("),
+    "ceil_instead_of_floor": ("Ho, Wo = H // 2, W // 2", "Ho, Wo = (H + 1) // 2, (W + 1) // 2"),
+    "min_for_one_pair": ("np.maximum(x[:, :, 2 * i + 1, 2 * j]", "np.minimum(x[:, :, 2 * i + 1, 2 * j]"),
+}
+
+
+def _load_glue(tmp_path, name, old, new):
+    src = open(os.path.join(ROOT, "oracle", "glue.py")).read()
+    assert src.count(old) == 1, name
+    if name == "nan_ignored":
+        src = src.replace(old, new).replace("np.maximum(x[:, :, 2 * i + 1", "np.fmax(x[:, :, 2 * i + 1")
+    else:
+        src = src.replace(old, new)
+    path = tmp_path / ("glue_%s.py" % name)
+    path.write_text(src)
+    spec = importlib.util.spec_from_file_location("planted_glue_%s" % name, str(path))
+    mod = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(mod)
+    return mod
+
+
+def _glue_pins_pass(G) -> bool:
+    import tests.test_oracle_direct as T
+    import oracle
+    saved = oracle.glue if hasattr(oracle, "glue") else None
+    import sys
+    saved_mod = sys.modules.get("oracle.glue")
+    sys.modules["oracle.glue"] = G
+    oracle.glue = G
+    try:
+        try:
+            T.test_maxpool_golden_example()
+            for shape in [(2, 3, 4, 4), (1, 2, 5, 7), (3, 1, 9, 2), (1, 1, 1, 6)]:
+                T.test_maxpool_matches_brute_force_with_nonfinite_values(shape)
+        except Exception:
+            return False
+        return True
+    finally:
+        if saved_mod is not None:
+            sys.modules["oracle.glue"] = saved_mod
+        if saved is not None:
+            oracle.glue = saved
+
+
+def test_unmodified_glue_copy_passes_the_pins(tmp_path):
+    assert _glue_pins_pass(_load_glue(tmp_path, "none", "import numpy as np", "import numpy as np"))
+
+
+@pytest.mark.parametrize("name", sorted(GLUE_MUTATIONS))
+def test_planted_maxpool_mistake_is_caught(tmp_path, name):
+    old, new = GLUE_MUTATIONS[name]
+    assert not _glue_pins_pass(_load_glue(tmp_path, name, old, new))

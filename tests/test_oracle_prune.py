@@ -46,6 +46,42 @@ def test_golden_row_mask_and_pack():
     assert pk["values"].tolist() == ex["values"]
 
 
+@pytest.mark.parametrize("reg", [P.COL, P.ROW])
+def test_golden_ragged_blocks_mask_and_pack(reg):
+    """Blocks anchored at (0, 0) with a ragged last block-row and block-column, worked
+    by hand (5x7 matrix, 2x3 blocks, rate 2)."""
+    g = GOLD["ragged_5x7"]
+    W = np.array(g["W"], dtype=np.float32)
+    ex = g["col_2x3_rate2" if reg == P.COL else "row_2x3_rate2"]
+    m = P.prune_mask(W.astype(np.float64), 2, 3, reg, 2)
+    assert m.tolist() == ex["mask"]
+    pk = P.pack(W, m, 2, 3, reg, 2)
+    assert pk["indices"].tolist() == ex["indices"]
+    assert pk["rowptr"].tolist() == ex["rowptr"]
+    assert pk["values"].tolist() == ex["values"]
+    assert P.mask_is_valid(m, 2, 3, reg, 2)
+
+
+def test_ragged_block_edges_without_the_oracles_block_ranges():
+    """The last block starts at a multiple of the block size: a column that the
+    last (ragged) block holds alone is always kept, whatever its score; a column of
+    a full block with the lowest score of its block is removed (rate 2, bw 3)."""
+    rng = np.random.default_rng(3)
+    for R, C, bh, bw in ((5, 7, 2, 3), (9, 10, 4, 3), (37, 53, 8, 16)):
+        W = rng.standard_normal((R, C))
+        W[:, C - 1] *= 1e-6                    # weakest column of all
+        m = P.prune_mask(W, bh, bw, P.COL, 2)
+        last0 = (C - 1) // bw * bw             # first column of the last block
+        width = C - last0
+        assert m[:, C - 1].all() == (width == 1)
+        assert m[:, last0:].sum(axis=1).tolist() == [-(-width // 2)] * R
+        Wr = rng.standard_normal((R, C))
+        Wr[R - 1, :] *= 1e-6
+        mr = P.prune_mask(Wr, bh, bw, P.ROW, 2)
+        first_last_row = (R - 1) // bh * bh
+        assert mr[R - 1, :].all() == (R - first_last_row == 1)
+
+
 def test_golden_whole_matrix_conv_taps():
     g = GOLD["conv_plus_3x3"]
     wg = np.array(g["w"], dtype=np.float64).reshape(1, 9)
