@@ -159,6 +159,7 @@ struct Plan {
     int lds_d, lds_a, lds_patch, lds_astage, lds_buf, lds_total;   // dynamic LDS bytes
     // pointwise kernel (1x1 without padding, stride 1 or 2; linear layers)
     int pw;                       // 1: the pointwise kernel runs this layer
+    int pl;                       // 1: the identity-list pointwise kernel (k_pl) runs it
     int NGR;                      // 16-byte granules per patch row (one channel of a tile)
     int gpg;                      // 4-pixel groups per granule
     int occ;                      // workgroups per CU the plan is sized for
@@ -244,6 +245,8 @@ struct PwArgs {
     FastDiv div_nmb;              // workgroup -> (pixel tile, m-block)
     const int32_t *rowmap;        // output row of each computed row (row-mapped kernels only)
     int Rout;                     // output channels (R is the number of computed rows)
+    int Cin;                      // input channels (in_features)
+    int SMAX;                     // steps per stage (identity-list kernel)
 };
 
 // Workgroups per CU the pointwise kernel's register budget allows (its launch

@@ -1,9 +1,16 @@
 // Launcher of the forward kernel: argument set-up and instantiation choice.  The
 // kernel template lives in bsp_fwd.h; its instantiations are compiled in
 // bsp_fwd_*.hip (one translation unit per element type and gather mode).
+#include "bsp_pl.h"
 #include "bsp_pw.h"
 
 namespace bsp {
+namespace pl {
+
+pl_fn pick_1(int NSUB, int TM, bool map);
+pl_fn pick_2(int NSUB, int TM, bool map);
+
+}  // namespace pl
 namespace pw {
 
 pw_fn pick_b1(int TM, int TPG, int KS, bool map);
@@ -105,6 +112,8 @@ static hipError_t launch_pw(const Plan &p, int n, const void *x, const uint8_t *
     a.out_bf16 = out_bf16;
     a.R = p.RK;
     a.Rout = p.R;
+    a.Cin = p.Cin;
+    a.SMAX = p.SMAX;
     a.rowmap = p.rowmap ? (const int32_t *)(tiles + p.off_rowmap) : nullptr;
     a.SW = p.SW;
     int64_t images;
@@ -158,8 +167,15 @@ static hipError_t launch_pw(const Plan &p, int n, const void *x, const uint8_t *
     a.div_nmb = make_fastdiv((uint32_t)p.n_mb);
     pw::pw_fn fn = nullptr;
     const bool map = p.rowmap != 0;
-    if (p.dt == BSP_F32) fn = p.SW == 1 ? pw::pick_f(p.TM, p.TPG, p.KS, map) : nullptr;
-    else fn = p.SW == 1 ? pw::pick_b1(p.TM, p.TPG, p.KS, map) : pw::pick_b2(p.TM, p.TPG, p.KS, map);
+    int threads = kThreads;
+    if (p.pl) {
+        fn = p.dt == BSP_BF16 ? (p.SW == 1 ? pl::pick_1(p.NSUB, p.TM, map) : pl::pick_2(p.NSUB, p.TM, map)) : nullptr;
+        threads = pl::kPlThreads;
+    } else if (p.dt == BSP_F32) {
+        fn = p.SW == 1 ? pw::pick_f(p.TM, p.TPG, p.KS, map) : nullptr;
+    } else {
+        fn = p.SW == 1 ? pw::pick_b1(p.TM, p.TPG, p.KS, map) : pw::pick_b2(p.TM, p.TPG, p.KS, map);
+    }
     if (!fn) return hipErrorInvalidValue;
     const int grid = (int)(div_up64(gv, 8) * 8);
     if (p.lds_total > 48 * 1024) {
@@ -167,7 +183,7 @@ static hipError_t launch_pw(const Plan &p, int n, const void *x, const uint8_t *
                                            p.lds_total);
         if (e != hipSuccess) return e;
     }
-    hipLaunchKernelGGL(fn, dim3(grid), dim3(kThreads), (size_t)p.lds_total, st, a);
+    hipLaunchKernelGGL(fn, dim3(grid), dim3(threads), (size_t)p.lds_total, st, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     return launch_fill_pruned(p, images, a.y_cs, a.y_is, a.y_cs, tiles, bias, relu, out_bf16, y, st);

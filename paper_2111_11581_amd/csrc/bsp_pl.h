@@ -1,0 +1,373 @@
+// Forward kernel of pointwise layers whose kept columns are one identity list (row
+// blocks stored with zeros for their removed rows, dense and unstructured layers):
+// 1x1 convolutions without padding at stride 1 or 2, and fully connected layers
+// (Sec. 4.2: the GEMM form of a 1x1 layer has one column per input channel).
+// Template; instantiated in bsp_pl_*.hip.
+//
+// With an identity list every 32-wide step of the K loop is 32 consecutive input
+// channels, so the loop needs no chunk table and no gather offsets: a step's operands
+// sit at fixed LDS offsets.  A workgroup has 8 waves and owns one m-block (MB rows)
+// and a run of pixel tiles (NP = 64 NSUB output pixels each):
+//  * waves 4-7 copy: per stage (SPS steps) each issues the same number of 16-byte
+//    direct-to-LDS copies: for every step, its share of the stage's input granules
+//    (32 channels x NP pixels) and, unless the m-block's weights stay in LDS for the
+//    whole run (copied once at the start), of its weight tiles (MB / 64 tiles of 1 KB);
+//    the sources are set up once per tile and advance by 32 channels per step.  Copies
+//    run NB - 1 stages ahead, so every wait is for a constant count;
+//  * waves 0-3 multiply: wave w works on sub-tile w % NSUB and m-tiles
+//    (w / NSUB) * TM .. + TM - 1; per step it reads its weights (one 16-byte LDS read
+//    per m-tile) and the 8 channels x 4 pixels of its lane (8-byte reads, 16-byte at
+//    stride 2) at compile-time offsets, re-packs them with v_perm into the B operands
+//    of 4 MFMA 16x16x32 bf16 and multiplies; steps of a stage are software-pipelined.
+//    At the end of a tile they add bias, apply ReLU, round to bf16 and store.
+// One barrier per stage; the stores of a finished tile overlap the next tile.
+#pragma once
+
+#include "bsp_fwd.h"
+
+namespace bsp {
+namespace pl {
+
+using namespace bsp::fwd;
+
+constexpr int kPlThreads = 512;
+
+// MODE 1: stride 1, a granule holds two 4-pixel groups; MODE 2: stride 2, a granule
+// holds the 8 input pixels of one group (the even ones are used).
+template <int MODE, int NSUB, int TM, bool MAP = false>
+__global__ __launch_bounds__(kPlThreads, 1) void k_pl(PwArgs a) {
+    typedef Gat<uint16_t, MODE> GT;
+    constexpr int Q = kWaves / NSUB;              // multiplying waves per sub-tile
+    constexpr int MT = TM * Q;                    // m-tiles of the m-block
+    constexpr int NP = 64 * NSUB;                 // output pixels of a tile
+    constexpr int RB = NP * 2 * MODE;             // patch bytes per channel
+    constexpr int GPC = RB / 16;                  // granules per channel
+    constexpr int PCOPY = 32 * GPC / kThreads;    // patch copies per producer wave and step
+    constexpr int WCOPY = MT / kWaves;            // weight copies per producer wave and step
+    static_assert(32 * GPC % kThreads == 0 && MT % kWaves == 0, "whole copies per wave");
+    constexpr int PB = 32 * RB;                   // LDS bytes of one step's patch
+    extern __shared__ __attribute__((aligned(256))) unsigned char lds[];
+    __shared__ float s_bias[kMaxMBRows];
+    __shared__ int s_orow[MAP ? kMaxMBRows : 1];
+
+    // workgroup -> (range of pixel tiles, m-block); each XCD (workgroup id % 8) gets
+    // a contiguous range of logical ids, the m-blocks of a tile range adjacent
+    const int per = gridDim.x >> 3;
+    const int lid = (int)(blockIdx.x & 7) * per + (int)(blockIdx.x >> 3);
+    if (lid >= a.grid_valid) return;
+    const int jr = (int)fdiv((uint32_t)lid, a.div_nmb);
+    const int mb = lid - jr * a.n_mb;
+    const int t_begin = jr * a.tiles_per_wg;
+    const int t_end = min(a.n_pt, t_begin + a.tiles_per_wg);
+    if (t_begin >= t_end) return;
+
+    const TileHeader *hdr = (const TileHeader *)a.tiles;
+    const bool ok = hdr->magic == kMagic && hdr->fp_lo == a.fp_lo && hdr->fp_hi == a.fp_hi;
+    const unsigned char *A_g = a.tiles + a.off_a;
+    const unsigned char *xb = (const unsigned char *)a.x;
+    const unsigned char *zero = a.tiles + kZeroOffset;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
+    const bool prod = wave >= kWaves;
+    const int rw = wave & (kWaves - 1);   // wave index inside its role
+    const int n16 = lane & 15, kg = lane >> 4;
+    const int ps = rw % NSUB, q = rw / NSUB;
+    const int m_loc0 = q * TM;
+    const int mt_first = mb * MT;
+    const int S = a.S;                    // steps (32 channels each) of the K loop
+    const int SPS = a.SMAX;               // steps per stage
+    const int NS = (S + SPS - 1) / SPS;   // stages per tile
+    const int NB = a.NB;
+    const bool res = a.resident;          // the m-block's weights stay in LDS ([m-tile][step], 1 KB each)
+    const int wcopy = res ? 0 : WCOPY;
+    const int stage_b = SPS * PB + (res ? 0 : SPS * MT * 1024);   // patches of the stage, then its weights
+    unsigned char *bufs = lds + (res ? MT * S * 1024 : 0);
+    const uint32_t lds0 = lds_addr(lds);
+    const uint32_t bufs0 = lds_addr(bufs);
+    const int n_items = (t_end - t_begin) * (ok ? NS : 1);
+
+    // ---- producers: copy k of a step fills LDS granules gid = (rw * PCOPY + k) * 64 + lane
+    // of the step's patch (byte 16 gid): channel c = gid / GPC, granule g = gid % GPC of
+    // the tile row; a wave's copies are 1 KB apart, so four share one M0 ----
+    const int xcs = (int)a.x_cs;
+    const uint32_t x_last = (uint32_t)(a.x_total - 8);   // last granule start inside x
+    int e_base[PCOPY];     // element offset of the copy's granule at its channel (channel 0 of the step)
+    int c_of[PCOPY];       // its channel within a step
+    bool g_live[PCOPY];    // the granule holds output pixels
+    int cur_tile = -1;
+    auto set_tile = [&](int t) {
+        if (t == cur_tile) return;
+        cur_tile = t;
+#pragma unroll
+        for (int k = 0; k < PCOPY; ++k) {
+            const int gid = (rw * PCOPY + k) * 64 + lane;
+            const int c = gid / GPC, g = gid % GPC;
+            const int64_t Gg = (int64_t)t * (kGroups * NSUB) + (int64_t)g * a.gpg;
+            g_live[k] = Gg < a.n_groups_total;
+            int64_t off = 0;
+            if (g_live[k]) {
+                const int row = (int)fdiv((uint32_t)Gg, a.div_GPR);
+                const int gi = (int)Gg - row * a.GPR;
+                const int img = (int)fdiv((uint32_t)row, a.div_Ho);
+                const int oh = row - img * a.Ho;
+                off = (int64_t)img * a.x_is + (int64_t)oh * a.in_row + gi * 4 * a.SW + (int64_t)c * a.x_cs;
+            }
+            e_base[k] = (int)off;   // x holds fewer than 2^31 elements
+            c_of[k] = c;
+        }
+    };
+    // copies of stage st of tile t into buffer b; every producer wave issues exactly
+    // SPS * (PCOPY + wcopy) copies (steps past the K loop read zeros)
+    auto fill = [&](int t, int st, int b) {
+        set_tile(t);
+        const uint32_t buf = bufs0 + (uint32_t)(b * stage_b);
+        for (int j = 0; j < SPS; ++j) {
+            const int s = st * SPS + j;
+            const uint32_t pb = buf + (uint32_t)(j * PB);
+            const unsigned char *src[PCOPY];
+#pragma unroll
+            for (int k = 0; k < PCOPY; ++k) {
+                const int e = e_base[k] + s * 32 * xcs;
+                const bool live = g_live[k] && s < S && s * 32 + c_of[k] < a.Cin && (uint32_t)e <= x_last;
+                src[k] = live ? xb + (int64_t)e * 2 : zero;
+            }
+#pragma unroll
+            for (int k = 0; k < PCOPY; k += 4)
+                dma_b4(src[k], src[min(k + 1, PCOPY - 1)], src[min(k + 2, PCOPY - 1)], src[min(k + 3, PCOPY - 1)],
+                       pb + (uint32_t)((rw * PCOPY + k) * 1024), min(4, PCOPY - k));
+            if (!res) {
+                // weight tiles m = rw * WCOPY + u of the m-block
+                const uint32_t wb = buf + (uint32_t)(SPS * PB + j * MT * 1024);
+                const unsigned char *ws[WCOPY];
+#pragma unroll
+                for (int u = 0; u < WCOPY; ++u)
+                    ws[u] = s < S ? A_g + ((size_t)(mt_first + rw * WCOPY + u) * S + s) * 1024 + lane * 16 : zero;
+#pragma unroll
+                for (int u = 0; u < WCOPY; u += 4)
+                    dma_b4(ws[u], ws[min(u + 1, WCOPY - 1)], ws[min(u + 2, WCOPY - 1)], ws[min(u + 3, WCOPY - 1)],
+                           wb + (uint32_t)((rw * WCOPY + u) * 1024), min(4, WCOPY - u));
+            }
+        }
+    };
+    // after stage st of tile t landed in buffer b: granules that would read past the
+    // end of x, element by element (only granules of the last tile can)
+    auto tail = [&](int t, int st, int b) {
+        if (t != a.n_pt - 1) return;
+        set_tile(t);
+        for (int j = 0; j < SPS; ++j) {
+            const int s = st * SPS + j;
+#pragma unroll
+            for (int k = 0; k < PCOPY; ++k) {
+                const int64_t e = (int64_t)e_base[k] + (int64_t)s * 32 * xcs;
+                if (g_live[k] && s < S && s * 32 + c_of[k] < a.Cin && e + 8 > a.x_total) {
+                    uint16_t *dst = (uint16_t *)(bufs + b * stage_b + j * PB + ((rw * PCOPY + k) * 64 + lane) * 16);
+                    const uint16_t *sx = (const uint16_t *)a.x + e;
+                    for (int i2 = 0; i2 < 8; ++i2) dst[i2] = e + i2 < a.x_total ? sx[i2] : (uint16_t)0;
+                }
+            }
+        }
+    };
+
+    // ---- multiplying waves ----
+    f32x4 acc[TM][4];
+    auto clear_acc = [&]() {
+#pragma unroll
+        for (int t = 0; t < TM; ++t)
+#pragma unroll
+            for (int nt = 0; nt < 4; ++nt) acc[t][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    };
+    clear_acc();
+    // lane's 8 channels x 4 pixels of a step: channel 8 kg + j at byte j * RB, pixels of
+    // group n16 of sub-tile ps
+    const int b_lane = 8 * kg * RB + (ps * kGroups + n16) * 4 * 2 * MODE;
+    // weights of step j of a stage (m-tile t at + t * a_mstr)
+    const int a_mstr = res ? S * 1024 : 1024;
+    auto read_step = [&](const unsigned char *pb, const unsigned char *w, typename GT::Raw &r, uint4 (&ar)[TM]) {
+        const unsigned char *p = pb + b_lane;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) __builtin_memcpy(&r.v[j], p + j * RB, sizeof(r.v[j]));
+#pragma unroll
+        for (int t = 0; t < TM; ++t) ar[t] = *(const uint4 *)(w + t * a_mstr);
+    };
+    auto mul_step = [&](const typename GT::Raw &r, const uint4 (&ar)[TM]) {
+        typename GT::Frag f;
+        GT::finish(r, f);
+#pragma unroll
+        for (int t = 0; t < TM; ++t) GT::mma(ar[t], f, acc[t]);
+    };
+    auto compute = [&](int st, int b) {
+        const int nst = min(SPS, S - st * SPS);
+        const unsigned char *buf = bufs + b * stage_b;
+        // weights of the stage's first step for this wave's first m-tile and lane; step j: + j * a_step
+        const unsigned char *w0 = res ? lds + ((m_loc0 * S + st * SPS) * 1024 + lane * 16)
+                                      : buf + SPS * PB + m_loc0 * 1024 + lane * 16;
+        const int a_step = res ? 1024 : MT * 1024;
+        typename GT::Raw r0, r1;
+        uint4 a0[TM], a1[TM];
+        read_step(buf, w0, r0, a0);
+        int j = 0;
+        for (; j + 1 < nst; j += 2) {
+            read_step(buf + (j + 1) * PB, w0 + (j + 1) * a_step, r1, a1);
+            mul_step(r0, a0);
+            if (j + 2 < nst) read_step(buf + (j + 2) * PB, w0 + (j + 2) * a_step, r0, a0);
+            mul_step(r1, a1);
+        }
+        if (j < nst) mul_step(r0, a0);
+    };
+
+    // bias + ReLU + rounding; each lane stores its group's 4 pixels of its 4 rows per
+    // m-tile (8 contiguous bytes, 16 for fp32 outputs; 16 lanes cover 64 pixels),
+    // masked by ballots
+    auto epilogue = [&](int t) {
+        const int64_t grp = (int64_t)t * (kGroups * NSUB) + ps * kGroups + n16;
+        const bool pix_ok = grp < a.n_groups_total;
+        const int64_t gq = pix_ok ? grp : 0;
+        const int row = (int)fdiv((uint32_t)gq, a.div_GPR);
+        const int gi = (int)gq - row * a.GPR;
+        const int img = (int)fdiv((uint32_t)row, a.div_Ho);
+        const int oh = row - img * a.Ho;
+        const int p0 = oh * a.Wo + 4 * gi;
+        const int nvalid = pix_ok ? max(0, min(4, a.Wo - 4 * gi)) : 0;
+        const float qnan = __builtin_nanf("");
+#pragma unroll
+        for (int t2 = 0; t2 < TM; ++t2) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int r = (m_loc0 + t2) * kMT + 4 * kg + i;   // row of the m-block
+                const int crow = mt_first * kMT + r;               // computed row
+                const bool row_ok = crow < a.R;
+                const int orow = MAP ? s_orow[r] : crow;
+                const float bv = a.bias ? s_bias[r] : 0.f;
+                float o[4];
+#pragma unroll
+                for (int nt = 0; nt < 4; ++nt) o[nt] = ok ? epi(acc[t2][nt][i], bv, a.relu) : qnan;
+                const int64_t yo = (int64_t)img * a.y_is + (int64_t)(row_ok ? orow : 0) * a.y_cs + p0;
+                const uint64_t full = ballot(row_ok && nvalid == 4);
+                const uint64_t part = ballot(row_ok && nvalid > 0 && nvalid < 4);
+                if (a.out_bf16) {
+                    uint16_t *y = (uint16_t *)a.y + yo;
+                    uint32_t h[4];
+#pragma unroll
+                    for (int nt = 0; nt < 4; ++nt) h[nt] = f32_to_bf16_rne(o[nt]);
+                    if (full) st_mask_b64(y, u32x2{h[0] | (h[1] << 16), h[2] | (h[3] << 16)}, full);
+                    if (part) {
+#pragma unroll
+                        for (int e = 0; e < 3; ++e) {
+                            const uint64_t me = part & ballot(e < nvalid);
+                            if (me) st_mask_b16(y + e, h[e], me);
+                        }
+                    }
+                } else {
+                    float *y = (float *)a.y + yo;
+                    if (full)
+                        st_mask_b128(y, u32x4{__float_as_uint(o[0]), __float_as_uint(o[1]), __float_as_uint(o[2]),
+                                              __float_as_uint(o[3])}, full);
+                    if (part) {
+#pragma unroll
+                        for (int e = 0; e < 3; ++e) {
+                            const uint64_t me = part & ballot(e < nvalid);
+                            if (me) st_mask_b32(y + e, __float_as_uint(o[e]), me);
+                        }
+                    }
+                }
+            }
+        }
+    };
+
+    // bias and row map of the m-block (multiplying waves; read before the first barrier)
+    if (!prod && (a.bias || MAP)) {
+        for (int r = tid; r < MT * kMT; r += kThreads) {
+            const int crow = mt_first * kMT + r;
+            // tiles of another plan (!ok): no map is read; output rows stay in range
+            const int out = MAP ? (crow < a.R && ok ? min(max(a.rowmap[crow], 0), a.Rout - 1) : min(crow, a.Rout - 1))
+                                : crow;
+            if constexpr (MAP) s_orow[r] = out;
+            if (a.bias) s_bias[r] = crow < a.R ? a.bias[out] : 0.f;
+        }
+    }
+    // every producer wave issues NCP copies per item (tile, stage), so when an item is
+    // awaited the copies of the NB - 2 items issued after it may still be in flight.
+    // Items are walked with cursors (tile, stage, buffer); nothing is divided in the loop.
+    const int NCP = SPS * (PCOPY + wcopy);
+    int ft = t_begin, fs = 0, fb = 0;   // next item to copy
+    int wt = t_begin, ws = 0, wb = 0;   // next item to await
+    auto adv = [&](int &t, int &st, int &b) {
+        if (++st == NS) { st = 0; ++t; }
+        if (++b == NB) b = 0;
+    };
+    if (prod && ok) {
+        if (res) {   // the m-block's weights: MT * S blocks of 1 KB, contiguous in dev_tiles
+            const unsigned char *src = A_g + (size_t)mt_first * S * 1024 + lane * 16;
+            const int nblk = MT * S;
+            for (int b0 = rw * 4; b0 < nblk; b0 += 16) {
+                const unsigned char *s0 = src + (size_t)b0 * 1024;
+                dma_b4(s0, s0 + 1024, s0 + 2048, s0 + 3072, lds0 + (uint32_t)b0 * 1024, min(4, nblk - b0));
+            }
+        }
+        for (int i = 0; i < NB - 1 && i < n_items; ++i) {
+            fill(ft, fs, fb);
+            adv(ft, fs, fb);
+        }
+        wait_vm(min(NB - 2, n_items - 1) * NCP);
+        tail(wt, ws, wb);
+        adv(wt, ws, wb);
+    }
+    __syncthreads();
+    int ct = t_begin, cs = 0, cb = 0;   // item computed now
+    const int nsx = ok ? NS : 1;
+    for (int i = 0; i < n_items; ++i) {
+        if (prod) {
+            if (ok) {
+                const bool more = i + NB - 1 < n_items;   // item i + NB - 1 goes out now
+                if (more) {
+                    fill(ft, fs, fb);
+                    adv(ft, fs, fb);
+                }
+                if (i + 1 < n_items) {
+                    // item i + 1 landed: the copies of items i + 2 .. min(i + NB - 1, last) may be pending
+                    wait_vm(more ? (NB - 2) * NCP : max(0, n_items - 2 - i) * NCP);
+                    tail(wt, ws, wb);
+                    adv(wt, ws, wb);
+                }
+            }
+        } else if (ok) {
+            compute(cs, cb);
+        }
+        __syncthreads();
+        // output of a finished tile: its stores overlap the next items
+        if (!prod && cs == nsx - 1) {
+            epilogue(ct);
+            clear_acc();
+        }
+        if (++cs == nsx) { cs = 0; ++ct; }
+        if (++cb == NB) cb = 0;
+    }
+}
+
+typedef void (*pl_fn)(PwArgs);
+
+// Instantiation choice: the m-block must hold a multiple of 4 m-tiles (one weight
+// tile per copying wave and step), so with two sub-tiles a wave has 2 or 4 m-tiles.
+template <int MODE>
+pl_fn pl_pick(int NSUB, int TM, bool map) {
+    if (NSUB == 1) {
+        switch (TM) {
+            case 1: return map ? k_pl<MODE, 1, 1, true> : k_pl<MODE, 1, 1, false>;
+            case 2: return map ? k_pl<MODE, 1, 2, true> : k_pl<MODE, 1, 2, false>;
+            case 4: return map ? k_pl<MODE, 1, 4, true> : k_pl<MODE, 1, 4, false>;
+            default: return nullptr;
+        }
+    }
+    if (NSUB == 2) {
+        switch (TM) {
+            case 2: return map ? k_pl<MODE, 2, 2, true> : k_pl<MODE, 2, 2, false>;
+            case 4: return map ? k_pl<MODE, 2, 4, true> : k_pl<MODE, 2, 4, false>;
+            default: return nullptr;
+        }
+    }
+    return nullptr;
+}
+
+}  // namespace pl
+}  // namespace bsp

@@ -73,7 +73,7 @@ static void finish_layout(Plan *p, int n_mt, int astep) {
                        p->mt_per_group, p->LP, p->S, p->CH_STRIDE, p->RS, p->LEFT, p->NSLOT,
                        p->CC, p->KH, p->KW, p->is_linear, p->SW, p->NSUB, p->SMAX, p->resident,
                        p->MBT, p->MBG, p->n_mt_pad, p->n_g_pad, p->GE, p->NB, p->pw, p->NGR, p->VS, p->V,
-                       p->rowmap, p->RK, p->khw, (int)p->counts_hash, p->counts != nullptr, 11};
+                       p->rowmap, p->RK, p->khw, (int)p->counts_hash, p->counts != nullptr, p->pl, 12};
     p->fingerprint = fnv1a(fpv, (int)(sizeof(fpv) / sizeof(fpv[0])));
 }
 
@@ -208,6 +208,103 @@ static bool plan_pointwise(Plan *p, int span_req, int n_mt, int mpg, int astep) 
                                 bestp = q;
                             }
                         }
+                    }
+                }
+            }
+        }
+    }
+    if (best >= 1e300) return false;
+    *p = bestp;
+    return true;
+}
+
+// Tiling of a bf16 pointwise layer with one identity list for its own kernel
+// (k_pl): one workgroup of 8 waves per CU, 4 multiplying and 4 copying, an m-block of
+// MT = TM * 4 / NSUB m-tiles (a multiple of 4) and tiles of 64 NSUB pixels; stages of
+// SPS steps in NB LDS buffers.  Scored for the nominal batch with a serial model of a
+// stage: the copying waves' issue time (about 90 cycles per 1 KB copy per wave, 2.2
+// times that from input rows off 16-byte boundaries), the multiplying waves' steps
+// (4 MFMAs of 16 cycles per m-tile and about 100 cycles of gathers and LDS latency),
+// at least the copy latency spread over the stages ahead, plus a fixed cost per
+// stage (barrier, waits, loop); per tile the epilogue's stores (10 bytes per cycle);
+// never below the HBM time.  The fixed and latency costs were fitted to a GPU sweep
+// of every tiling of the ResNet-50 pointwise layers (the model's choice is within 1%
+// of the fastest tiling there), which found large stages (4 steps) with two or three
+// buffers best.  Returns false when nothing fits.
+static bool plan_pl(Plan *p, int n_mt, int astep) {
+    const int gpg = p->SW == 1 ? 2 : 1;
+    int64_t groups_nom;   // groups of the nominal batch
+    double hbm_bytes;
+    bool mis;             // granule sources off 16-byte boundaries
+    if (p->is_linear) {
+        groups_nom = round_up(div_up(kNominalVectors, 4), gpg);
+        hbm_bytes = ((double)p->Cin + p->RK) * kNominalVectors * 2;
+        mis = false;
+    } else if (p->SW == 1) {
+        groups_nom = (int64_t)kNominalImages * round_up(div_up(p->H * p->W, 4), gpg);
+        hbm_bytes = ((double)p->Cin + p->RK) * kNominalImages * p->H * p->W * 2;
+        mis = ((int64_t)p->H * p->W * 2) % 16 != 0;
+    } else {
+        groups_nom = (int64_t)kNominalImages * p->Ho * div_up(p->Wo, 4);
+        hbm_bytes = ((double)p->Cin * p->H * p->W / 2 + (double)p->RK * p->Ho * p->Wo) * kNominalImages * 2;
+        mis = ((int64_t)p->W * 2) % 16 != 0;
+    }
+    hbm_bytes += (double)n_mt * p->S * astep;
+    const double t_hbm = hbm_bytes / 5.5e12 * 2.4e9;
+    const int64_t budget = 160 * 1024 - 2048 - 512;   // minus static LDS (bias, row map) and slack
+    const int mode = p->SW;
+
+    double best = 1e300;
+    Plan bestp = *p;
+    for (int nsub = 1; nsub <= 2; ++nsub) {
+        const int np = 64 * nsub;
+        const int rb = np * 2 * mode;                 // patch bytes per channel
+        const int pcopy = 32 * (rb / 16) / kThreads;  // patch copies per copying wave and step
+        const double n_pt = std::ceil((double)groups_nom / (kGroups * nsub));
+        for (int TM = 1; TM <= 4; TM *= 2) {
+            const int MT = TM * (kWaves / nsub);
+            if (MT % kWaves != 0) continue;
+            if (MT > 4 && MT >= 2 * n_mt) continue;   // mostly idle waves
+            const int n_mb = div_up(n_mt, MT);
+            for (int resident = 0; resident <= 1; ++resident)
+            for (int sps = 1; sps <= 4 && sps <= p->S; sps *= 2) {
+                const int wcopy = resident ? 0 : MT / kWaves;
+                const int64_t a_res = resident ? (int64_t)MT * p->S * 1024 : 0;
+                const int64_t step_b = 32 * rb + (resident ? 0 : (int64_t)MT * 1024);
+                for (int nb = 2; nb <= 8; ++nb) {
+                    const int64_t total = a_res + nb * sps * step_b;
+                    if (total > budget) continue;
+                    const int ncp = sps * (pcopy + wcopy);
+                    const double ns = std::ceil((double)p->S / sps);
+                    double wpm = std::max(1.0, std::ceil(256.0 / n_mb));
+                    if (wpm > n_pt) wpm = n_pt;
+                    const double tpw = std::ceil(n_pt / wpm);
+                    const double n_wg = std::ceil(n_pt / tpw) * n_mb;
+                    const double rounds = std::ceil(n_wg / 256.0);
+                    const double prod = sps * (pcopy * (mis ? 200.0 : 90.0) + wcopy * 90.0) + 100.0;
+                    const double comp = sps * (TM * 64.0 + 100.0) + 150.0;
+                    const double stage = std::max(std::max(prod, comp), 1000.0 / (nb - 1)) + 1500.0;
+                    const double out_bytes = (double)MT * kMT * np * 2;
+                    const double epi = TM * 4 * 60.0 + out_bytes / 10.0;
+                    double cyc = rounds * (tpw * (ns * stage + epi) + a_res / 1024.0 * 25.0) + 5000.0;
+                    if ((nb - 1) * ncp > 63) cyc *= 1.05;   // more copies in flight than a wave can count
+                    cyc = std::max(cyc, t_hbm);
+                    if (cyc < best * (1 - 1e-9)) {
+                        best = cyc;
+                        Plan q = *p;
+                        q.pw = 1; q.pl = 1; q.gpg = gpg; q.occ = 1;
+                        q.NSUB = nsub; q.NGR = rb / 16;
+                        q.CH_STRIDE = np * mode; q.CC = 32 * sps; q.SMAX = sps;
+                        q.FR = pcopy;
+                        q.qmode = 0; q.KS = 1; q.TM = TM; q.TPG = TM;
+                        q.MBT = MT; q.MBG = 1; q.n_mb = n_mb;
+                        q.resident = resident; q.NB = nb;
+                        q.lds_d = 0; q.lds_a = (int)a_res;
+                        q.lds_patch = 32 * rb * sps;
+                        q.lds_astage = resident ? 0 : MT * 1024 * sps;
+                        q.lds_buf = (int)(sps * step_b);
+                        q.lds_total = (int)total;
+                        bestp = q;
                     }
                 }
             }
@@ -506,7 +603,8 @@ bsp_status make_plan(const bsp_scheme *s, const bsp_conv_shape *conv, bsp_dtype 
         else if (p->counts && p->nbc > 1) cols = max_step_span_cols(*p);
         else if (p->counts)   // one block column: lists stretched over L slots, twice the mean spacing
             cols = std::min<int64_t>(p->C, 2 * (int64_t)kKS * p->C / p->L + 1);
-        else if (p->reg == BSP_PUNCHED) cols = (int64_t)div_up(kKS, kept_count(p->khw, p->rate)) * khw;
+        else if (p->reg == BSP_PUNCHED)   // a step may start at the last kept location of a channel
+            cols = (int64_t)(div_up(kKS, kept_count(p->khw, p->rate)) + 1) * p->khw;
         else if (p->nbc > 1) cols = (int64_t)(div_up(kKS, kept_count(p->bw_eff, p->rate)) + 1) * p->bw_eff;
         else cols = (int64_t)2 * kKS * p->rate;
         span_req = (int)std::min<int64_t>(p->Cin, cols / khw + 2);
@@ -529,7 +627,11 @@ bsp_status make_plan(const bsp_scheme *s, const bsp_conv_shape *conv, bsp_dtype 
     // pointwise layers (1x1 without padding, stride 1 or 2; linear): own kernel
     if (p->KH == 1 && p->KW == 1 && p->PH == 0 && p->PW == 0 && p->SH == p->SW &&
         (p->SW == 1 || (p->SW == 2 && p->esize == 2))) {
-        if (plan_pointwise(p, span_req, n_mt, mpg, astep)) {
+        // the identity-list kernel for 1x1 convs with more than 64 input channels; with
+        // 64 or fewer (weights resident, two workgroups per CU) and for linear layers the
+        // general pointwise kernel was faster in the measured sweep
+        if ((p->esize == 2 && p->shared && !p->is_linear && p->Cin > 64 && plan_pl(p, n_mt, astep)) ||
+            plan_pointwise(p, span_req, n_mt, mpg, astep)) {
             finish_layout(p, n_mt, astep);
             return BSP_OK;
         }
