@@ -47,7 +47,8 @@ typedef enum {
     BSP_EINVAL = -1,        /* bad argument, shape or null pointer            */
     BSP_EUNSUPPORTED = -2,  /* valid request this library does not implement  */
     BSP_EDEVICE = -3,       /* HIP launch / copy / allocation failure          */
-    BSP_EMASK = -4          /* mask given to bsp_pack lacks the block structure */
+    BSP_EMASK = -4,         /* mask given to bsp_pack lacks the block structure */
+    BSP_ETOOLARGE = -5      /* input beyond the fixed scratch of bsp_prune_noalloc */
 } bsp_status;
 
 typedef enum { BSP_F32 = 0, BSP_BF16 = 1 } bsp_dtype;
@@ -124,6 +125,24 @@ bsp_status bsp_packed_sizes(const bsp_scheme *scheme, const bsp_conv_shape *conv
  * `stream` before returning. */
 bsp_status bsp_prune(const bsp_scheme *scheme, bsp_dtype wdt, const void *w, uint8_t *mask,
                      void *stream);
+
+/* bsp_prune for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc): the
+ * same masks, bit for bit, and no allocation of any kind.
+ *  - BSP_UNSTRUCTURED ranks the layer in the library's fixed scratch: one
+ *    static device array per GPU (about 257 KB, held until the process ends)
+ *    that serves rows * cols <= 2^28 weights; larger layers return
+ *    BSP_ETOOLARGE before anything is launched.  Every call on a GPU shares
+ *    that GPU's array: calls that overlap on one GPU (concurrent streams or
+ *    threads) race and must be serialised by the caller.  What the select
+ *    reads of the array is first written by the same call.
+ *  - The block regularities (ROW, COL, PUNCHED, ROWCOL) and DENSE use no
+ *    scratch.
+ *  - BSP_PATTERN and per-block counts (which need a buffer sized by the
+ *    layer) return BSP_EUNSUPPORTED.
+ * Async on `stream`; nothing else changes from bsp_prune. */
+bsp_status bsp_prune_noalloc(const bsp_scheme *scheme, bsp_dtype wdt, const void *w, uint8_t *mask,
+                             void *stream);
 
 /* Pack the masked weights (the compact storage idea of Sec. 4.3, in this
  * library's own layout).  SYNCHRONOUS: checks on the device that the mask

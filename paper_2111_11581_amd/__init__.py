@@ -15,7 +15,7 @@ import os
 
 __all__ = [
     "F32", "BF16", "ROW", "COL", "UNSTRUCTURED", "DENSE", "PUNCHED", "ROWCOL", "PATTERN", "BspError", "Scheme", "ConvShape",
-    "lib", "lib_path", "bsp_packed_sizes", "bsp_prune", "bsp_pack", "bsp_unpack", "bsp_conv2d",
+    "lib", "lib_path", "bsp_packed_sizes", "bsp_prune", "bsp_prune_noalloc", "bsp_pack", "bsp_unpack", "bsp_conv2d",
     "bsp_linear", "bsp_maxpool2x2", "bsp_status_string", "bsp_version", "bsp_to_bcs",
 ]
 
@@ -71,6 +71,7 @@ def lib():
     sch, cs = P(Scheme), P(ConvShape)
     L.bsp_packed_sizes.argtypes = [sch, cs, I32, P(I64), P(I64), P(I64), P(I64)]
     L.bsp_prune.argtypes = [sch, I32, VP, VP, VP]
+    L.bsp_prune_noalloc.argtypes = [sch, I32, VP, VP, VP]
     L.bsp_pack.argtypes = [sch, I32, VP, VP, VP, VP, VP, VP, cs, VP]
     L.bsp_unpack.argtypes = [sch, I32, VP, VP, VP, VP, VP]
     L.bsp_conv2d.argtypes = [sch, cs, I32, I32, VP, VP, VP, I32, VP, VP]
@@ -79,7 +80,7 @@ def lib():
     L.bsp_status_string.argtypes = [I32]
     L.bsp_status_string.restype = ctypes.c_char_p
     L.bsp_version.argtypes = []
-    for f in ("bsp_packed_sizes", "bsp_prune", "bsp_pack", "bsp_unpack", "bsp_conv2d",
+    for f in ("bsp_packed_sizes", "bsp_prune", "bsp_prune_noalloc", "bsp_pack", "bsp_unpack", "bsp_conv2d",
               "bsp_linear", "bsp_maxpool2x2", "bsp_version", "bsp_to_bcs"):
         getattr(L, f).restype = I32
     _lib = L
@@ -153,6 +154,14 @@ def bsp_prune(scheme, wdt: int, w, mask, stream=None):
     _need("w", w, s.rows * s.cols * _esize(wdt))
     _need("mask", mask, s.rows * s.cols)
     _check("bsp_prune", lib().bsp_prune(ctypes.byref(s), int(wdt), _p(w), _p(mask), _stream(stream)))
+
+
+def bsp_prune_noalloc(scheme, wdt: int, w, mask, stream=None):
+    s = _scheme(scheme)
+    _need("w", w, s.rows * s.cols * _esize(wdt))
+    _need("mask", mask, s.rows * s.cols)
+    _check("bsp_prune_noalloc", lib().bsp_prune_noalloc(ctypes.byref(s), int(wdt), _p(w), _p(mask),
+                                                        _stream(stream)))
 
 
 def bsp_pack(scheme, wdt: int, w, mask, values, indices, rowptr, dev_tiles, conv=None, stream=None):

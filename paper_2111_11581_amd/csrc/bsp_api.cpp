@@ -36,6 +36,7 @@ const char *bsp_status_string(bsp_status s) {
         case BSP_EUNSUPPORTED: return "unsupported configuration";
         case BSP_EDEVICE: return "device error";
         case BSP_EMASK: return "mask does not have the block structure of the scheme";
+        case BSP_ETOOLARGE: return "input larger than the fixed scratch of the allocation-free entry point";
         default: return "unknown status";
     }
 }
@@ -64,6 +65,18 @@ bsp_status bsp_prune(const bsp_scheme *scheme, bsp_dtype wdt, const void *w, uin
     if (st != BSP_OK) return st;
     if ((st = check_scheme_for_prune(p)) != BSP_OK) return st;
     return launch_prune(p, w, mask, S(stream)) == hipSuccess ? BSP_OK : BSP_EDEVICE;
+}
+
+bsp_status bsp_prune_noalloc(const bsp_scheme *scheme, bsp_dtype wdt, const void *w, uint8_t *mask,
+                             void *stream) {
+    if (!scheme || !w || !mask) return BSP_EINVAL;
+    Plan p;
+    bsp_status st = make_plan(scheme, nullptr, wdt, -1, &p);
+    if (st != BSP_OK) return st;
+    if ((st = check_scheme_for_prune(p)) != BSP_OK) return st;
+    if (p.reg == BSP_PATTERN || p.counts) return BSP_EUNSUPPORTED;
+    if (p.reg == BSP_UNSTRUCTURED && (uint64_t)p.R * (uint64_t)p.C > kNoAllocMaxWeights) return BSP_ETOOLARGE;
+    return launch_prune_noalloc(p, w, mask, S(stream)) == hipSuccess ? BSP_OK : BSP_EDEVICE;
 }
 
 bsp_status bsp_pack(const bsp_scheme *scheme, bsp_dtype wdt, const void *w, const uint8_t *mask,

@@ -9,6 +9,15 @@ namespace bsp {
 
 hipError_t launch_prune(const Plan &p, const void *w, uint8_t *mask, hipStream_t st);
 
+// Weights the allocation-free prune handles (its fixed per-device scratch holds the
+// radix select of this many).
+constexpr size_t kNoAllocMaxWeights = (size_t)1 << 28;
+
+// As launch_prune, allocating nothing: UNSTRUCTURED uses the library's fixed
+// per-device scratch (R * C <= kNoAllocMaxWeights), the block kinds need none;
+// PATTERN and per-block counts are not handled (hipErrorInvalidValue).
+hipError_t launch_prune_noalloc(const Plan &p, const void *w, uint8_t *mask, hipStream_t st);
+
 // Synchronous: returns BSP_OK, BSP_EMASK, BSP_EUNSUPPORTED or BSP_EDEVICE.
 bsp_status run_pack(const Plan &p, const void *w, const uint8_t *mask, void *values,
                     int32_t *indices, int32_t *rowptr, uint8_t *tiles, hipStream_t st);

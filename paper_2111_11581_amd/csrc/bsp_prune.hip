@@ -18,6 +18,8 @@
 
 #include <hipcub/hipcub.hpp>
 
+#include <mutex>
+
 #include "bsp_kernels.h"
 
 namespace bsp {
@@ -408,15 +410,26 @@ __global__ void k_sel_write(const E *__restrict__ w, size_t n, const SelState *s
     }
 }
 
+// scratch of the radix select: the state, then one count per chunk of kSelChunk weights
+inline size_t sel_scratch_bytes(size_t n) {
+    return sizeof(SelState) + sizeof(uint32_t) * ((n + kSelChunk - 1) / kSelChunk);
+}
+
+// fixed: a caller's scratch of at least sel_scratch_bytes(n) bytes (nothing allocated),
+// or null (a stream-ordered allocation, freed before returning).  Every part of the
+// scratch that is read is first written by a kernel of this call.
 template <typename E>
-static hipError_t prune_unstructured(const Plan &p, const E *w, uint8_t *mask, hipStream_t st) {
+static hipError_t prune_unstructured(const Plan &p, const E *w, uint8_t *mask, hipStream_t st,
+                                     void *fixed = nullptr) {
     const size_t n = (size_t)p.R * p.C;
     const uint32_t k = (uint32_t)((n + p.rate - 1) / p.rate);
     const int nchunks = (int)((n + kSelChunk - 1) / kSelChunk);
-    void *scr = nullptr;
-    const size_t bytes = sizeof(SelState) + sizeof(uint32_t) * (size_t)nchunks;
-    hipError_t e = hipMallocAsync(&scr, bytes, st);
-    if (e != hipSuccess) return e;
+    void *scr = fixed;
+    hipError_t e = hipSuccess;
+    if (!fixed) {
+        e = hipMallocAsync(&scr, sel_scratch_bytes(n), st);
+        if (e != hipSuccess) return e;
+    }
     SelState *s = (SelState *)scr;
     uint32_t *cc = (uint32_t *)((char *)scr + sizeof(SelState));
     const int hblocks = (int)std::min<size_t>(2048, (n + 255) / 256);
@@ -430,8 +443,54 @@ static hipError_t prune_unstructured(const Plan &p, const E *w, uint8_t *mask, h
     k_sel_scan<<<1, 1, 0, st>>>(cc, nchunks);
     k_sel_write<E><<<nchunks, 256, 0, st>>>(w, n, s, cc, mask);
     e = hipGetLastError();
+    if (fixed) return e;
     hipError_t e2 = hipFreeAsync(scr, st);
     return e != hipSuccess ? e : e2;
+}
+
+// ---- scratch of the allocation-free entry point -------------------------------------
+// One fixed array per GPU (the module's device copy), sized for the radix select of
+// up to kNoAllocMaxWeights weights.  Host code never uses the array's name as an
+// address: the device address comes from hipGetSymbolAddress, once per device.
+static __device__ __align__(256) unsigned char scratch[sizeof(SelState) +
+                                                       sizeof(uint32_t) * (kNoAllocMaxWeights / kSelChunk)];
+static_assert(kNoAllocMaxWeights % kSelChunk == 0, "whole chunks");
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices];   // device address of `scratch` on each device, once known
+}  // namespace
+
+// Device address of the current device's scratch (looked up on its first use there).
+static hipError_t scratch_address(void **out) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void *ptr = nullptr;
+        e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        if (!ptr) return hipErrorInvalidSymbol;
+        g_scratch_ptr[dev] = ptr;
+    }
+    *out = g_scratch_ptr[dev];
+    return hipSuccess;
+}
+
+hipError_t launch_prune_noalloc(const Plan &p, const void *w, uint8_t *mask, hipStream_t st) {
+    if (p.reg == BSP_UNSTRUCTURED) {
+        if ((size_t)p.R * p.C > kNoAllocMaxWeights) return hipErrorInvalidValue;
+        void *scr = nullptr;
+        hipError_t e = scratch_address(&scr);
+        if (e != hipSuccess) return e;
+        return p.dt == BSP_F32 ? prune_unstructured(p, (const float *)w, mask, st, scr)
+                               : prune_unstructured(p, (const uint16_t *)w, mask, st, scr);
+    }
+    if (p.reg == BSP_PATTERN || p.counts) return hipErrorInvalidValue;
+    return launch_prune(p, w, mask, st);   // block kinds: no scratch
 }
 
 hipError_t launch_prune(const Plan &p, const void *w, uint8_t *mask, hipStream_t st) {

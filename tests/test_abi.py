@@ -229,3 +229,19 @@ def test_per_block_counts_out_of_range_are_rejected(bsp):
     assert L.bsp_packed_sizes(ctypes.byref(s), None, 1, *[ctypes.byref(o) for o in out]) == -1
     s = bsp.Scheme(32, 64, 16, 32, 1, 2).set_counts([[3, -1], [0, 1]])
     assert L.bsp_packed_sizes(ctypes.byref(s), None, 1, *[ctypes.byref(o) for o in out]) == -1
+
+
+def test_prune_noalloc_rejects_before_any_launch(bsp):
+    """The allocation-free prune validates on the host: too large an unstructured
+    layer gives BSP_ETOOLARGE, pattern-based pruning and per-block counts
+    BSP_EUNSUPPORTED, and nothing is launched (the pointers are never touched)."""
+    L = bsp.lib()
+    fake = ctypes.c_void_p(16)
+    big = bsp.Scheme(1 << 15, (1 << 13) + 1, 1, 1, bsp.UNSTRUCTURED, 4)       # 2^28 + 2^15 weights
+    assert L.bsp_prune_noalloc(ctypes.byref(big), bsp.BF16, fake, fake, None) == -5
+    assert "fixed scratch" in bsp.bsp_status_string(-5)
+    pat = bsp.Scheme(64, 64 * 9, 8, 0, bsp.PATTERN, 4, 9)
+    assert L.bsp_prune_noalloc(ctypes.byref(pat), bsp.BF16, fake, fake, None) == -2
+    cnt = bsp.Scheme(64, 64, 32, 32, bsp.COL, 4).set_counts([[4, 5], [6, 7]])
+    assert L.bsp_prune_noalloc(ctypes.byref(cnt), bsp.BF16, fake, fake, None) == -2
+    assert L.bsp_prune_noalloc(None, bsp.BF16, fake, fake, None) == -1
