@@ -73,7 +73,7 @@ static void finish_layout(Plan *p, int n_mt, int astep) {
                        p->mt_per_group, p->LP, p->S, p->CH_STRIDE, p->RS, p->LEFT, p->NSLOT,
                        p->CC, p->KH, p->KW, p->is_linear, p->SW, p->NSUB, p->SMAX, p->resident,
                        p->MBT, p->MBG, p->n_mt_pad, p->n_g_pad, p->GE, p->NB, p->pw, p->NGR, p->VS, p->V,
-                       p->rowmap, p->RK, p->khw, (int)p->counts_hash, p->counts != nullptr, p->pl, 12};
+                       p->rowmap, p->RK, p->khw, (int)p->counts_hash, p->counts != nullptr, p->pl, 13};
     p->fingerprint = fnv1a(fpv, (int)(sizeof(fpv) / sizeof(fpv[0])));
 }
 
@@ -400,6 +400,175 @@ static int64_t max_step_span_cols(const Plan &p) {
     return worst;
 }
 
+// Channels one 32-wide step of a forward list can span (a chunk's channel window must
+// hold at least that many) and the mean channels a step advances.  Identity lists: 32
+// consecutive columns.  Column blocks keep the same count in every block, so a step
+// covers a known number of blocks; whole-width blocks are data dependent (twice the
+// mean spacing is used).
+// Block-punched lists keep the same number of locations of every channel.
+static void list_spans(const Plan &p, int *span_req, double *step_ch) {
+    {
+        const int khw = p.KH * p.KW;
+        int64_t cols;
+        if (p.shared) cols = kKS;
+        else if (p.counts && p.nbc > 1) cols = max_step_span_cols(p);
+        else if (p.counts)   // one block column: lists stretched over L slots, twice the mean spacing
+            cols = std::min<int64_t>(p.C, 2 * (int64_t)kKS * p.C / p.L + 1);
+        else if (p.reg == BSP_PUNCHED)   // a step may start at the last kept location of a channel
+            cols = (int64_t)(div_up(kKS, kept_count(p.khw, p.rate)) + 1) * p.khw;
+        else if (p.nbc > 1) cols = (int64_t)(div_up(kKS, kept_count(p.bw_eff, p.rate)) + 1) * p.bw_eff;
+        else cols = (int64_t)2 * kKS * p.rate;
+        *span_req = (int)std::min<int64_t>(p.Cin, cols / khw + 2);
+    }
+    // mean channels one step advances (for the chunk count of a channel window)
+    {
+        const int khw = p.KH * p.KW;
+        if (p.shared) *step_ch = (double)kKS / khw;
+        else if (p.counts) *step_ch = (double)kKS * p.nbr * p.C / std::max<int64_t>(p.n_indices, 1) / khw;
+        else if (p.reg == BSP_PUNCHED) *step_ch = (double)kKS / kept_count(p.khw, p.rate);
+        else if (p.nbc > 1) *step_ch = (double)kKS * p.bw_eff / kept_count(p.bw_eff, p.rate) / khw;
+        else *step_ch = (double)kKS * p.rate / khw;
+    }
+}
+
+// Tiling of the general forward kernel for the plan's list layout, scored for the
+// nominal batch (CU cycles).  Sets *p to the best tiling and returns its score, or
+// 1e300 (p unchanged) when nothing fits.
+static double search_tiling(Plan *p, int span_req, double step_ch, int n_mt, int mpg, int astep,
+                            int nominal_rows) {
+    const double total_groups = (double)nominal_rows * p->GPR;
+    // LDS budgets per workgroup: 1, 2, 3 or 4 workgroups per CU (160 KB, minus static tables)
+    const int budgets[4] = {160 * 1024 - kLdsStatic, 80 * 1024 - kLdsStatic, 53 * 1024 - kLdsStatic,
+                            40 * 1024 - kLdsStatic};
+
+    double best = 1e300;
+    Plan bestp = *p;
+    // a second pass admits m-blocks much larger than the layer when nothing else fits
+    for (int relax = 0; relax < 2 && best >= 1e300; ++relax)
+    for (int nsub = 1; nsub <= 4; nsub *= 2) {
+        const int TG = kGroups * nsub;
+        const int trw = rows_spanned(TG, p->GPR);
+        if (trw > kMaxTileRows) continue;
+        const int nslot = max_slots(TG, p->GPR, p->Ho, p->KH, p->SH, p->PH);
+        if (nslot > kMaxSlots) continue;
+        const int chs = p->V * nslot * p->RS;             // patch elements per channel
+        if (p->V * nslot * p->RG > 512) continue;         // granules per channel: per-tile lookup table
+        const int Q = kWaves / nsub;
+        const double n_pt = std::ceil(total_groups / TG);
+        for (int qmode = 0; qmode <= 1; ++qmode) {
+            if (qmode == 1 && Q == 1) continue;
+            const int KS = qmode ? Q : 1;
+            for (int TM = 1; TM <= 4; TM *= 2) {
+                // instantiated kernels: fp32 and per-element gathers at most 2 m-tiles per
+                // wave and no step split; 16-byte stride-2 gathers at most 4 m-tiles
+                const bool narrow = p->esize == 4 || p->gather == 0;
+                if (narrow && (TM > 2 || qmode == 1)) continue;
+                if (p->gather == 2 && TM > 4) continue;
+                int TPG, MBT, MBG, n_mb;
+                MBT = TM * (qmode == 0 ? Q : 1);
+                if (p->shared) {
+                    TPG = TM;
+                    if (!relax && MBT > 1 && MBT >= 2 * n_mt) continue;     // mostly idle waves
+                    MBG = 1;
+                    n_mb = div_up(n_mt, MBT);
+                } else {
+                    TPG = std::min(TM, mpg);
+                    if (TM % TPG) continue;
+                    if (MBT % mpg != 0 && mpg % MBT != 0) continue;
+                    if (!relax && MBT > 1 && MBT >= 2 * n_mt) continue;
+                    MBG = std::max(1, MBT / mpg);
+                    n_mb = div_up(n_mt, MBT);
+                }
+                const int64_t d_res = align256((int64_t)MBG * p->LP * 2);
+                const int64_t a_all = (int64_t)MBT * p->S * astep;
+                for (int bi = 0; bi < (relax ? 4 : 1); ++bi) {   // measured: one workgroup per CU with large chunks is best
+                    const int64_t budget = budgets[bi];
+                    for (int opt = 0; opt < 10; ++opt) {
+                        const int nb = opt < 5 ? 3 : 2;   // buffers (two when three do not fit)
+                        const int resident = opt % 5 == 0;
+                        const int smax = resident ? 0 : (1 << (opt % 5 - 1));   // 1, 2, 4, 8
+                        if (!resident && smax > p->S) continue;
+                        const int64_t astage = resident ? 0 : (int64_t)MBT * smax * astep;
+                        const int64_t fixed = d_res + (resident ? align256(a_all) : 0) + 256;
+                        const int64_t free_b = budget - fixed - nb * align256(astage) - nb * 512;
+                        if (free_b <= 0) continue;
+                        // patches are whole 1 KB copy slots of four waves (256 granules)
+                        int64_t cc = free_b / (nb * 4096) * kThreads / ((int64_t)p->V * nslot * p->RG);
+                        cc = std::min<int64_t>(cc, std::min(p->Cin, kMaxCC));
+                        cc = std::min<int64_t>(cc, 65536 / chs);                       // 16-bit offsets
+                        if (cc < span_req || cc < 1) continue;
+                        int fr = (int)div_up64(cc * p->V * nslot * p->RG, kThreads);
+                        if (fr > 32) {   // copies per wave and chunk: one bit each in the fixup mask
+                            cc = 32 * kThreads / ((int64_t)p->V * nslot * p->RG);
+                            if (cc < span_req || cc < 1) continue;
+                            fr = (int)div_up64(cc * p->V * nslot * p->RG, kThreads);
+                        }
+                        const int64_t lds_patch = (int64_t)fr * 4096;   // whole 1 KB copy slots of four waves
+                        const int64_t lds_buf = lds_patch + align256(astage);
+                        int64_t total = fixed + nb * lds_buf + (p->gather == 3 ? 256 : 0);   // MODE 3 reads run past the patch
+                        if (qmode == 1) total = std::max<int64_t>(total, (int64_t)2 * TM * 4096);   // partial sums
+                        if (total > budget) continue;
+
+                        // ---- score (nominal batch), in CU cycles ----
+                        // persistent workgroups: occ per CU, each walking tpw pixel tiles
+                        const int occ = std::min(fwd_occ(p->gather, TM, TPG), (160 * 1024) / (int)(total + kLdsStatic));
+                        if (occ < 1) continue;
+                        double wpm = std::max(1.0, std::ceil(256.0 * occ / n_mb));
+                        if (KS > 1 || wpm > n_pt) wpm = n_pt;
+                        const double tpw = std::ceil(n_pt / wpm);
+                        const double n_wg = std::ceil(n_pt / tpw) * n_mb;
+                        const double rounds = std::ceil(n_wg / (256.0 * occ));
+                        // steps per chunk: consecutive steps advance step_ch channels each
+                        // (staged weights: at most SMAX); the real count depends on the lists
+                        double spc = std::max(1.0, (cc - 1) / step_ch);
+                        if (!resident) spc = std::min<double>(spc, smax);
+                        const double nch = std::max(1.0, p->S / spc);
+                        // Serial time of one wave per chunk, fitted to measured plans on gfx950
+                        // (ResNet-50 3x3 layers, 4x column pruning): a fixed cost (copy table
+                        // reads, fixups, barrier, pipeline refill), each stage (8 kept columns
+                        // gathered and 4 MFMAs per m-tile list; stride-2 gathers read 4 dwords
+                        // per column), each 1 KB copy (twice when input rows start off 16-byte
+                        // boundaries); three buffers make chunks smaller and cost more per chunk.
+                        const double stages = std::ceil(spc / KS) * (TM / TPG);
+                        const double copies = fr + (resident ? 0.0 : (double)astage / 4096.0);
+                        const bool mis = ((int64_t)p->W * p->esize) % 16 != 0;
+                        double per_chunk = 3000.0 + stages * (p->SW == 2 ? 900.0 : 500.0) + copies * (mis ? 100.0 : 50.0);
+                        if (nb == 3) per_chunk *= 1.2;
+                        if (occ > 1) per_chunk *= 0.8 * occ;                               // workgroups sharing a CU
+                        // per tile: epilogue; per workgroup: header, tables, first fill
+                        double cyc = rounds * (tpw * nch * per_chunk + tpw * 8000.0 + 8000.0);
+                        const double hbm = ((double)nominal_rows / p->Ho * p->Cin * p->H * p->W * p->esize +
+                                            total_groups * 4 * p->RK * 2.0) / 5.5e12 * 2.4e9;
+                        // L2-to-LDS copies of the whole job (every m-block copies the patch of
+                        // every tile it computes) at about 8 bytes per CU cycle
+                        const double copy_bytes = n_mb * n_pt * nch * ((double)fr * 4096 + (resident ? 0.0 : (double)astage));
+                        cyc = std::max(std::max(cyc, hbm), copy_bytes / (256.0 * 8.0));
+                        if (qmode == 1) cyc = cyc * 1.5 + 1500.0;                           // partial-sum reduction
+                        if (cyc < best * (1 - 1e-9)) {
+                            best = cyc;
+                            Plan q = *p;
+                            q.NSUB = nsub; q.TRWMAX = trw; q.NSLOT = nslot; q.CH_STRIDE = chs; q.VS = nslot * p->RS;
+                            q.CC = (int)cc; q.FR = fr;
+                            q.qmode = qmode; q.KS = KS; q.TM = TM; q.TPG = TPG;
+                            q.MBT = MBT; q.MBG = MBG; q.n_mb = n_mb;
+                            q.resident = resident; q.SMAX = smax; q.NB = nb;
+                            q.lds_d = (int)d_res;
+                            q.lds_a = resident ? (int)align256(a_all) : 0;
+                            q.lds_patch = (int)lds_patch;
+                            q.lds_astage = (int)align256(astage);
+                            q.lds_buf = (int)lds_buf;
+                            q.lds_total = (int)total;
+                            bestp = q;
+                        }
+                    }
+                }
+            }
+        }
+    }
+    if (best < 1e300) *p = bestp;
+    return best;
+}
+
 bsp_status make_plan(const bsp_scheme *s, const bsp_conv_shape *conv, bsp_dtype wdt,
                      int batch_for_linear, Plan *p) {
     if (!s || !p) return BSP_EINVAL;
@@ -590,35 +759,9 @@ bsp_status make_plan(const bsp_scheme *s, const bsp_conv_shape *conv, bsp_dtype 
     }
     p->RG = p->RS / p->GE;
 
-    // Channels one 32-wide step of a kept list can span: a chunk's channel window
-    // must hold at least that many.  Identity lists: 32 consecutive columns.  Column
-    // blocks keep the same count in every block, so a step covers a known number of
-    // blocks; whole-width blocks are data dependent (twice the mean spacing is used).
-    // Block-punched lists keep the same number of locations of every channel.
     int span_req;
-    {
-        const int khw = p->KH * p->KW;
-        int64_t cols;
-        if (p->shared) cols = kKS;
-        else if (p->counts && p->nbc > 1) cols = max_step_span_cols(*p);
-        else if (p->counts)   // one block column: lists stretched over L slots, twice the mean spacing
-            cols = std::min<int64_t>(p->C, 2 * (int64_t)kKS * p->C / p->L + 1);
-        else if (p->reg == BSP_PUNCHED)   // a step may start at the last kept location of a channel
-            cols = (int64_t)(div_up(kKS, kept_count(p->khw, p->rate)) + 1) * p->khw;
-        else if (p->nbc > 1) cols = (int64_t)(div_up(kKS, kept_count(p->bw_eff, p->rate)) + 1) * p->bw_eff;
-        else cols = (int64_t)2 * kKS * p->rate;
-        span_req = (int)std::min<int64_t>(p->Cin, cols / khw + 2);
-    }
-    // mean channels one step advances (for the chunk count of a channel window)
     double step_ch;
-    {
-        const int khw = p->KH * p->KW;
-        if (p->shared) step_ch = (double)kKS / khw;
-        else if (p->counts) step_ch = (double)kKS * p->nbr * p->C / std::max<int64_t>(p->n_indices, 1) / khw;
-        else if (p->reg == BSP_PUNCHED) step_ch = (double)kKS / kept_count(p->khw, p->rate);
-        else if (p->nbc > 1) step_ch = (double)kKS * p->bw_eff / kept_count(p->bw_eff, p->rate) / khw;
-        else step_ch = (double)kKS * p->rate / khw;
-    }
+    list_spans(*p, &span_req, &step_ch);
 
     const int astep = 64 * 8 * p->esize;   // weight bytes of one m-tile and step
     const int n_mt = p->n_groups * p->mt_per_group;
@@ -636,135 +779,46 @@ bsp_status make_plan(const bsp_scheme *s, const bsp_conv_shape *conv, bsp_dtype 
             return BSP_OK;
         }
     }
-    const double total_groups = (double)nominal_rows * p->GPR;
-    // LDS budgets per workgroup: 1, 2, 3 or 4 workgroups per CU (160 KB, minus static tables)
-    const int budgets[4] = {160 * 1024 - kLdsStatic, 80 * 1024 - kLdsStatic, 53 * 1024 - kLdsStatic,
-                            40 * 1024 - kLdsStatic};
-
-    double best = 1e300;
-    Plan bestp = *p;
-    // a second pass admits m-blocks much larger than the layer when nothing else fits
-    for (int relax = 0; relax < 2 && best >= 1e300; ++relax)
-    for (int nsub = 1; nsub <= 4; nsub *= 2) {
-        const int TG = kGroups * nsub;
-        const int trw = rows_spanned(TG, p->GPR);
-        if (trw > kMaxTileRows) continue;
-        const int nslot = max_slots(TG, p->GPR, p->Ho, p->KH, p->SH, p->PH);
-        if (nslot > kMaxSlots) continue;
-        const int chs = p->V * nslot * p->RS;             // patch elements per channel
-        if (p->V * nslot * p->RG > 512) continue;         // granules per channel: per-tile lookup table
-        const int Q = kWaves / nsub;
-        const double n_pt = std::ceil(total_groups / TG);
-        for (int qmode = 0; qmode <= 1; ++qmode) {
-            if (qmode == 1 && Q == 1) continue;
-            const int KS = qmode ? Q : 1;
-            for (int TM = 1; TM <= 4; TM *= 2) {
-                // instantiated kernels: fp32 and per-element gathers at most 2 m-tiles per
-                // wave and no step split; 16-byte stride-2 gathers at most 4 m-tiles
-                const bool narrow = p->esize == 4 || p->gather == 0;
-                if (narrow && (TM > 2 || qmode == 1)) continue;
-                if (p->gather == 2 && TM > 4) continue;
-                int TPG, MBT, MBG, n_mb;
-                MBT = TM * (qmode == 0 ? Q : 1);
-                if (p->shared) {
-                    TPG = TM;
-                    if (!relax && MBT > 1 && MBT >= 2 * n_mt) continue;     // mostly idle waves
-                    MBG = 1;
-                    n_mb = div_up(n_mt, MBT);
-                } else {
-                    TPG = std::min(TM, mpg);
-                    if (TM % TPG) continue;
-                    if (MBT % mpg != 0 && mpg % MBT != 0) continue;
-                    if (!relax && MBT > 1 && MBT >= 2 * n_mt) continue;
-                    MBG = std::max(1, MBT / mpg);
-                    n_mb = div_up(n_mt, MBT);
-                }
-                const int64_t d_res = align256((int64_t)MBG * p->LP * 2);
-                const int64_t a_all = (int64_t)MBT * p->S * astep;
-                for (int bi = 0; bi < (relax ? 4 : 1); ++bi) {   // measured: one workgroup per CU with large chunks is best
-                    const int64_t budget = budgets[bi];
-                    for (int opt = 0; opt < 10; ++opt) {
-                        const int nb = opt < 5 ? 3 : 2;   // buffers (two when three do not fit)
-                        const int resident = opt % 5 == 0;
-                        const int smax = resident ? 0 : (1 << (opt % 5 - 1));   // 1, 2, 4, 8
-                        if (!resident && smax > p->S) continue;
-                        const int64_t astage = resident ? 0 : (int64_t)MBT * smax * astep;
-                        const int64_t fixed = d_res + (resident ? align256(a_all) : 0) + 256;
-                        const int64_t free_b = budget - fixed - nb * align256(astage) - nb * 512;
-                        if (free_b <= 0) continue;
-                        // patches are whole 1 KB copy slots of four waves (256 granules)
-                        int64_t cc = free_b / (nb * 4096) * kThreads / ((int64_t)p->V * nslot * p->RG);
-                        cc = std::min<int64_t>(cc, std::min(p->Cin, kMaxCC));
-                        cc = std::min<int64_t>(cc, 65536 / chs);                       // 16-bit offsets
-                        if (cc < span_req || cc < 1) continue;
-                        int fr = (int)div_up64(cc * p->V * nslot * p->RG, kThreads);
-                        if (fr > 32) {   // copies per wave and chunk: one bit each in the fixup mask
-                            cc = 32 * kThreads / ((int64_t)p->V * nslot * p->RG);
-                            if (cc < span_req || cc < 1) continue;
-                            fr = (int)div_up64(cc * p->V * nslot * p->RG, kThreads);
-                        }
-                        const int64_t lds_patch = (int64_t)fr * 4096;   // whole 1 KB copy slots of four waves
-                        const int64_t lds_buf = lds_patch + align256(astage);
-                        int64_t total = fixed + nb * lds_buf + (p->gather == 3 ? 256 : 0);   // MODE 3 reads run past the patch
-                        if (qmode == 1) total = std::max<int64_t>(total, (int64_t)2 * TM * 4096);   // partial sums
-                        if (total > budget) continue;
-
-                        // ---- score (nominal batch), in CU cycles ----
-                        // persistent workgroups: occ per CU, each walking tpw pixel tiles
-                        const int occ = std::min(fwd_occ(p->gather, TM, TPG), (160 * 1024) / (int)(total + kLdsStatic));
-                        if (occ < 1) continue;
-                        double wpm = std::max(1.0, std::ceil(256.0 * occ / n_mb));
-                        if (KS > 1 || wpm > n_pt) wpm = n_pt;
-                        const double tpw = std::ceil(n_pt / wpm);
-                        const double n_wg = std::ceil(n_pt / tpw) * n_mb;
-                        const double rounds = std::ceil(n_wg / (256.0 * occ));
-                        // steps per chunk: consecutive steps advance step_ch channels each
-                        // (staged weights: at most SMAX); the real count depends on the lists
-                        double spc = std::max(1.0, (cc - 1) / step_ch);
-                        if (!resident) spc = std::min<double>(spc, smax);
-                        const double nch = std::max(1.0, p->S / spc);
-                        // Serial time of one wave per chunk, fitted to measured plans on gfx950
-                        // (ResNet-50 3x3 layers, 4x column pruning): a fixed cost (copy table
-                        // reads, fixups, barrier, pipeline refill), each stage (8 kept columns
-                        // gathered and 4 MFMAs per m-tile list; stride-2 gathers read 4 dwords
-                        // per column), each 1 KB copy (twice when input rows start off 16-byte
-                        // boundaries); three buffers make chunks smaller and cost more per chunk.
-                        const double stages = std::ceil(spc / KS) * (TM / TPG);
-                        const double copies = fr + (resident ? 0.0 : (double)astage / 4096.0);
-                        const bool mis = ((int64_t)p->W * p->esize) % 16 != 0;
-                        double per_chunk = 3000.0 + stages * (p->SW == 2 ? 900.0 : 500.0) + copies * (mis ? 100.0 : 50.0);
-                        if (nb == 3) per_chunk *= 1.2;
-                        if (occ > 1) per_chunk *= 0.8 * occ;                               // workgroups sharing a CU
-                        // per tile: epilogue; per workgroup: header, tables, first fill
-                        double cyc = rounds * (tpw * nch * per_chunk + tpw * 8000.0 + 8000.0);
-                        const double hbm = ((double)nominal_rows / p->Ho * p->Cin * p->H * p->W * p->esize +
-                                            total_groups * 4 * p->RK * 2.0) / 5.5e12 * 2.4e9;
-                        cyc = std::max(cyc, hbm);
-                        if (qmode == 1) cyc = cyc * 1.5 + 1500.0;                           // partial-sum reduction
-                        if (cyc < best * (1 - 1e-9)) {
-                            best = cyc;
-                            Plan q = *p;
-                            q.NSUB = nsub; q.TRWMAX = trw; q.NSLOT = nslot; q.CH_STRIDE = chs; q.VS = nslot * p->RS;
-                            q.CC = (int)cc; q.FR = fr;
-                            q.qmode = qmode; q.KS = KS; q.TM = TM; q.TPG = TPG;
-                            q.MBT = MBT; q.MBG = MBG; q.n_mb = n_mb;
-                            q.resident = resident; q.SMAX = smax; q.NB = nb;
-                            q.lds_d = (int)d_res;
-                            q.lds_a = resident ? (int)align256(a_all) : 0;
-                            q.lds_patch = (int)lds_patch;
-                            q.lds_astage = (int)align256(astage);
-                            q.lds_buf = (int)lds_buf;
-                            q.lds_total = (int)total;
-                            bestp = q;
-                        }
-                    }
-                }
-            }
+    // The forward layout.  Per-block-row lists (column, block-punched and row-and-column
+    // blocks without per-block counts) against the zero-expanded layout (one identity
+    // list shared by every m-tile, pruned weights zero in the tiles).  Block-rows shorter
+    // than a 16-row MFMA tile each take a tile of their own, so their lists execute
+    // (16 / bh) x the kept fraction of the dense work, with a gather per tile.  Measured
+    // on the block-size sweep layer (3x3 256->256 56x56), such lists were slower than the
+    // zero-expanded layout whenever that product was 1/5 or more, and the model's score
+    // of them was low by about 1.34 times more than its score of the zero-expanded
+    // layout; so with that product at 1/5 or more the zero-expanded layout is taken when
+    // its score is under 1.34 of the lists'.  Other lists give way to it when its score
+    // is under 0.7 of theirs (lists whose channel windows are very wide).
+    auto search = [&](Plan *q) {
+        int sr;
+        double sc;
+        list_spans(*q, &sr, &sc);
+        return search_tiling(q, sr, sc, q->n_groups * q->mt_per_group, q->mt_per_group, astep, nominal_rows);
+    };
+    Plan lists = *p;
+    const bool alt = !p->shared && !p->counts && !p->is_linear;
+    const bool padded_dense = alt && p->bh_eff < kMT &&
+                              (double)kMT / p->bh_eff * ((double)p->L / p->C) >= 0.2;
+    double best = search(&lists);
+    if (alt) {
+        Plan d = *p;
+        d.shared = 1;
+        d.L = p->C;
+        d.n_groups = 1;
+        d.group_rows = p->R;
+        d.mt_per_group = div_up(p->R, kMT);
+        d.LP = div_up(d.L, kKS) * kKS;
+        d.S = d.LP / kKS;
+        const double bd = search(&d);
+        if (bd < (padded_dense ? 1.34 : 0.7) * best) {
+            lists = d;
+            best = bd;
         }
     }
     if (best >= 1e300) return BSP_EUNSUPPORTED;
-    *p = bestp;
-    finish_layout(p, n_mt, astep);
+    *p = lists;
+    finish_layout(p, p->n_groups * p->mt_per_group, astep);
     return BSP_OK;
 }
 

@@ -84,6 +84,50 @@ class Setting:
         return (self.bh or rows) * (self.bw or cols)
 
 
+# MI355X peaks the roofline fractions are taken against (dense bf16 MFMA, HBM3E)
+PEAK_BF16_FLOPS = 2.5166e15
+PEAK_HBM_BYTES = 8.0e12
+
+
+def _kept_of(extent: int, block: int, rate: int) -> int:
+    """Kept groups of an extent cut into blocks (0: one block), each keeping
+    ceil(block / rate) (Sec. 4.1.1; the last block may be ragged)."""
+    b = block or extent
+    full, last = divmod(extent, b)
+    return full * -(-b // rate) + (-(-last // rate) if last else 0)
+
+
+def kept_fraction(s: Setting) -> float:
+    """Fraction of the GEMM-form weights a setting keeps, from its scheme alone."""
+    khw = s.kh * s.kw
+    rows, cols = s.cout, s.cin * khw
+    if s.regularity == 3:
+        return 1.0
+    if s.regularity == 1:
+        return _kept_of(cols, s.bw, s.rate) / cols
+    if s.regularity == 0:
+        return _kept_of(rows, s.bh, s.rate) / rows
+    if s.regularity == 4:
+        return -(-khw // s.rate) / khw
+    if s.regularity == 6:      # 4 of 9 weights of each kept kernel; connectivity keeps ceil(9 n / 4 r) of n
+        n = rows * s.cin
+        return 4.0 * min(n, -(-9 * n // (4 * s.rate))) / (9 * n)
+    n = rows * cols
+    return -(-n // s.rate) / n
+
+
+def roofline(s: Setting, ms: float):
+    """(roofline fraction, bound) of one measured setting: the larger of the kept-FLOP
+    time at the bf16 MFMA peak and the algorithmic HBM time (input, output, kept
+    weights, bf16) at the HBM peak, over the measured time."""
+    kept = kept_fraction(s)
+    t_mfma = 2.0 * s.macs() * kept / PEAK_BF16_FLOPS
+    nbytes = 2.0 * (s.batch * s.cin * s.h * s.w + s.batch * s.cout * s.ho * s.wo +
+                    kept * s.cout * s.cin * s.kh * s.kw)
+    t_hbm = nbytes / PEAK_HBM_BYTES
+    return max(t_mfma, t_hbm) / (ms * 1e-3), ("mfma" if t_mfma > t_hbm else "hbm")
+
+
 class LatencyModel:
     """Measured forward latency (milliseconds) per setting."""
 
@@ -266,11 +310,30 @@ def report(model: LatencyModel, betas=(0.0, 0.1, 0.2, 0.5)) -> str:
                 name = "whole" if b == (0, 0) else f"{b[0]}x{b[1]}"
                 out.append(f"| {name} | " + " | ".join(cells) + " |")
             out.append("")
+        out.append("roofline fraction of each setting (the larger of the kept-FLOP time at the bf16 MFMA peak and the "
+                   "algorithmic HBM time at 8 TB/s, over the measured time; m: MFMA-bound, h: HBM-bound)\n")
+        out.append("| regularity | block | " + " | ".join(f"{r}x" for r in rates) + " |")
+        out.append("|---|---|" + "---|" * len(rates))
+        for reg in BLOCK_REGS:
+            rs = [s for s in st if s.regularity == reg]
+            for b in sorted({(s.bh, s.bw) for s in rs}, key=lambda b: (b == (0, 0), b)):
+                cells = []
+                for r in rates:
+                    x = [s for s in rs if (s.bh, s.bw) == b and s.rate == r]
+                    if not x:
+                        cells.append("-")
+                        continue
+                    f, bound = roofline(x[0], model.latency(x[0]))
+                    cells.append(f"{f:.3f} {bound[0]}")
+                name = "whole" if b == (0, 0) else f"{b[0]}x{b[1]}"
+                out.append(f"| {REG_NAMES[reg]} | {name} | " + " | ".join(cells) + " |")
+        out.append("")
         refs = [s for s in st if s.regularity in (2, 3, 6)]
         if refs:
             names = {2: "unstructured", 3: "dense", 6: "pattern (8 patterns)"}
             out.append("reference points: " + ", ".join(
-                f"{names[s.regularity]}{'' if s.regularity == 3 else f' {s.rate}x'} {model.latency(s) * 1e3:.1f} us"
+                f"{names[s.regularity]}{'' if s.regularity == 3 else f' {s.rate}x'} {model.latency(s) * 1e3:.1f} us "
+                f"(roofline {roofline(s, model.latency(s))[0]:.3f})"
                 for s in sorted(refs, key=lambda s: (s.regularity, s.rate))) + "\n")
         out.append("rule choice (smallest block within (1 + beta) of whole-matrix blocks, latency per dense MAC):\n")
         out.append("| regularity | rate | " + " | ".join(f"beta {b:g}" for b in betas) + " |")

@@ -127,3 +127,24 @@ def test_network_settings_cover_every_distinct_layer():
                                           "1x1/2 256->512 56x56 b64"}
     assert all(s.pad == s.kh // 2 for s in st)
     assert {s.regularity for s in st if s.kh == 3} == {0, 1, 4}
+
+
+def test_kept_fraction_from_the_scheme_and_roofline_bound():
+    # kept groups per block are ceil(extent / rate) (Sec. 4.1.1): a 4-column block keeps
+    # 1 at 4x, 8x and 16x alike; a ragged last block keeps ceil(its width / rate)
+    from paper_2111_11581_amd.latency import kept_fraction, roofline
+    col44 = [Setting(256, 256, 56, 56, 3, 3, 1, 1, 64, 1, 4, 4, r) for r in (2, 4, 8, 16)]
+    assert [kept_fraction(s) for s in col44] == [0.5, 0.25, 0.25, 0.25]
+    # 10 columns in blocks of 4: 4 + 4 + 2 -> at 4x keep 1 + 1 + 1 of 10
+    assert kept_fraction(Setting(10, 8, 1, 1, 1, 1, 1, 0, 1, 1, 8, 4, 4)) == 3 / 10
+    # rows of 20 in blocks of 8 (8 + 8 + 4) at 3x keep 3 + 3 + 2 of 20
+    assert kept_fraction(Setting(10, 20, 1, 1, 1, 1, 1, 0, 1, 0, 8, 8, 3)) == 8 / 20
+    # block-punched at 4x keeps ceil(9 / 4) = 3 of 9 kernel locations
+    assert kept_fraction(Setting(64, 64, 8, 8, 3, 3, 1, 1, 1, 4, 16, 8, 4)) == 3 / 9
+    dense = Setting(256, 256, 56, 56, 3, 3, 1, 1, 64, 3, 0, 0, 1)
+    assert kept_fraction(dense) == 1.0
+    # dense 3x3 256->256 56x56 b64: 2 * 64 * 256 * 56 * 56 * 2304 flops at 2.5166 PFLOP/s
+    # is 94.1 us (MFMA-bound: the bytes take 13.2 us at 8 TB/s)
+    t_roof = 2.0 * 64 * 256 * 56 * 56 * 2304 / 2.5166e15
+    f, bound = roofline(dense, t_roof * 1e3 * 2)
+    assert bound == "mfma" and abs(f - 0.5) < 1e-12
