@@ -519,8 +519,13 @@ static double search_tiling(Plan *p, int span_req, double step_ch, int n_mt, int
                         const double n_wg = std::ceil(n_pt / tpw) * n_mb;
                         const double rounds = std::ceil(n_wg / (256.0 * occ));
                         // steps per chunk: consecutive steps advance step_ch channels each
-                        // (staged weights: at most SMAX); the real count depends on the lists
-                        double spc = std::max(1.0, (cc - 1) / step_ch);
+                        // (staged weights: at most SMAX); the real count depends on the lists.
+                        // Block-punched steps cover whole channels from a channel boundary,
+                        // so a chunk holds a whole number of them.
+                        double spc = p->reg == BSP_PUNCHED && !p->counts
+                                         ? std::floor((double)cc / step_ch + 1e-9)
+                                         : (cc - 1) / step_ch;
+                        spc = std::max(1.0, spc);
                         if (!resident) spc = std::min<double>(spc, smax);
                         const double nch = std::max(1.0, p->S / spc);
                         // Serial time of one wave per chunk, fitted to measured plans on gfx950
