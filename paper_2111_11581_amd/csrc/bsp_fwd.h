@@ -81,6 +81,26 @@ __device__ __forceinline__ void dma16(const void *src, uint32_t lds_base) {
                  : "memory");
 }
 
+// Pointer made wave-uniform (held in scalar registers).
+__device__ __forceinline__ const void *uni_ptr(const void *p) {
+    const uint64_t v = (uint64_t)(uintptr_t)p;
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)v);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(v >> 32));
+    return (const void *)(uintptr_t)(((uint64_t)hi << 32) | lo);
+}
+
+// As dma16 with the source split into a wave-uniform base (scalar registers) and a
+// per-lane 32-bit byte offset: lane l copies 16 bytes at sbase + voff to LDS byte
+// m0 + 16 l.  No 64-bit address arithmetic per copy.
+__device__ __forceinline__ void dma_sv(const void *sbase, uint32_t voff, uint32_t m0) {
+    uint32_t saved;
+    asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %3\n\ts_nop 0\n\t"
+                 "global_load_lds_dwordx4 %1, %2\n\ts_mov_b32 m0, %0"
+                 : "=&s"(saved)
+                 : "v"(voff), "s"(uni_ptr(sbase)), "s"(uni((int)m0))
+                 : "memory");
+}
+
 // Contiguous copy of n16 16-byte granules from src to the LDS byte address dst.
 __device__ __forceinline__ void dma_run(const unsigned char *src, uint32_t dst, int n16) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -718,9 +738,15 @@ __global__ __launch_bounds__(kFwdThreads, 1) void k_fwd(ConvArgs a) {
             E *dst = (E *)gp;
             const int64_t e = (int64_t)off + cbase;
             if (e < 0 || e + a.GE > a.x_total) {
+                // all loads first, then the writes: one wait for the granule
+                constexpr int kGE = 16 / (int)sizeof(E);
                 const E *src = (const E *)a.x + e;
-                for (int i2 = 0; i2 < a.GE; ++i2)
-                    dst[i2] = (i2 >= head && i2 < a.GE - tail && e + i2 >= 0 && e + i2 < a.x_total) ? src[i2] : (E)0;
+                E v[kGE];
+#pragma unroll
+                for (int i2 = 0; i2 < kGE; ++i2)
+                    v[i2] = (i2 >= head && i2 < kGE - tail && e + i2 >= 0 && e + i2 < a.x_total) ? src[i2] : (E)0;
+#pragma unroll
+                for (int i2 = 0; i2 < kGE; ++i2) dst[i2] = v[i2];
             } else {
                 // keep bytes [head, GE - tail) elements of the 16-byte granule, zero the rest
                 const int lo = head * (int)sizeof(E), hi = 16 - tail * (int)sizeof(E);

@@ -96,6 +96,12 @@ __global__ __launch_bounds__(kPlThreads, 1) void k_pl(PwArgs a) {
     int c_of[PCOPY];       // its channel within a step
     bool g_live[PCOPY];    // the granule holds output pixels
     int cur_tile = -1;
+    // fast path: sources as a scalar base plus a 32-bit per-lane byte offset
+    const int rwu = uni(rw);
+    const unsigned char *xbu = (const unsigned char *)uni_ptr(xb);
+    uint32_t w_voff[WCOPY];   // weight tile u of this wave: lane bytes, relative to tile 0
+#pragma unroll
+    for (int u = 0; u < WCOPY; ++u) w_voff[u] = (uint32_t)(lane * 16 + u * S * 1024);
     auto set_tile = [&](int t) {
         if (t == cur_tile) return;
         cur_tile = t;
@@ -122,6 +128,25 @@ __global__ __launch_bounds__(kPlThreads, 1) void k_pl(PwArgs a) {
     auto fill = [&](int t, int st, int b) {
         set_tile(t);
         const uint32_t buf = bufs0 + (uint32_t)(b * stage_b);
+        if (t != a.n_pt - 1 && (st + 1) * SPS <= S && (st + 1) * SPS * 32 <= a.Cin) {
+            // every granule of the stage is inside x and every channel exists (not the
+            // last tile, not past the K loop): scalar bases, one VALU add per copy
+            for (int j = 0; j < SPS; ++j) {
+                const int s = st * SPS + j;
+                const uint32_t pb = buf + (uint32_t)(j * PB);
+                const uint32_t step_b = (uint32_t)s * 64u * (uint32_t)xcs;   // 32 channels, bytes
+#pragma unroll
+                for (int k = 0; k < PCOPY; ++k)
+                    dma_sv(xbu, (uint32_t)e_base[k] * 2u + step_b, pb + (uint32_t)((rwu * PCOPY + k) * 1024));
+                if (!res) {
+                    const unsigned char *wbase = A_g + ((size_t)(mt_first + rwu * WCOPY) * S + s) * 1024;
+                    const uint32_t wb = buf + (uint32_t)(SPS * PB + j * MT * 1024);
+#pragma unroll
+                    for (int u = 0; u < WCOPY; ++u) dma_sv(wbase, w_voff[u], wb + (uint32_t)((rwu * WCOPY + u) * 1024));
+                }
+            }
+            return;
+        }
         for (int j = 0; j < SPS; ++j) {
             const int s = st * SPS + j;
             const uint32_t pb = buf + (uint32_t)(j * PB);
@@ -151,9 +176,11 @@ __global__ __launch_bounds__(kPlThreads, 1) void k_pl(PwArgs a) {
         }
     };
     // after stage st of tile t landed in buffer b: granules that would read past the
-    // end of x, element by element (only granules of the last tile can)
+    // end of x, element by element.  Only the last channel of the last image ends
+    // there, so only the last stage of the last tile can hold such granules; every
+    // other item returns at once (the element loads wait for all copies in flight).
     auto tail = [&](int t, int st, int b) {
-        if (t != a.n_pt - 1) return;
+        if (t != a.n_pt - 1 || st != NS - 1) return;
         set_tile(t);
         for (int j = 0; j < SPS; ++j) {
             const int s = st * SPS + j;
@@ -163,7 +190,12 @@ __global__ __launch_bounds__(kPlThreads, 1) void k_pl(PwArgs a) {
                 if (g_live[k] && s < S && s * 32 + c_of[k] < a.Cin && e + 8 > a.x_total) {
                     uint16_t *dst = (uint16_t *)(bufs + b * stage_b + j * PB + ((rw * PCOPY + k) * 64 + lane) * 16);
                     const uint16_t *sx = (const uint16_t *)a.x + e;
-                    for (int i2 = 0; i2 < 8; ++i2) dst[i2] = e + i2 < a.x_total ? sx[i2] : (uint16_t)0;
+                    // all loads first, then the writes: one wait for the granule
+                    uint16_t v[8];
+#pragma unroll
+                    for (int i2 = 0; i2 < 8; ++i2) v[i2] = e + i2 < a.x_total ? sx[i2] : (uint16_t)0;
+#pragma unroll
+                    for (int i2 = 0; i2 < 8; ++i2) dst[i2] = v[i2];
                 }
             }
         }
