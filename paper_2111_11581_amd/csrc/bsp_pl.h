@@ -47,7 +47,7 @@ __global__ __launch_bounds__(kPlThreads, 1) void k_pl(PwArgs a) {
     static_assert(32 * GPC % kThreads == 0 && MT % kWaves == 0, "whole copies per wave");
     constexpr int PB = 32 * RB;                   // LDS bytes of one step's patch
     extern __shared__ __attribute__((aligned(256))) unsigned char lds[];
-    __shared__ float s_bias[kMaxMBRows];
+    __shared__ __attribute__((aligned(16))) float s_bias[kMaxMBRows];
     __shared__ int s_orow[MAP ? kMaxMBRows : 1];
 
     // workgroup -> (range of pixel tiles, m-block); each XCD (workgroup id % 8) gets
@@ -262,31 +262,44 @@ __global__ __launch_bounds__(kPlThreads, 1) void k_pl(PwArgs a) {
         const int p0 = oh * a.Wo + 4 * gi;
         const int nvalid = pix_ok ? max(0, min(4, a.Wo - 4 * gi)) : 0;
         const float qnan = __builtin_nanf("");
+        // lane masks of the tile: whole 4-pixel groups, and element e of partial groups
+        const uint64_t full_px = ballot(nvalid == 4);
+        const uint64_t part_px = ballot(nvalid > 0 && nvalid < 4);
+        uint64_t part_e[3];
+#pragma unroll
+        for (int e = 0; e < 3; ++e) part_e[e] = part_px & ballot(e < nvalid);
+        const int64_t ybase = (int64_t)img * a.y_is + p0;   // output row 0 at the lane's pixels
 #pragma unroll
         for (int t2 = 0; t2 < TM; ++t2) {
+            const int r0 = (m_loc0 + t2) * kMT + 4 * kg;     // the lane's first row in the m-block
+            const int crow0 = mt_first * kMT + r0;             // its computed row
+            const bool all_rows = uni((mt_first + m_loc0 + t2 + 1) * kMT <= a.R ? 1 : 0) != 0;   // wave-uniform
+            float4 bv = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (a.bias) bv = *(const float4 *)&s_bias[r0];
+            const float bvs[4] = {bv.x, bv.y, bv.z, bv.w};
+            int64_t yrow = ybase + (int64_t)(crow0 < a.R ? crow0 : 0) * a.y_cs;
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                const int r = (m_loc0 + t2) * kMT + 4 * kg + i;   // row of the m-block
-                const int crow = mt_first * kMT + r;               // computed row
+                const int crow = crow0 + i;
                 const bool row_ok = crow < a.R;
-                const int orow = MAP ? s_orow[r] : crow;
-                const float bv = a.bias ? s_bias[r] : 0.f;
+                const uint64_t rmask = all_rows ? ~0ull : ballot(row_ok);
+                int64_t yo = yrow + (int64_t)i * a.y_cs;
+                if constexpr (MAP) yo = ybase + (int64_t)(row_ok ? s_orow[r0 + i] : 0) * a.y_cs;
+                if (!all_rows && !row_ok) yo = ybase;
                 float o[4];
 #pragma unroll
-                for (int nt = 0; nt < 4; ++nt) o[nt] = ok ? epi(acc[t2][nt][i], bv, a.relu) : qnan;
-                const int64_t yo = (int64_t)img * a.y_is + (int64_t)(row_ok ? orow : 0) * a.y_cs + p0;
-                const uint64_t full = ballot(row_ok && nvalid == 4);
-                const uint64_t part = ballot(row_ok && nvalid > 0 && nvalid < 4);
+                for (int nt = 0; nt < 4; ++nt) o[nt] = ok ? epi(acc[t2][nt][i], bvs[i], a.relu) : qnan;
+                const uint64_t full = full_px & rmask;
                 if (a.out_bf16) {
                     uint16_t *y = (uint16_t *)a.y + yo;
                     uint32_t h[4];
 #pragma unroll
                     for (int nt = 0; nt < 4; ++nt) h[nt] = f32_to_bf16_rne(o[nt]);
                     if (full) st_mask_b64(y, u32x2{h[0] | (h[1] << 16), h[2] | (h[3] << 16)}, full);
-                    if (part) {
+                    if (part_px) {
 #pragma unroll
                         for (int e = 0; e < 3; ++e) {
-                            const uint64_t me = part & ballot(e < nvalid);
+                            const uint64_t me = part_e[e] & rmask;
                             if (me) st_mask_b16(y + e, h[e], me);
                         }
                     }
@@ -295,10 +308,10 @@ __global__ __launch_bounds__(kPlThreads, 1) void k_pl(PwArgs a) {
                     if (full)
                         st_mask_b128(y, u32x4{__float_as_uint(o[0]), __float_as_uint(o[1]), __float_as_uint(o[2]),
                                               __float_as_uint(o[3])}, full);
-                    if (part) {
+                    if (part_px) {
 #pragma unroll
                         for (int e = 0; e < 3; ++e) {
-                            const uint64_t me = part & ballot(e < nvalid);
+                            const uint64_t me = part_e[e] & rmask;
                             if (me) st_mask_b32(y + e, __float_as_uint(o[e]), me);
                         }
                     }
