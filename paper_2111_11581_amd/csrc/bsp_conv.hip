@@ -45,6 +45,33 @@ static fwd_fn pick(int dt, int mode, int TM, int TPG, int KS, bool map) {
 // 16-byte stores where the plane allows them.  Tiles packed for another plan (header
 // check): the list of pruned rows is not read; rows R - n_pruned .. R - 1 get NaN,
 // the forward kernel fills the others with NaN, so the whole output is NaN.
+__device__ __forceinline__ int fill_row(const int32_t *pruned, bool ok, int R, int n_pruned, int j) {
+    return ok ? pruned[j] : R - n_pruned + j;
+}
+template <typename E>
+__device__ __forceinline__ E fill_value(bool ok, const float *bias, int o, int relu) {
+    const float v = ok ? fwd::epi(0.f, bias ? bias[o] : 0.f, relu) : __builtin_nanf("");
+    if constexpr (sizeof(E) == 2) return (E)fwd::f32_to_bf16_rne(v);
+    else return v;
+}
+// Planes smaller than a workgroup (small images): one thread per element of the
+// flattened (plane, element) range, fewer than 2^32 elements.
+template <typename E>
+__global__ void k_fill_pruned_small(E *__restrict__ y, const uint8_t *__restrict__ tiles, int64_t off_pruned,
+                                    uint32_t fp_lo, uint32_t fp_hi, const float *__restrict__ bias, int relu, int R,
+                                    int n_pruned, uint32_t total, uint32_t plane, int64_t img_stride,
+                                    int64_t ch_stride) {
+    const TileHeader *hdr = (const TileHeader *)tiles;
+    const bool ok = hdr->magic == kMagic && hdr->fp_lo == fp_lo && hdr->fp_hi == fp_hi;
+    const int32_t *pruned = (const int32_t *)(tiles + off_pruned);
+    for (uint32_t idx = blockIdx.x * blockDim.x + threadIdx.x; idx < total; idx += gridDim.x * blockDim.x) {
+        const uint32_t pi = idx / plane, e = idx - pi * plane;
+        const uint32_t img = pi / (uint32_t)n_pruned, j = pi - img * (uint32_t)n_pruned;
+        const int o = fill_row(pruned, ok, R, n_pruned, (int)j);
+        if (o < 0 || o >= R) continue;   // not a row of the output
+        y[(int64_t)img * img_stride + (int64_t)o * ch_stride + e] = fill_value<E>(ok, bias, o, relu);
+    }
+}
 template <typename E>
 __global__ void k_fill_pruned(E *__restrict__ y, const uint8_t *__restrict__ tiles, int64_t off_pruned, uint32_t fp_lo,
                               uint32_t fp_hi, const float *__restrict__ bias, int relu, int R, int n_pruned,
@@ -56,12 +83,9 @@ __global__ void k_fill_pruned(E *__restrict__ y, const uint8_t *__restrict__ til
     for (int64_t pi = blockIdx.x; pi < n_planes; pi += gridDim.x) {
         const int64_t img = pi / n_pruned;
         const int j = (int)(pi - img * n_pruned);
-        const int o = ok ? pruned[j] : R - n_pruned + j;
+        const int o = fill_row(pruned, ok, R, n_pruned, j);
         if (o < 0 || o >= R) continue;   // not a row of the output
-        const float v = ok ? fwd::epi(0.f, bias ? bias[o] : 0.f, relu) : __builtin_nanf("");
-        E ev;
-        if constexpr (sizeof(E) == 2) ev = fwd::f32_to_bf16_rne(v);
-        else ev = v;
+        const E ev = fill_value<E>(ok, bias, o, relu);
         E *base = y + img * img_stride + (int64_t)o * ch_stride;
         if (((uintptr_t)base & 15) == 0 && plane % VE == 0) {
             union { E e[VE]; uint4 u; } w;
@@ -81,8 +105,21 @@ static hipError_t launch_fill_pruned(const Plan &p, int64_t n_img, int64_t plane
     const int n_pruned = p.R - p.RK;
     const int64_t n_planes = n_img * n_pruned;
     if (!p.rowmap || n_planes <= 0 || plane <= 0) return hipSuccess;
-    const int grid = (int)std::min<int64_t>(n_planes, 16384);
     const uint32_t lo = (uint32_t)p.fingerprint, hi = (uint32_t)(p.fingerprint >> 32);
+    const int64_t total = n_planes * plane;
+    if (plane < 256 && total < ((int64_t)1 << 32)) {
+        const int g = (int)std::min<int64_t>((total + 255) / 256, 16384);
+        if (out_bf16)
+            k_fill_pruned_small<uint16_t><<<g, 256, 0, st>>>((uint16_t *)y, tiles, p.off_pruned, lo, hi, bias, relu,
+                                                             p.R, n_pruned, (uint32_t)total, (uint32_t)plane,
+                                                             img_stride, ch_stride);
+        else
+            k_fill_pruned_small<float><<<g, 256, 0, st>>>((float *)y, tiles, p.off_pruned, lo, hi, bias, relu, p.R,
+                                                          n_pruned, (uint32_t)total, (uint32_t)plane, img_stride,
+                                                          ch_stride);
+        return hipGetLastError();
+    }
+    const int grid = (int)std::min<int64_t>(n_planes, 16384);
     if (out_bf16)
         k_fill_pruned<uint16_t><<<grid, 256, 0, st>>>((uint16_t *)y, tiles, p.off_pruned, lo, hi, bias, relu, p.R,
                                                       n_pruned, n_planes, plane, img_stride, ch_stride);

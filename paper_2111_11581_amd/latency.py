@@ -277,14 +277,48 @@ def measure(settings, reps: int = 10, rounds: int = 10, seed: int = 1234, device
     return model
 
 
+def summary(model: LatencyModel, beta: float = 0.2) -> str:
+    """Markdown table of the rule's block size per layer, regularity and rate at one
+    beta, with the chosen setting's latency beside the whole-matrix one (us)."""
+    layers = {}
+    for s in model.settings.values():
+        layers.setdefault(s.layer_key(), []).append(s)
+    out = []
+    for r in sorted({s.rate for s in model.settings.values() if s.regularity in BLOCK_REGS}):
+        regs = [g for g in BLOCK_REGS if any(s.regularity == g and s.rate == r for s in model.settings.values())]
+        out.append(f"## Block size per layer at beta = {beta:g} (rate {r}): choice (its latency / whole-matrix "
+                   f"latency, us)\n")
+        out.append("| layer | " + " | ".join(REG_NAMES[g] for g in regs) + " |")
+        out.append("|---|" + "---|" * len(regs))
+        for lk in sorted(layers):
+            st = layers[lk]
+            cells = []
+            for g in regs:
+                try:
+                    bh, bw = select_block_size(model, st[0], g, r, beta)
+                except KeyError:
+                    cells.append("-")
+                    continue
+                pick = [s for s in st if s.regularity == g and s.rate == r and (s.bh, s.bw) == (bh, bw)]
+                whole = [s for s in st if s.regularity == g and s.rate == r and (s.bh, s.bw) == (0, 0)]
+                name = "whole" if (bh, bw) == (0, 0) else f"{bh}x{bw}"
+                cells.append(f"{name} ({model.latency(pick[0]) * 1e3:.0f} / {model.latency(whole[0]) * 1e3:.0f})")
+            out.append(f"| {lk} | " + " | ".join(cells) + " |")
+        out.append("")
+    return "\n".join(out)
+
+
 def report(model: LatencyModel, betas=(0.0, 0.1, 0.2, 0.5)) -> str:
     """Markdown summary of a model: per layer, the latency of every block size and
     rate (and its ratio to whole-matrix pruning at the same regularity and rate), the
-    reference points, and the rule's choice for each beta."""
+    reference points, and the rule's choice for each beta.  A model of several layers
+    starts with the per-layer choice at beta 0.2 (or the middle beta given)."""
     out = []
     layers = {}
     for s in model.settings.values():
         layers.setdefault(s.layer_key(), []).append(s)
+    if len(layers) > 1:
+        out.append(summary(model, 0.2 if 0.2 in betas else betas[len(betas) // 2]))
     for lk in sorted(layers):
         st = layers[lk]
         rates = sorted({s.rate for s in st if s.regularity in BLOCK_REGS})
