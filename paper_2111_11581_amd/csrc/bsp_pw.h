@@ -156,7 +156,12 @@ __global__ __launch_bounds__(kThreads, pw_occ((int)sizeof(E), MODE, TM)) void k_
             if (c_rel < cd.w && e + GE > a.x_total) {
                 E *dst = (E *)(buf + ((size_t)v * 64 + lane) * 16);
                 const E *src = (const E *)a.x + e;
-                for (int i2 = 0; i2 < GE; ++i2) dst[i2] = e + i2 < a.x_total ? src[i2] : (E)0;
+                // all loads first, then the writes: one wait for the granule
+                E w[GE];
+#pragma unroll
+                for (int i2 = 0; i2 < GE; ++i2) w[i2] = e + i2 < a.x_total ? src[i2] : (E)0;
+#pragma unroll
+                for (int i2 = 0; i2 < GE; ++i2) dst[i2] = w[i2];
             }
         }
     };
