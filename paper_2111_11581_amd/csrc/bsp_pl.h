@@ -274,9 +274,29 @@ __global__ __launch_bounds__(kPlThreads, 1) void k_pl(PwArgs a) {
             const int r0 = (m_loc0 + t2) * kMT + 4 * kg;     // the lane's first row in the m-block
             const int crow0 = mt_first * kMT + r0;             // its computed row
             const bool all_rows = uni((mt_first + m_loc0 + t2 + 1) * kMT <= a.R ? 1 : 0) != 0;   // wave-uniform
-            float4 bv = make_float4(0.f, 0.f, 0.f, 0.f);
-            if (a.bias) bv = *(const float4 *)&s_bias[r0];
-            const float bvs[4] = {bv.x, bv.y, bv.z, bv.w};
+            // bias, ReLU and the header check on the accumulators, each only when it applies
+            // (uniform branches: most layers need one of them or none)
+            if (!ok) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+#pragma unroll
+                    for (int nt = 0; nt < 4; ++nt) acc[t2][nt][i] = qnan;
+            } else {
+                if (a.bias) {
+                    const float4 bv = *(const float4 *)&s_bias[r0];
+                    const float bvs[4] = {bv.x, bv.y, bv.z, bv.w};
+#pragma unroll
+                    for (int i = 0; i < 4; ++i)
+#pragma unroll
+                        for (int nt = 0; nt < 4; ++nt) acc[t2][nt][i] += bvs[i];
+                }
+                if (a.relu) {
+#pragma unroll
+                    for (int i = 0; i < 4; ++i)
+#pragma unroll
+                        for (int nt = 0; nt < 4; ++nt) acc[t2][nt][i] = acc[t2][nt][i] < 0.f ? 0.f : acc[t2][nt][i];
+                }
+            }
             int64_t yrow = ybase + (int64_t)(crow0 < a.R ? crow0 : 0) * a.y_cs;
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
@@ -288,7 +308,7 @@ __global__ __launch_bounds__(kPlThreads, 1) void k_pl(PwArgs a) {
                 if (!all_rows && !row_ok) yo = ybase;
                 float o[4];
 #pragma unroll
-                for (int nt = 0; nt < 4; ++nt) o[nt] = ok ? epi(acc[t2][nt][i], bvs[i], a.relu) : qnan;
+                for (int nt = 0; nt < 4; ++nt) o[nt] = acc[t2][nt][i];
                 const uint64_t full = full_px & rmask;
                 if (a.out_bf16) {
                     uint16_t *y = (uint16_t *)a.y + yo;

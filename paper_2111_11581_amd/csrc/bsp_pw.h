@@ -41,7 +41,7 @@ __global__ __launch_bounds__(kThreads, pw_occ((int)sizeof(E), MODE, TM)) void k_
     constexpr int AI = ASTEP / 1024;         // 1 KB copies per m-tile and step
     constexpr int GE = 16 / (int)sizeof(E);  // elements per granule
     extern __shared__ __attribute__((aligned(256))) unsigned char lds[];
-    __shared__ float s_bias[kMaxMBRows];
+    __shared__ __attribute__((aligned(16))) float s_bias[kMaxMBRows];
     __shared__ int s_orow[MAP ? kMaxMBRows : 1];   // output row of each row of the m-block (row map)
 
     // workgroup -> (range of pixel tiles, m-block); each XCD (workgroup id % 8) gets
@@ -211,33 +211,62 @@ __global__ __launch_bounds__(kThreads, pw_occ((int)sizeof(E), MODE, TM)) void k_
         const int oh = row - img * a.Ho;
         const int p0 = oh * a.Wo + 4 * gi;
         const int nvalid = pix_ok ? max(0, min(4, a.Wo - 4 * gi)) : 0;
-        const float qnan = __builtin_nanf("");
-        // row map (kept filter of each computed row), staged in LDS at the start
-        int omap[TM][4] = {};
-        if constexpr (MAP) {
+        // tiles of another plan: every output NaN (a NaN bias makes every sum NaN, and
+        // ReLU keeps NaN)
+        const float bad = ok ? 0.f : __builtin_nanf("");
+        // lane masks of the tile: whole 4-pixel groups, and element e of partial groups
+        const uint64_t full_px = ballot(nvalid == 4);
+        const uint64_t part_px = ballot(nvalid > 0 && nvalid < 4);
+        uint64_t part_e[3];
 #pragma unroll
-            for (int t2 = 0; t2 < TM; ++t2)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) omap[t2][i] = s_orow[(m_loc0 + t2) * kMT + 4 * kg + i];
-        }
+        for (int e = 0; e < 3; ++e) part_e[e] = part_px & ballot(e < nvalid);
+        const int64_t ybase = (int64_t)img * a.y_is + p0;   // output row 0 at the lane's pixels
         int n = 0;
 #pragma unroll
         for (int t2 = 0; t2 < TM; ++t2) {
             const int gm = mt_first + m_loc0 + t2;   // global m-tile
             const int gidx = gm / a.mt_per_group, mt_in = gm - gidx * a.mt_per_group;
+            const int r0 = (m_loc0 + t2) * kMT + 4 * kg;       // the lane's first row in the m-block
+            const int rig0 = mt_in * kMT + 4 * kg;             // ... inside the list group
+            const int crow0 = gidx * a.group_rows + rig0;      // its computed row
+            const bool all_rows = uni((mt_in + 1) * kMT <= a.group_rows &&
+                                      gidx * a.group_rows + (mt_in + 1) * kMT <= a.R ? 1 : 0) != 0;
+            // bias, ReLU and the header check on the accumulators, each only when it applies
+            // (uniform branches: most layers need one of them or none)
+            if (!ok) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+#pragma unroll
+                    for (int nt = 0; nt < 4; ++nt) acc[t2][nt][i] = bad;
+            } else {
+                if (a.bias) {
+                    const float4 bv = *(const float4 *)&s_bias[r0];
+                    const float bvs[4] = {bv.x, bv.y, bv.z, bv.w};
+#pragma unroll
+                    for (int i = 0; i < 4; ++i)
+#pragma unroll
+                        for (int nt = 0; nt < 4; ++nt) acc[t2][nt][i] += bvs[i];
+                }
+                if (a.relu) {
+#pragma unroll
+                    for (int i = 0; i < 4; ++i)
+#pragma unroll
+                        for (int nt = 0; nt < 4; ++nt) acc[t2][nt][i] = acc[t2][nt][i] < 0.f ? 0.f : acc[t2][nt][i];
+                }
+            }
+            const int64_t yrow = ybase + (int64_t)(rig0 < a.group_rows && crow0 < a.R ? crow0 : 0) * a.y_cs;
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                const int rig = mt_in * kMT + 4 * kg + i;   // row inside the list group
-                const int crow = gidx * a.group_rows + rig;
+                const int rig = rig0 + i, crow = crow0 + i;
                 const bool row_ok = rig < a.group_rows && crow < a.R;
-                const int orow = MAP ? omap[t2][i] : crow;
-                const float bv = a.bias ? s_bias[(m_loc0 + t2) * kMT + 4 * kg + i] : 0.f;
+                const uint64_t rmask = all_rows ? ~0ull : ballot(row_ok);
+                int64_t yo = yrow + (int64_t)i * a.y_cs;
+                if constexpr (MAP) yo = ybase + (int64_t)(row_ok ? s_orow[r0 + i] : 0) * a.y_cs;
+                if (!all_rows && !row_ok) yo = ybase;
                 float o[4];
 #pragma unroll
-                for (int nt = 0; nt < 4; ++nt) o[nt] = ok ? epi(acc[t2][nt][i], bv, a.relu) : qnan;
-                const int64_t yo = (int64_t)img * a.y_is + (int64_t)(row_ok ? orow : 0) * a.y_cs + p0;
-                const uint64_t full = ballot(row_ok && nvalid == 4);
-                const uint64_t part = ballot(row_ok && nvalid > 0 && nvalid < 4);
+                for (int nt = 0; nt < 4; ++nt) o[nt] = acc[t2][nt][i];
+                const uint64_t full = full_px & rmask;
                 if (a.out_bf16) {
                     uint16_t *y = (uint16_t *)a.y + yo;
                     uint32_t h[4];
@@ -247,10 +276,10 @@ __global__ __launch_bounds__(kThreads, pw_occ((int)sizeof(E), MODE, TM)) void k_
                         st_mask_b64(y, u32x2{h[0] | (h[1] << 16), h[2] | (h[3] << 16)}, full);
                         ++n;
                     }
-                    if (part) {
+                    if (part_px) {
 #pragma unroll
                         for (int e = 0; e < 3; ++e) {
-                            const uint64_t me = part & ballot(e < nvalid);
+                            const uint64_t me = part_e[e] & rmask;
                             if (me) {
                                 st_mask_b16(y + e, h[e], me);
                                 ++n;
@@ -264,10 +293,10 @@ __global__ __launch_bounds__(kThreads, pw_occ((int)sizeof(E), MODE, TM)) void k_
                                               __float_as_uint(o[3])}, full);
                         ++n;
                     }
-                    if (part) {
+                    if (part_px) {
 #pragma unroll
                         for (int e = 0; e < 3; ++e) {
-                            const uint64_t me = part & ballot(e < nvalid);
+                            const uint64_t me = part_e[e] & rmask;
                             if (me) {
                                 st_mask_b32(y + e, __float_as_uint(o[e]), me);
                                 ++n;
