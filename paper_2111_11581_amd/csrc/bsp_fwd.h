@@ -799,7 +799,6 @@ __global__ __launch_bounds__(kFwdThreads, 1) void k_fwd(ConvArgs a) {
         const int lim = oh == a.Ho - 1 ? a.w_last_out : a.Wo;
         const int nvalid = pix_ok ? max(0, min(4, lim - ow)) : 0;
         const float qnan = __builtin_nanf("");
-        const bool plain = ok && !a.bias && !a.relu;
         // row map (kept filter of each computed row): loaded, and waited for, before the
         // first store, since the kernel counts its outstanding stores by hand
         // (tiles of another plan: no map is read and the rows below stay in range)
@@ -816,29 +815,60 @@ __global__ __launch_bounds__(kFwdThreads, 1) void k_fwd(ConvArgs a) {
                 wait_vm_all();
             }
         }
+        // lane masks of the tile: whole 4-pixel groups, and element e of partial groups
+        const uint64_t full_px = ballot(nvalid == 4);
+        const uint64_t part_px = ballot(nvalid > 0 && nvalid < 4);
+        uint64_t part_e[3];
+#pragma unroll
+        for (int e = 0; e < 3; ++e) part_e[e] = part_px & ballot(e < nvalid);
+        const size_t ybase = (size_t)img * a.Rout * a.y_cs + (size_t)oh * a.Wo + ow;   // row 0 at the lane's pixels
         int n = 0;
 #pragma unroll
         for (int t = 0; t < TM; ++t) {
             const int gm = mt_first + m_loc0 + t;                      // global m-tile
             const int gidx = gm / a.mt_per_group, mt_in = gm - gidx * a.mt_per_group;
+            const int rig0 = mt_in * kMT + 4 * kg;                     // the lane's first row inside the list group
+            const int row0 = gidx * a.group_rows + rig0;
+            const bool all_rows = uni((mt_in + 1) * kMT <= a.group_rows &&
+                                      gidx * a.group_rows + (mt_in + 1) * kMT <= a.R ? 1 : 0) != 0;
+            // bias, ReLU and the header check on the accumulators, each only when it applies
+            if (!ok) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+#pragma unroll
+                    for (int nt = 0; nt < 4; ++nt) acc[t][nt][i] = qnan;
+            } else {
+                if (a.bias) {
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const float bv = s_bias[(m_loc0 + t) * kMT + 4 * kg + i];
+#pragma unroll
+                        for (int nt = 0; nt < 4; ++nt) acc[t][nt][i] += bv;
+                    }
+                }
+                if (a.relu) {
+#pragma unroll
+                    for (int i = 0; i < 4; ++i)
+#pragma unroll
+                        for (int nt = 0; nt < 4; ++nt) acc[t][nt][i] = acc[t][nt][i] < 0.f ? 0.f : acc[t][nt][i];
+                }
+            }
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                const int rig = mt_in * kMT + 4 * kg + i;              // row inside the list group
-                const int row = gidx * a.group_rows + rig;
+                const int rig = rig0 + i, row = row0 + i;
                 const bool row_ok = rig < a.group_rows && row < a.R;
-                const int orow = MAP ? (ok ? min(max(omap[t][i], 0), a.Rout - 1) : min(row, a.Rout - 1)) : row;
-                float o[4];
-                if (plain) {
-#pragma unroll
-                    for (int nt = 0; nt < 4; ++nt) o[nt] = acc[t][nt][i];
+                const uint64_t rmask = all_rows ? ~0ull : ballot(row_ok);
+                size_t yo;
+                if constexpr (MAP) {
+                    const int orow = ok ? min(max(omap[t][i], 0), a.Rout - 1) : min(row, a.Rout - 1);
+                    yo = ybase + (size_t)(row_ok ? orow : 0) * a.y_cs;
                 } else {
-                    const float bv = a.bias ? s_bias[(m_loc0 + t) * kMT + 4 * kg + i] : 0.f;
-#pragma unroll
-                    for (int nt = 0; nt < 4; ++nt) o[nt] = ok ? epi(acc[t][nt][i], bv, a.relu) : qnan;
+                    yo = ybase + (size_t)(row_ok ? row : 0) * a.y_cs;
                 }
-                const size_t yo = ((size_t)img * a.Rout + (row_ok ? orow : 0)) * a.y_cs + (size_t)oh * a.Wo + ow;
-                const uint64_t full = ballot(row_ok && nvalid == 4);
-                const uint64_t part = ballot(row_ok && nvalid > 0 && nvalid < 4);
+                float o[4];
+#pragma unroll
+                for (int nt = 0; nt < 4; ++nt) o[nt] = acc[t][nt][i];
+                const uint64_t full = full_px & rmask;
                 if (a.out_bf16) {
                     uint16_t *y = (uint16_t *)a.y + yo;
                     uint32_t h[4];
@@ -848,10 +878,10 @@ __global__ __launch_bounds__(kFwdThreads, 1) void k_fwd(ConvArgs a) {
                         st_mask_b64(y, u32x2{h[0] | (h[1] << 16), h[2] | (h[3] << 16)}, full);
                         ++n;
                     }
-                    if (part) {
+                    if (part_px) {
 #pragma unroll
                         for (int e = 0; e < 3; ++e) {
-                            const uint64_t me = part & ballot(e < nvalid);
+                            const uint64_t me = part_e[e] & rmask;
                             if (me) {
                                 st_mask_b16(y + e, h[e], me);
                                 ++n;
@@ -865,10 +895,10 @@ __global__ __launch_bounds__(kFwdThreads, 1) void k_fwd(ConvArgs a) {
                                               __float_as_uint(o[3])}, full);
                         ++n;
                     }
-                    if (part) {
+                    if (part_px) {
 #pragma unroll
                         for (int e = 0; e < 3; ++e) {
-                            const uint64_t me = part & ballot(e < nvalid);
+                            const uint64_t me = part_e[e] & rmask;
                             if (me) {
                                 st_mask_b32(y + e, __float_as_uint(o[e]), me);
                                 ++n;
