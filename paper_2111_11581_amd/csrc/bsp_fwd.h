@@ -54,6 +54,14 @@ __device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
     return __builtin_bit_cast(uint16_t, h);
 }
 
+// Two floats rounded to bf16 (RNE, as f32_to_bf16_rne) in one instruction: lo in bits
+// 15..0, hi in bits 31..16.
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t pk_bf16(float lo, float hi) {
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t){lo, hi}, bf16x2_t));
+}
+
 __device__ __forceinline__ void wait_vm_all() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
 __device__ __forceinline__ uint32_t lds_addr(const void *p) {
@@ -871,11 +879,10 @@ __global__ __launch_bounds__(kFwdThreads, 1) void k_fwd(ConvArgs a) {
                 const uint64_t full = full_px & rmask;
                 if (a.out_bf16) {
                     uint16_t *y = (uint16_t *)a.y + yo;
-                    uint32_t h[4];
-#pragma unroll
-                    for (int nt = 0; nt < 4; ++nt) h[nt] = f32_to_bf16_rne(o[nt]);
+                    const uint32_t w01 = pk_bf16(o[0], o[1]), w23 = pk_bf16(o[2], o[3]);
+                    const uint32_t h[3] = {w01 & 0xffffu, w01 >> 16, w23 & 0xffffu};
                     if (full) {
-                        st_mask_b64(y, u32x2{h[0] | (h[1] << 16), h[2] | (h[3] << 16)}, full);
+                        st_mask_b64(y, u32x2{w01, w23}, full);
                         ++n;
                     }
                     if (part_px) {

@@ -269,11 +269,10 @@ __global__ __launch_bounds__(kThreads, pw_occ((int)sizeof(E), MODE, TM)) void k_
                 const uint64_t full = full_px & rmask;
                 if (a.out_bf16) {
                     uint16_t *y = (uint16_t *)a.y + yo;
-                    uint32_t h[4];
-#pragma unroll
-                    for (int nt = 0; nt < 4; ++nt) h[nt] = f32_to_bf16_rne(o[nt]);
+                    const uint32_t w01 = pk_bf16(o[0], o[1]), w23 = pk_bf16(o[2], o[3]);
+                    const uint32_t h[3] = {w01 & 0xffffu, w01 >> 16, w23 & 0xffffu};
                     if (full) {
-                        st_mask_b64(y, u32x2{h[0] | (h[1] << 16), h[2] | (h[3] << 16)}, full);
+                        st_mask_b64(y, u32x2{w01, w23}, full);
                         ++n;
                     }
                     if (part_px) {
