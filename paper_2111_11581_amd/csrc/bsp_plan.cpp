@@ -288,6 +288,9 @@ static bool plan_pl(Plan *p, int n_mt, int astep) {
                     const double epi = TM * 4 * 60.0 + out_bytes / 10.0;
                     double cyc = rounds * (tpw * (ns * stage + epi) + a_res / 1024.0 * 25.0) + 5000.0;
                     if ((nb - 1) * ncp > 63) cyc *= 1.05;   // more copies in flight than a wave can count
+                    // at equal cost three buffers measure best (two stages in flight, one barrier
+                    // per stage), more than three slightly worse
+                    cyc *= 1.0 + 0.01 * std::abs(nb - 3);
                     cyc = std::max(cyc, t_hbm);
                     if (cyc < best * (1 - 1e-9)) {
                         best = cyc;
