@@ -132,6 +132,13 @@ bsp_status bsp_conv2d(const bsp_scheme *scheme, const bsp_conv_shape *shape, bsp
         (int64_t)shape->n * p.R * p.Ho * p.Wo > INT32_MAX || (int64_t)shape->n * p.Ho > INT32_MAX / 2)
         return BSP_EUNSUPPORTED;
     if (shape->n == 0) return BSP_OK;
+    if (p.im2col) {
+        if ((int64_t)shape->n * p.Cin * p.H * p.W > INT32_MAX) return BSP_EUNSUPPORTED;
+        return launch_conv_im2col(p, *shape, x, (const uint8_t *)dev_tiles, bias, relu ? 1 : 0,
+                                  out_dt == BSP_BF16, y, S(stream)) == hipSuccess
+                   ? BSP_OK
+                   : BSP_EDEVICE;
+    }
     return launch_conv(p, shape->n, x, (const uint8_t *)dev_tiles, bias, relu ? 1 : 0,
                        out_dt == BSP_BF16, y, S(stream)) == hipSuccess
                ? BSP_OK

@@ -1,6 +1,8 @@
 // Launcher of the forward kernel: argument set-up and instantiation choice.  The
 // kernel template lives in bsp_fwd.h; its instantiations are compiled in
 // bsp_fwd_*.hip (one translation unit per element type and gather mode).
+#include <mutex>
+
 #include "bsp_pl.h"
 #include "bsp_pw.h"
 
@@ -309,6 +311,71 @@ hipError_t launch_conv(const Plan &p, int n, const void *x, const uint8_t *tiles
     // images of the output: conv NCHW planes of Ho * Wo; linear one [R][n] matrix
     return launch_fill_pruned(p, a.N, p.is_linear ? n : a.y_cs, (int64_t)p.R * a.y_cs, a.y_cs, tiles, bias,
                               relu, out_bf16, y, st);
+}
+
+// im2col of a conv for its 1x1 plan: ws[img][k][p], k = (c * kh + r) * kw + s (the GEMM
+// form's column), p = oh * wo + ow; taps outside the image are zero.  One thread per
+// element of the expanded input (fewer than 2^31).
+template <typename E>
+__global__ void k_im2col(const E *__restrict__ x, E *__restrict__ ws, int total, int cols, int cin, int h, int w,
+                         int kh, int kw, int sh, int sw, int ph, int pw, int ho, int wo) {
+    const int plane = ho * wo, khw = kh * kw;
+    for (int idx = blockIdx.x * blockDim.x + threadIdx.x; idx < total; idx += gridDim.x * blockDim.x) {
+        const int pix = idx % plane, k = (idx / plane) % cols, img = idx / (plane * cols);
+        const int c = k / khw, rs = k - c * khw, r = rs / kw, s = rs - r * kw;
+        const int oh = pix / wo, ow = pix - oh * wo;
+        const int ih = oh * sh - ph + r, iw = ow * sw - pw + s;
+        ws[idx] = (ih >= 0 && ih < h && iw >= 0 && iw < w) ? x[(((int64_t)img * cin + c) * h + ih) * w + iw] : (E)0;
+    }
+}
+
+// One workspace per device, grown on demand and kept until the process ends.  Layers on
+// the im2col path share it, so such calls that overlap on one device (other streams) race.
+static hipError_t workspace(size_t bytes, void **out) {
+    static std::mutex mu;
+    static void *buf[64] = {};
+    static size_t size[64] = {};
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(mu);
+    if (size[dev] < bytes) {
+        if (buf[dev]) {
+            e = hipFree(buf[dev]);
+            buf[dev] = nullptr;
+            size[dev] = 0;
+            if (e != hipSuccess) return e;
+        }
+        e = hipMalloc(&buf[dev], bytes);
+        if (e != hipSuccess) {
+            buf[dev] = nullptr;
+            return e;
+        }
+        size[dev] = bytes;
+    }
+    *out = buf[dev];
+    return hipSuccess;
+}
+
+hipError_t launch_conv_im2col(const Plan &p, const bsp_conv_shape &c, const void *x, const uint8_t *tiles,
+                              const float *bias, int relu, int out_bf16, void *y, hipStream_t st) {
+    const int64_t total = (int64_t)c.n * p.Cin * p.H * p.W;   // the 1x1 plan: Cin = cin kh kw, H x W = Ho x Wo
+    if (total <= 0) return hipSuccess;
+    if (total > INT32_MAX) return hipErrorInvalidValue;
+    void *ws = nullptr;
+    hipError_t e = workspace((size_t)total * p.esize, &ws);
+    if (e != hipSuccess) return e;
+    const int grid = (int)std::min<int64_t>((total + 255) / 256, 16384);
+    if (p.esize == 2)
+        k_im2col<uint16_t><<<grid, 256, 0, st>>>((const uint16_t *)x, (uint16_t *)ws, (int)total, p.Cin, c.cin, c.h,
+                                                 c.w, c.kh, c.kw, c.stride_h, c.stride_w, c.pad_h, c.pad_w, p.H, p.W);
+    else
+        k_im2col<float><<<grid, 256, 0, st>>>((const float *)x, (float *)ws, (int)total, p.Cin, c.cin, c.h, c.w,
+                                              c.kh, c.kw, c.stride_h, c.stride_w, c.pad_h, c.pad_w, p.H, p.W);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    return launch_conv(p, c.n, ws, tiles, bias, relu, out_bf16, y, st);
 }
 
 }  // namespace bsp

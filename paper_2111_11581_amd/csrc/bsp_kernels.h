@@ -34,4 +34,9 @@ hipError_t launch_conv(const Plan &p, int n, const void *x, const uint8_t *tiles
 hipError_t launch_maxpool2x2(int dt, int n, int c, int h, int w, const void *x, void *y,
                              hipStream_t st);
 
+// A conv whose plan is a 1x1 layer over its im2col input (Plan::im2col): the input is
+// expanded into the library's per-device workspace, then the pointwise kernel runs.
+hipError_t launch_conv_im2col(const Plan &p, const bsp_conv_shape &c, const void *x, const uint8_t *tiles,
+                              const float *bias, int relu, int out_bf16, void *y, hipStream_t st);
+
 }  // namespace bsp

@@ -577,8 +577,35 @@ static double search_tiling(Plan *p, int span_req, double step_ch, int n_mt, int
     return best;
 }
 
+static bsp_status make_plan_impl(const bsp_scheme *s, const bsp_conv_shape *conv, bsp_dtype wdt,
+                                 int batch_for_linear, Plan *p, bool im2col_inner);
+
+// Output planes of at most this many pixels: the general kernel stages whole input rows
+// per output row, which for 2x2 and 4x4 planes copies mostly padding, so such layers run
+// as a 1x1 layer over their im2col input (its columns are the GEMM form's columns).
+constexpr int kIm2colMaxPixels = 16;
+
 bsp_status make_plan(const bsp_scheme *s, const bsp_conv_shape *conv, bsp_dtype wdt,
                      int batch_for_linear, Plan *p) {
+    if (s && conv && conv->kh > 0 && conv->kw > 0 && (conv->kh > 1 || conv->kw > 1) && conv->stride_h > 0 &&
+        conv->stride_w > 0 && conv->pad_h >= 0 && conv->pad_w >= 0 && conv->cin > 0 &&
+        conv->h + 2 * conv->pad_h >= conv->kh && conv->w + 2 * conv->pad_w >= conv->kw) {
+        const int ho = (conv->h + 2 * conv->pad_h - conv->kh) / conv->stride_h + 1;
+        const int wo = (conv->w + 2 * conv->pad_w - conv->kw) / conv->stride_w + 1;
+        if ((int64_t)ho * wo <= kIm2colMaxPixels) {
+            if ((int64_t)conv->cin * conv->kh * conv->kw != s->cols) return BSP_EINVAL;
+            if (s->regularity == BSP_PUNCHED && conv->kh * conv->kw != s->khw) return BSP_EINVAL;
+            const bsp_conv_shape c2 = {conv->n, conv->cin * conv->kh * conv->kw, ho, wo, 1, 1, 1, 1, 0, 0};
+            const bsp_status st = make_plan_impl(s, &c2, wdt, batch_for_linear, p, true);
+            if (st == BSP_OK) p->im2col = 1;
+            return st;
+        }
+    }
+    return make_plan_impl(s, conv, wdt, batch_for_linear, p, false);
+}
+
+static bsp_status make_plan_impl(const bsp_scheme *s, const bsp_conv_shape *conv, bsp_dtype wdt,
+                                 int batch_for_linear, Plan *p, bool im2col_inner) {
     if (!s || !p) return BSP_EINVAL;
     std::memset(p, 0, sizeof(*p));
     if (s->rows <= 0 || s->cols <= 0 || s->bh < 0 || s->bw < 0 || s->rate < 1) return BSP_EINVAL;
@@ -711,7 +738,7 @@ bsp_status make_plan(const bsp_scheme *s, const bsp_conv_shape *conv, bsp_dtype 
             c.stride_w <= 0 || c.pad_h < 0 || c.pad_w < 0)
             return BSP_EINVAL;
         if ((int64_t)c.cin * c.kh * c.kw != p->C) return BSP_EINVAL;
-        if (p->reg == BSP_PUNCHED && c.kh * c.kw != p->khw) return BSP_EINVAL;
+        if (p->reg == BSP_PUNCHED && c.kh * c.kw != p->khw && !im2col_inner) return BSP_EINVAL;
         p->is_linear = 0;
         p->Cin = c.cin; p->H = c.h; p->W = c.w; p->KH = c.kh; p->KW = c.kw;
         p->SH = c.stride_h; p->SW = c.stride_w; p->PH = c.pad_h; p->PW = c.pad_w;

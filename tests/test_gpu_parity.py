@@ -186,6 +186,16 @@ CONV_CASES = [
     _conv_case("3x3 rowcol 16x32 r2 bias relu", 2, 64, 12, 12, 64, 3, 1, 1, 16, 32, ROWCOL, 2, relu=True, bias=True),
     _conv_case("1x1 rowcol 32x32 r2 s2", 2, 64, 14, 14, 96, 1, 2, 0, 32, 32, ROWCOL, 2),
     _conv_case("f32 3x3 rowcol 8x8 r2", 1, 16, 10, 10, 32, 3, 1, 1, 8, 8, ROWCOL, 2, dtype="f32", out="f32"),
+    # output planes of at most 16 pixels run as a 1x1 layer over the im2col input
+    _conv_case("im2col 3x3 col8x16 r8 2x2", 5, 64, 2, 2, 64, 3, 1, 1, 8, 16, COL, 8),
+    _conv_case("im2col 3x3 col16x32 r4 4x4 relu bias", 3, 96, 4, 4, 80, 3, 1, 1, 16, 32, COL, 4, relu=True,
+               bias=True),
+    _conv_case("im2col 3x3 s2 8x8 row whole r4 bias", 2, 32, 8, 8, 40, 3, 2, 1, 0, 0, ROW, 4, bias=True),
+    _conv_case("im2col 3x3 punched 16x8 r3 4x4", 2, 32, 4, 4, 48, 3, 1, 1, 16, 8, PUNCHED, 3),
+    _conv_case("im2col f32 3x3 col16x16 r2 4x4", 2, 16, 4, 4, 32, 3, 1, 1, 16, 16, COL, 2, dtype="f32", out="f32"),
+    _conv_case("im2col 5x5 pad0 dense 6x6", 3, 12, 6, 6, 24, 5, 1, 0, 0, 0, DENSE, 1),
+    _conv_case("im2col 3x3 pad0 unstructured 4x5", 4, 24, 4, 5, 40, 3, 1, 0, 1, 1, UNSTRUCTURED, 4),
+    _conv_case("im2col 3x3 row32x32 r2 3x3 ragged", 7, 40, 3, 3, 72, 3, 1, 1, 32, 32, ROW, 2),
 ]
 
 
