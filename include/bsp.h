@@ -202,7 +202,13 @@ bsp_status bsp_to_bcs(const bsp_scheme *scheme, const int32_t *indices, const in
  * y: NCHW [n][rows][Ho][Wo] of out_dt (fp32 accumulation, RNE to bf16).
  * Only kept weights are multiplied; inputs must be finite (a removed weight
  * is never multiplied, so Inf/NaN inputs do not propagate through it).
- * bias may be NULL.  Async. */
+ * bias may be NULL.  Async.
+ * Layers whose output plane has at most 16 pixels (Ho * Wo <= 16, kernel
+ * larger than 1x1) expand x into a workspace (n x cin*kh*kw x Ho x Wo of
+ * in_dt) that the library allocates on the device at the first call that
+ * needs it (or a larger one) and keeps until the process ends; such calls
+ * must not overlap on one device (they share the workspace), and the first
+ * one cannot be captured into a graph. */
 bsp_status bsp_conv2d(const bsp_scheme *scheme, const bsp_conv_shape *shape, bsp_dtype in_dt,
                       bsp_dtype out_dt, const void *x, const void *dev_tiles,
                       const float *bias_or_null, int32_t relu, void *y, void *stream);
