@@ -23,7 +23,7 @@ OUT = os.path.join(PKG, "_build")
 LIB = os.path.join(OUT, "libbsp.so")
 ARCH = "gfx950"
 
-SOURCES = ["bsp_pl_1.hip", "bsp_pl_2.hip", "bsp_pw_b1.hip", "bsp_pw_b2.hip", "bsp_pw_f.hip", "bsp_fwd_b1_k1.hip", "bsp_fwd_b1_k24.hip", "bsp_fwd_b2.hip", "bsp_fwd_b3.hip", "bsp_fwd_b0.hip",
+SOURCES = ["bsp_pl_1.hip", "bsp_pl_2.hip", "bsp_pl_g.hip", "bsp_pw_b1.hip", "bsp_pw_b2.hip", "bsp_pw_f.hip", "bsp_fwd_b1_k1.hip", "bsp_fwd_b1_k24.hip", "bsp_fwd_b2.hip", "bsp_fwd_b3.hip", "bsp_fwd_b0.hip",
            "bsp_fwd_f.hip", "bsp_plan.cpp", "bsp_api.cpp", "bsp_prune.hip", "bsp_pack.hip",
            "bsp_conv.hip", "bsp_glue.hip"]
 

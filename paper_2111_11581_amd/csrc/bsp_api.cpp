@@ -133,7 +133,8 @@ bsp_status bsp_conv2d(const bsp_scheme *scheme, const bsp_conv_shape *shape, bsp
         return BSP_EUNSUPPORTED;
     if (shape->n == 0) return BSP_OK;
     if (p.im2col) {
-        if ((int64_t)shape->n * p.Cin * p.H * p.W > INT32_MAX) return BSP_EUNSUPPORTED;
+        if ((int64_t)shape->n * p.Cin * (p.xplane ? p.xplane : (int64_t)p.H * p.W) > INT32_MAX)
+            return BSP_EUNSUPPORTED;
         return launch_conv_im2col(p, *shape, x, (const uint8_t *)dev_tiles, bias, relu ? 1 : 0,
                                   out_dt == BSP_BF16, y, S(stream)) == hipSuccess
                    ? BSP_OK

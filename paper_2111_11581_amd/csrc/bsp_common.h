@@ -128,8 +128,10 @@ struct Plan {
     int shared;                   // 1 = identity list shared by all m-tiles
     int n_groups, group_rows, mt_per_group;
     int RK;                       // rows the kernels compute (R, or the kept filters with a row map)
-    int im2col;                   // 1: a conv with a tiny output plane, planned as a 1x1 layer over
-                                  // its im2col input (channels cin * kh * kw, image Ho x Wo)
+    int im2col;                   // 1: a conv planned as a 1x1 layer over its im2col input
+                                  // (channels cin * kh * kw, image Ho x Wo)
+    int xplane;                   // input plane stride (elements) of a stride-1 pointwise plan
+                                  // when not H * W: im2col planes padded to whole granules
     int rowmap;                   // 1: row pruning with whole-width blocks (filter pruning): the
                                   // kernels compute the kept rows only, the epilogue writes row
                                   // rowmap[i] of the output, a fill writes the pruned rows

@@ -11,6 +11,7 @@ namespace pl {
 
 pl_fn pick_1(int NSUB, int TM, bool map);
 pl_fn pick_2(int NSUB, int TM, bool map);
+pl_fn pick_g(int NSUB, int TM, int G);
 
 }  // namespace pl
 namespace pw {
@@ -163,7 +164,7 @@ static hipError_t launch_pw(const Plan &p, int n, const void *x, const uint8_t *
     } else if (p.SW == 1) {
         images = n;
         a.Ho = 1; a.Wo = p.H * p.W; a.in_row = 0;
-        a.x_cs = (int64_t)p.H * p.W; a.y_cs = a.x_cs;
+        a.x_cs = p.xplane ? p.xplane : (int64_t)p.H * p.W; a.y_cs = (int64_t)p.H * p.W;
         a.x_is = (int64_t)p.Cin * a.x_cs; a.y_is = (int64_t)p.R * a.y_cs;
     } else {
         images = n;
@@ -208,7 +209,9 @@ static hipError_t launch_pw(const Plan &p, int n, const void *x, const uint8_t *
     const bool map = p.rowmap != 0;
     int threads = kThreads;
     if (p.pl) {
-        fn = p.dt == BSP_BF16 ? (p.SW == 1 ? pl::pick_1(p.NSUB, p.TM, map) : pl::pick_2(p.NSUB, p.TM, map)) : nullptr;
+        if (p.dt == BSP_BF16)
+            fn = !p.shared ? (p.SW == 1 ? pl::pick_g(p.NSUB, p.TM, p.MBG) : nullptr)
+                           : (p.SW == 1 ? pl::pick_1(p.NSUB, p.TM, map) : pl::pick_2(p.NSUB, p.TM, map));
         threads = pl::kPlThreads;
     } else if (p.dt == BSP_F32) {
         fn = p.SW == 1 ? pw::pick_f(p.TM, p.TPG, p.KS, map) : nullptr;
@@ -329,6 +332,42 @@ __global__ void k_im2col(const E *__restrict__ x, E *__restrict__ ws, int total,
     }
 }
 
+// As k_im2col for planes padded to whole 16-byte granules (xplane elements, a multiple
+// of GE = 16 / sizeof(E)): one thread per granule of a row (img, k) of the expanded
+// input (fewer than 2^31 granules), GE loads and one 16-byte store; padding elements
+// are zero.  Divisions by the layer's sizes are multiply-shifts.
+struct Im2colArgs {
+    uint32_t n_gran;              // granules of the expanded input
+    int cin, h, w, kh, kw, sh, sw, ph, pw, ho, wo, xplane;
+    FastDiv div_gpr, div_cols, div_khw, div_kw, div_wo;
+};
+
+template <typename E>
+__global__ void k_im2col_g(const E *__restrict__ x, E *__restrict__ ws, Im2colArgs a) {
+    constexpr int GE = 16 / sizeof(E);
+    const int plane = a.ho * a.wo, gpr = a.xplane / GE;
+    for (uint32_t idx = blockIdx.x * blockDim.x + threadIdx.x; idx < a.n_gran; idx += gridDim.x * blockDim.x) {
+        const uint32_t row = fdiv(idx, a.div_gpr);
+        const int g = (int)(idx - row * (uint32_t)gpr);
+        const uint32_t img = fdiv(row, a.div_cols);
+        const int k = (int)(row - img * a.div_cols.d);
+        const int c = (int)fdiv((uint32_t)k, a.div_khw), rs = k - c * a.kh * a.kw;
+        const int r = (int)fdiv((uint32_t)rs, a.div_kw), s = rs - r * a.kw;
+        const E *xc = x + ((int64_t)img * a.cin + c) * a.h * a.w;
+        int pix = g * GE;
+        int oh = (int)fdiv((uint32_t)pix, a.div_wo), ow = pix - oh * a.wo;
+        E v[GE];
+#pragma unroll
+        for (int e = 0; e < GE; ++e) {
+            const int ih = oh * a.sh - a.ph + r, iw = ow * a.sw - a.pw + s;
+            v[e] = (pix < plane && ih >= 0 && ih < a.h && iw >= 0 && iw < a.w) ? xc[ih * a.w + iw] : (E)0;
+            ++pix;
+            if (++ow == a.wo) { ow = 0; ++oh; }
+        }
+        *(uint4 *)(ws + (int64_t)row * a.xplane + g * GE) = *(const uint4 *)v;
+    }
+}
+
 // One workspace per device, grown on demand and kept until the process ends.  Layers on
 // the im2col path share it, so such calls that overlap on one device (other streams) race.
 static hipError_t workspace(size_t bytes, void **out) {
@@ -360,12 +399,34 @@ static hipError_t workspace(size_t bytes, void **out) {
 
 hipError_t launch_conv_im2col(const Plan &p, const bsp_conv_shape &c, const void *x, const uint8_t *tiles,
                               const float *bias, int relu, int out_bf16, void *y, hipStream_t st) {
-    const int64_t total = (int64_t)c.n * p.Cin * p.H * p.W;   // the 1x1 plan: Cin = cin kh kw, H x W = Ho x Wo
+    // the 1x1 plan: Cin = cin kh kw, H x W = Ho x Wo, planes of xplane elements when padded
+    const int64_t plane = p.xplane ? p.xplane : (int64_t)p.H * p.W;
+    const int64_t total = (int64_t)c.n * p.Cin * plane;
     if (total <= 0) return hipSuccess;
     if (total > INT32_MAX) return hipErrorInvalidValue;
     void *ws = nullptr;
     hipError_t e = workspace((size_t)total * p.esize, &ws);
     if (e != hipSuccess) return e;
+    if (p.xplane) {
+        Im2colArgs ia;
+        ia.n_gran = (uint32_t)(total / (16 / p.esize));
+        ia.cin = c.cin; ia.h = c.h; ia.w = c.w; ia.kh = c.kh; ia.kw = c.kw;
+        ia.sh = c.stride_h; ia.sw = c.stride_w; ia.ph = c.pad_h; ia.pw = c.pad_w;
+        ia.ho = p.H; ia.wo = p.W; ia.xplane = p.xplane;
+        ia.div_gpr = make_fastdiv((uint32_t)(p.xplane / (16 / p.esize)));
+        ia.div_cols = make_fastdiv((uint32_t)p.Cin);
+        ia.div_khw = make_fastdiv((uint32_t)(c.kh * c.kw));
+        ia.div_kw = make_fastdiv((uint32_t)c.kw);
+        ia.div_wo = make_fastdiv((uint32_t)p.W);
+        const int grid = (int)std::min<int64_t>(((int64_t)ia.n_gran + 255) / 256, 65536);
+        if (p.esize == 2)
+            k_im2col_g<uint16_t><<<grid, 256, 0, st>>>((const uint16_t *)x, (uint16_t *)ws, ia);
+        else
+            k_im2col_g<float><<<grid, 256, 0, st>>>((const float *)x, (float *)ws, ia);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        return launch_conv(p, c.n, ws, tiles, bias, relu, out_bf16, y, st);
+    }
     const int grid = (int)std::min<int64_t>((total + 255) / 256, 16384);
     if (p.esize == 2)
         k_im2col<uint16_t><<<grid, 256, 0, st>>>((const uint16_t *)x, (uint16_t *)ws, (int)total, p.Cin, c.cin, c.h,

@@ -440,6 +440,20 @@ __global__ void k_desc16(const int32_t *__restrict__ desc, const int4 *__restric
     }
 }
 
+// 16-bit channels of the pointwise kernel's gathered lists (the lists' channel
+// numbers themselves; no chunks).
+__global__ void k_desc16_abs(const int32_t *__restrict__ desc, int n, uint16_t *__restrict__ desc16, int *flag) {
+    for (int e = blockIdx.x * blockDim.x + threadIdx.x; e < n; e += gridDim.x * blockDim.x) {
+        const int v = desc[e];
+        if (v < 0 || v > 0xffff) {
+            atomicOr(flag, 2);
+            desc16[e] = 0;
+        } else {
+            desc16[e] = (uint16_t)v;
+        }
+    }
+}
+
 template <typename E>
 __global__ void k_fill(E *p, size_t n, E v) {
     for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n;
@@ -638,13 +652,20 @@ bsp_status pack_t(const Plan &p, const E *w, const uint8_t *mask, E *values, int
         k_fill<int32_t><<<grid_for(nrm), 256, 0, st>>>(rm, nrm, 0);
         k_rowmap<<<grid_for(p.R), 256, 0, st>>>(indices, p.RK, p.R, rm, (int32_t *)(tiles + p.off_pruned));
     }
-    int4 *table = (int4 *)(tiles + p.off_chunks);
-    k_step_spans<<<grid_for(p.S), 256, 0, st>>>(desc, p.n_groups, p.LP, p.S, p.CH_STRIDE, table);
-    k_build_chunks<<<1, 256, sizeof(int) * 2 * p.S, st>>>(
-        table, p.S, p.CC, p.SMAX, (int *)(tiles + offsetof(TileHeader, n_chunks)), flag);
-    k_desc16<<<grid_for((size_t)p.n_groups * p.LP), 256, 0, st>>>(
-        desc, table, (const int *)(tiles + offsetof(TileHeader, n_chunks)), p.n_groups, p.LP,
-        p.CH_STRIDE, (uint16_t *)(tiles + p.off_desc16), flag);
+    if (p.pl && !p.shared) {
+        // the pointwise kernel with gathered lists reads the channels of the lists (its
+        // plan's channel stride is 1) and no chunk table
+        k_desc16_abs<<<grid_for((size_t)p.n_groups * p.LP), 256, 0, st>>>(
+            desc, p.n_groups * p.LP, (uint16_t *)(tiles + p.off_desc16), flag);
+    } else {
+        int4 *table = (int4 *)(tiles + p.off_chunks);
+        k_step_spans<<<grid_for(p.S), 256, 0, st>>>(desc, p.n_groups, p.LP, p.S, p.CH_STRIDE, table);
+        k_build_chunks<<<1, 256, sizeof(int) * 2 * p.S, st>>>(
+            table, p.S, p.CC, p.SMAX, (int *)(tiles + offsetof(TileHeader, n_chunks)), flag);
+        k_desc16<<<grid_for((size_t)p.n_groups * p.LP), 256, 0, st>>>(
+            desc, table, (const int *)(tiles + offsetof(TileHeader, n_chunks)), p.n_groups, p.LP,
+            p.CH_STRIDE, (uint16_t *)(tiles + p.off_desc16), flag);
+    }
     if (p.n_g_pad > p.n_groups) {
         // offsets of the padding groups of the last m-block: 0 (a valid patch position)
         const size_t nd = (size_t)(p.n_g_pad - p.n_groups) * p.LP;

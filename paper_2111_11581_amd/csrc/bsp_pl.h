@@ -1,25 +1,32 @@
-// Forward kernel of pointwise layers whose kept columns are one identity list (row
-// blocks stored with zeros for their removed rows, dense and unstructured layers):
-// 1x1 convolutions without padding at stride 1 or 2, and fully connected layers
-// (Sec. 4.2: the GEMM form of a 1x1 layer has one column per input channel).
-// Template; instantiated in bsp_pl_*.hip.
+// Forward kernel of pointwise layers (1x1 convolutions without padding at stride 1 or
+// 2, fully connected layers, and convolutions run over their im2col input; Sec. 4.2:
+// the GEMM form of a 1x1 layer has one column per input channel).  Template;
+// instantiated in bsp_pl_*.hip.
 //
-// With an identity list every 32-wide step of the K loop is 32 consecutive input
-// channels, so the loop needs no chunk table and no gather offsets: a step's operands
-// sit at fixed LDS offsets.  A workgroup has 8 waves and owns one m-block (MB rows)
+// Two kinds of K loop:
+//  * identity list (G = 0: row blocks stored with zeros for their removed rows, dense
+//    and unstructured layers): every 32-wide step is 32 consecutive input channels;
+//  * gathered lists (G >= 1: column and block-punched blocks): the m-block holds G list
+//    groups (block-rows) and step s of group g is the 32 channels of entries 32 s ..
+//    32 s + 31 of g's list of kept columns (Sec. 4.1.1), each channel a row of the
+//    input; the lists of the m-block sit in LDS for the whole run and every step
+//    stages one patch per group.
+// Either way a step's operands sit at fixed LDS offsets, so the multiplying waves
+// need no gather offsets.  A workgroup has 8 waves and owns one m-block (MB rows)
 // and a run of pixel tiles (NP = 64 NSUB output pixels each):
 //  * waves 4-7 copy: per stage (SPS steps) each issues the same number of 16-byte
 //    direct-to-LDS copies: for every step, its share of the stage's input granules
-//    (32 channels x NP pixels) and, unless the m-block's weights stay in LDS for the
-//    whole run (copied once at the start), of its weight tiles (MB / 64 tiles of 1 KB);
-//    the sources are set up once per tile and advance by 32 channels per step.  Copies
-//    run NB - 1 stages ahead, so every wait is for a constant count;
+//    (G x 32 channels x NP pixels) and, unless the m-block's weights stay in LDS for
+//    the whole run (copied once at the start), of its weight tiles (MB / 64 tiles of
+//    1 KB); the sources are set up once per tile.  Copies run NB - 1 stages ahead, so
+//    every wait is for a constant count;
 //  * waves 0-3 multiply: wave w works on sub-tile w % NSUB and m-tiles
-//    (w / NSUB) * TM .. + TM - 1; per step it reads its weights (one 16-byte LDS read
-//    per m-tile) and the 8 channels x 4 pixels of its lane (8-byte reads, 16-byte at
-//    stride 2) at compile-time offsets, re-packs them with v_perm into the B operands
-//    of 4 MFMA 16x16x32 bf16 and multiplies; steps of a stage are software-pipelined.
-//    At the end of a tile they add bias, apply ReLU, round to bf16 and store.
+//    (w / NSUB) * TM .. + TM - 1 (one list group); per step it reads its weights (one
+//    16-byte LDS read per m-tile) and the 8 channels x 4 pixels of its lane of its
+//    group's patch (8-byte reads, 16-byte at stride 2) at compile-time offsets,
+//    re-packs them with v_perm into the B operands of 4 MFMA 16x16x32 bf16 and
+//    multiplies; steps of a stage are software-pipelined.  At the end of a tile they
+//    add bias, apply ReLU, round to bf16 and store.
 // One barrier per stage; the stores of a finished tile overlap the next tile.
 #pragma once
 
@@ -34,7 +41,10 @@ constexpr int kPlThreads = 512;
 
 // MODE 1: stride 1, a granule holds two 4-pixel groups; MODE 2: stride 2, a granule
 // holds the 8 input pixels of one group (the even ones are used).
-template <int MODE, int NSUB, int TM, bool MAP = false>
+// G: list groups of an m-block (0: the identity list).  With G > 1 the m-block's MT
+// m-tiles are G whole groups of MT / G m-tiles; with G = 1 the m-block lies inside one
+// group.  A wave's TM m-tiles always lie in one group.
+template <int MODE, int NSUB, int TM, bool MAP = false, int G = 0>
 __global__ __launch_bounds__(kPlThreads, 1) void k_pl(PwArgs a) {
     typedef Gat<uint16_t, MODE> GT;
     constexpr int Q = kWaves / NSUB;              // multiplying waves per sub-tile
@@ -42,10 +52,14 @@ __global__ __launch_bounds__(kPlThreads, 1) void k_pl(PwArgs a) {
     constexpr int NP = 64 * NSUB;                 // output pixels of a tile
     constexpr int RB = NP * 2 * MODE;             // patch bytes per channel
     constexpr int GPC = RB / 16;                  // granules per channel
-    constexpr int PCOPY = 32 * GPC / kThreads;    // patch copies per producer wave and step
+    constexpr int GG = G == 0 ? 1 : G;            // patches per step
+    constexpr int PCOPY = GG * 32 * GPC / kThreads;   // patch copies per producer wave and step
     constexpr int WCOPY = MT / kWaves;            // weight copies per producer wave and step
     static_assert(32 * GPC % kThreads == 0 && MT % kWaves == 0, "whole copies per wave");
-    constexpr int PB = 32 * RB;                   // LDS bytes of one step's patch
+    static_assert(G <= 1 || (MT % G == 0 && (MT / G) % TM == 0), "a wave's m-tiles lie in one group");
+    static_assert(!MAP || G == 0, "row maps come with the identity list");
+    constexpr int PB1 = 32 * RB;                  // LDS bytes of one group's patch of a step
+    constexpr int PB = GG * PB1;                  // LDS bytes of one step's patches
     extern __shared__ __attribute__((aligned(256))) unsigned char lds[];
     __shared__ __attribute__((aligned(16))) float s_bias[kMaxMBRows];
     __shared__ int s_orow[MAP ? kMaxMBRows : 1];
@@ -82,18 +96,24 @@ __global__ __launch_bounds__(kPlThreads, 1) void k_pl(PwArgs a) {
     const bool res = a.resident;          // the m-block's weights stay in LDS ([m-tile][step], 1 KB each)
     const int wcopy = res ? 0 : WCOPY;
     const int stage_b = SPS * PB + (res ? 0 : SPS * MT * 1024);   // patches of the stage, then its weights
-    unsigned char *bufs = lds + (res ? MT * S * 1024 : 0);
-    const uint32_t lds0 = lds_addr(lds);
+    unsigned char *const lds_w = lds + (G > 0 ? a.lds_d : 0);   // resident weights
+    unsigned char *bufs = lds_w + (res ? MT * S * 1024 : 0);
+    const uint32_t ldsw0 = lds_addr(lds_w);
     const uint32_t bufs0 = lds_addr(bufs);
     const int n_items = (t_end - t_begin) * (ok ? NS : 1);
+    // gathered lists: the m-block's G lists (16-bit channels, LP entries each) at LDS
+    // byte 0, before the weights and the buffers
+    const uint16_t *s_list = (const uint16_t *)lds;
 
     // ---- producers: copy k of a step fills LDS granules gid = (rw * PCOPY + k) * 64 + lane
-    // of the step's patch (byte 16 gid): channel c = gid / GPC, granule g = gid % GPC of
-    // the tile row; a wave's copies are 1 KB apart, so four share one M0 ----
+    // of the step's patches (byte 16 gid): list group lg = gid / (32 GPC), channel
+    // c = gid / GPC % 32 of the step, granule g = gid % GPC of the tile row; a wave's
+    // copies are 1 KB apart, so four share one M0 ----
     const int xcs = (int)a.x_cs;
     const uint32_t x_last = (uint32_t)(a.x_total - 8);   // last granule start inside x
-    int e_base[PCOPY];     // element offset of the copy's granule at its channel (channel 0 of the step)
-    int c_of[PCOPY];       // its channel within a step
+    int e_base[PCOPY];     // element offset of the copy's granule: at channel 0 of the step
+                           // (identity list), at channel 0 of x (gathered lists)
+    int c_of[PCOPY];       // its channel within a step (identity list), its list entry at step 0
     bool g_live[PCOPY];    // the granule holds output pixels
     int cur_tile = -1;
     // fast path: sources as a scalar base plus a 32-bit per-lane byte offset
@@ -108,7 +128,7 @@ __global__ __launch_bounds__(kPlThreads, 1) void k_pl(PwArgs a) {
 #pragma unroll
         for (int k = 0; k < PCOPY; ++k) {
             const int gid = (rw * PCOPY + k) * 64 + lane;
-            const int c = gid / GPC, g = gid % GPC;
+            const int c = gid / GPC % 32, g = gid % GPC;
             const int64_t Gg = (int64_t)t * (kGroups * NSUB) + (int64_t)g * a.gpg;
             g_live[k] = Gg < a.n_groups_total;
             int64_t off = 0;
@@ -117,10 +137,11 @@ __global__ __launch_bounds__(kPlThreads, 1) void k_pl(PwArgs a) {
                 const int gi = (int)Gg - row * a.GPR;
                 const int img = (int)fdiv((uint32_t)row, a.div_Ho);
                 const int oh = row - img * a.Ho;
-                off = (int64_t)img * a.x_is + (int64_t)oh * a.in_row + gi * 4 * a.SW + (int64_t)c * a.x_cs;
+                off = (int64_t)img * a.x_is + (int64_t)oh * a.in_row + gi * 4 * a.SW +
+                      (G == 0 ? (int64_t)c * a.x_cs : 0);
             }
             e_base[k] = (int)off;   // x holds fewer than 2^31 elements
-            c_of[k] = c;
+            c_of[k] = G == 0 ? c : gid / (32 * GPC) * a.LP + c;
         }
     };
     // copies of stage st of tile t into buffer b; every producer wave issues exactly
@@ -128,16 +149,37 @@ __global__ __launch_bounds__(kPlThreads, 1) void k_pl(PwArgs a) {
     auto fill = [&](int t, int st, int b) {
         set_tile(t);
         const uint32_t buf = bufs0 + (uint32_t)(b * stage_b);
-        if (t != a.n_pt - 1 && (st + 1) * SPS <= S && (st + 1) * SPS * 32 <= a.Cin) {
+        if (t != a.n_pt - 1 && (st + 1) * SPS <= S && (G > 0 || (st + 1) * SPS * 32 <= a.Cin)) {
             // every granule of the stage is inside x and every channel exists (not the
-            // last tile, not past the K loop): scalar bases, one VALU add per copy
+            // last tile, not past the K loop): scalar bases, one VALU add per copy (a
+            // multiply-add with the list's channel for gathered lists)
+            int ch[PCOPY];
+            if constexpr (G > 0) {
+#pragma unroll
+                for (int k = 0; k < PCOPY; ++k) ch[k] = s_list[c_of[k] + st * SPS * 32];
+            }
             for (int j = 0; j < SPS; ++j) {
                 const int s = st * SPS + j;
                 const uint32_t pb = buf + (uint32_t)(j * PB);
-                const uint32_t step_b = (uint32_t)s * 64u * (uint32_t)xcs;   // 32 channels, bytes
+                if constexpr (G > 0) {
+                    // this step's channels, the next step's read ahead
+                    int cur[PCOPY];
 #pragma unroll
-                for (int k = 0; k < PCOPY; ++k)
-                    dma_sv(xbu, (uint32_t)e_base[k] * 2u + step_b, pb + (uint32_t)((rwu * PCOPY + k) * 1024));
+                    for (int k = 0; k < PCOPY; ++k) cur[k] = ch[k];
+                    if (j + 1 < SPS) {
+#pragma unroll
+                        for (int k = 0; k < PCOPY; ++k) ch[k] = s_list[c_of[k] + (s + 1) * 32];
+                    }
+#pragma unroll
+                    for (int k = 0; k < PCOPY; ++k)
+                        dma_sv(xbu, (uint32_t)(e_base[k] + cur[k] * xcs) * 2u,
+                               pb + (uint32_t)((rwu * PCOPY + k) * 1024));
+                } else {
+                    const uint32_t step_b = (uint32_t)s * 64u * (uint32_t)xcs;   // 32 channels, bytes
+#pragma unroll
+                    for (int k = 0; k < PCOPY; ++k)
+                        dma_sv(xbu, (uint32_t)e_base[k] * 2u + step_b, pb + (uint32_t)((rwu * PCOPY + k) * 1024));
+                }
                 if (!res) {
                     const unsigned char *wbase = A_g + ((size_t)(mt_first + rwu * WCOPY) * S + s) * 1024;
                     const uint32_t wb = buf + (uint32_t)(SPS * PB + j * MT * 1024);
@@ -153,8 +195,15 @@ __global__ __launch_bounds__(kPlThreads, 1) void k_pl(PwArgs a) {
             const unsigned char *src[PCOPY];
 #pragma unroll
             for (int k = 0; k < PCOPY; ++k) {
-                const int e = e_base[k] + s * 32 * xcs;
-                const bool live = g_live[k] && s < S && s * 32 + c_of[k] < a.Cin && (uint32_t)e <= x_last;
+                int e;
+                bool live;
+                if constexpr (G > 0) {
+                    e = e_base[k] + (s < S ? (int)s_list[c_of[k] + s * 32] : 0) * xcs;
+                    live = g_live[k] && s < S && (uint32_t)e <= x_last;
+                } else {
+                    e = e_base[k] + s * 32 * xcs;
+                    live = g_live[k] && s < S && s * 32 + c_of[k] < a.Cin && (uint32_t)e <= x_last;
+                }
                 src[k] = live ? xb + (int64_t)e * 2 : zero;
             }
 #pragma unroll
@@ -177,17 +226,26 @@ __global__ __launch_bounds__(kPlThreads, 1) void k_pl(PwArgs a) {
     };
     // after stage st of tile t landed in buffer b: granules that would read past the
     // end of x, element by element.  Only the last channel of the last image ends
-    // there, so only the last stage of the last tile can hold such granules; every
-    // other item returns at once (the element loads wait for all copies in flight).
+    // there, so only the last tile can hold such granules, and with the identity list
+    // only its last stage; every other item returns at once (the element loads wait
+    // for all copies in flight).
     auto tail = [&](int t, int st, int b) {
-        if (t != a.n_pt - 1 || st != NS - 1) return;
+        if (t != a.n_pt - 1 || (G == 0 && st != NS - 1)) return;
         set_tile(t);
         for (int j = 0; j < SPS; ++j) {
             const int s = st * SPS + j;
 #pragma unroll
             for (int k = 0; k < PCOPY; ++k) {
-                const int64_t e = (int64_t)e_base[k] + (int64_t)s * 32 * xcs;
-                if (g_live[k] && s < S && s * 32 + c_of[k] < a.Cin && e + 8 > a.x_total) {
+                int64_t e;
+                bool chan;
+                if constexpr (G > 0) {
+                    e = (int64_t)e_base[k] + (int64_t)(s < S ? (int)s_list[c_of[k] + s * 32] : 0) * xcs;
+                    chan = true;
+                } else {
+                    e = (int64_t)e_base[k] + (int64_t)s * 32 * xcs;
+                    chan = s * 32 + c_of[k] < a.Cin;
+                }
+                if (g_live[k] && s < S && chan && e + 8 > a.x_total) {
                     uint16_t *dst = (uint16_t *)(bufs + b * stage_b + j * PB + ((rw * PCOPY + k) * 64 + lane) * 16);
                     const uint16_t *sx = (const uint16_t *)a.x + e;
                     // all loads first, then the writes: one wait for the granule
@@ -211,8 +269,9 @@ __global__ __launch_bounds__(kPlThreads, 1) void k_pl(PwArgs a) {
     };
     clear_acc();
     // lane's 8 channels x 4 pixels of a step: channel 8 kg + j at byte j * RB, pixels of
-    // group n16 of sub-tile ps
-    const int b_lane = 8 * kg * RB + (ps * kGroups + n16) * 4 * 2 * MODE;
+    // group n16 of sub-tile ps, in the patch of the wave's list group
+    const int glw = G > 1 ? m_loc0 / (MT / GG) : 0;
+    const int b_lane = glw * PB1 + 8 * kg * RB + (ps * kGroups + n16) * 4 * 2 * MODE;
     // weights of step j of a stage (m-tile t at + t * a_mstr)
     const int a_mstr = res ? S * 1024 : 1024;
     auto read_step = [&](const unsigned char *pb, const unsigned char *w, typename GT::Raw &r, uint4 (&ar)[TM]) {
@@ -232,7 +291,7 @@ __global__ __launch_bounds__(kPlThreads, 1) void k_pl(PwArgs a) {
         const int nst = min(SPS, S - st * SPS);
         const unsigned char *buf = bufs + b * stage_b;
         // weights of the stage's first step for this wave's first m-tile and lane; step j: + j * a_step
-        const unsigned char *w0 = res ? lds + ((m_loc0 * S + st * SPS) * 1024 + lane * 16)
+        const unsigned char *w0 = res ? lds_w + ((m_loc0 * S + st * SPS) * 1024 + lane * 16)
                                       : buf + SPS * PB + m_loc0 * 1024 + lane * 16;
         const int a_step = res ? 1024 : MT * 1024;
         typename GT::Raw r0, r1;
@@ -272,8 +331,21 @@ __global__ __launch_bounds__(kPlThreads, 1) void k_pl(PwArgs a) {
 #pragma unroll
         for (int t2 = 0; t2 < TM; ++t2) {
             const int r0 = (m_loc0 + t2) * kMT + 4 * kg;     // the lane's first row in the m-block
-            const int crow0 = mt_first * kMT + r0;             // its computed row
-            const bool all_rows = uni((mt_first + m_loc0 + t2 + 1) * kMT <= a.R ? 1 : 0) != 0;   // wave-uniform
+            // its computed row: m-tiles of the identity list follow each other; a list
+            // group's m-tiles hold its group_rows rows (rig: row inside the group)
+            int crow0, rig0 = 0;
+            bool all_rows;
+            if constexpr (G == 0) {
+                crow0 = mt_first * kMT + r0;
+                all_rows = uni((mt_first + m_loc0 + t2 + 1) * kMT <= a.R ? 1 : 0) != 0;   // wave-uniform
+            } else {
+                const int gm = mt_first + m_loc0 + t2;
+                const int gidx = gm / a.mt_per_group, mt_in = gm - gidx * a.mt_per_group;
+                rig0 = mt_in * kMT + 4 * kg;
+                crow0 = gidx * a.group_rows + rig0;
+                all_rows = uni((mt_in + 1) * kMT <= a.group_rows && gidx * a.group_rows + (mt_in + 1) * kMT <= a.R
+                                   ? 1 : 0) != 0;
+            }
             // bias, ReLU and the header check on the accumulators, each only when it applies
             // (uniform branches: most layers need one of them or none)
             if (!ok) {
@@ -297,11 +369,11 @@ __global__ __launch_bounds__(kPlThreads, 1) void k_pl(PwArgs a) {
                         for (int nt = 0; nt < 4; ++nt) acc[t2][nt][i] = acc[t2][nt][i] < 0.f ? 0.f : acc[t2][nt][i];
                 }
             }
-            int64_t yrow = ybase + (int64_t)(crow0 < a.R ? crow0 : 0) * a.y_cs;
+            int64_t yrow = ybase + (int64_t)(rig0 < a.group_rows && crow0 < a.R ? crow0 : 0) * a.y_cs;
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 const int crow = crow0 + i;
-                const bool row_ok = crow < a.R;
+                const bool row_ok = (G == 0 || rig0 + i < a.group_rows) && crow < a.R;
                 const uint64_t rmask = all_rows ? ~0ull : ballot(row_ok);
                 int64_t yo = yrow + (int64_t)i * a.y_cs;
                 if constexpr (MAP) yo = ybase + (int64_t)(row_ok ? s_orow[r0 + i] : 0) * a.y_cs;
@@ -342,7 +414,12 @@ __global__ __launch_bounds__(kPlThreads, 1) void k_pl(PwArgs a) {
     // bias and row map of the m-block (multiplying waves; read before the first barrier)
     if (!prod && (a.bias || MAP)) {
         for (int r = tid; r < MT * kMT; r += kThreads) {
-            const int crow = mt_first * kMT + r;
+            int crow = mt_first * kMT + r;
+            if constexpr (G > 0) {
+                const int gm = mt_first + r / kMT;
+                const int gidx = gm / a.mt_per_group;
+                crow = gidx * a.group_rows + (gm - gidx * a.mt_per_group) * kMT + r % kMT;
+            }
             // tiles of another plan (!ok): no map is read; output rows stay in range
             const int out = MAP ? (crow < a.R && ok ? min(max(a.rowmap[crow], 0), a.Rout - 1) : min(crow, a.Rout - 1))
                                 : crow;
@@ -360,13 +437,25 @@ __global__ __launch_bounds__(kPlThreads, 1) void k_pl(PwArgs a) {
         if (++st == NS) { st = 0; ++t; }
         if (++b == NB) b = 0;
     };
+    if constexpr (G > 0) {
+        // the m-block's lists (groups g_first .. g_first + GG - 1, consecutive in
+        // dev_tiles), before any copy is issued; not read from tiles of another plan
+        if (ok) {
+            const int g_first = mt_first / a.mt_per_group;
+            const uint32_t *src = (const uint32_t *)(a.tiles + a.off_desc16 + (size_t)g_first * a.LP * 2);
+            uint32_t *dst = (uint32_t *)lds;
+            const int nw = GG * a.LP / 2;
+            for (int i = tid; i < nw; i += kPlThreads) dst[i] = src[i];
+        }
+        __syncthreads();
+    }
     if (prod && ok) {
         if (res) {   // the m-block's weights: MT * S blocks of 1 KB, contiguous in dev_tiles
             const unsigned char *src = A_g + (size_t)mt_first * S * 1024 + lane * 16;
             const int nblk = MT * S;
             for (int b0 = rw * 4; b0 < nblk; b0 += 16) {
                 const unsigned char *s0 = src + (size_t)b0 * 1024;
-                dma_b4(s0, s0 + 1024, s0 + 2048, s0 + 3072, lds0 + (uint32_t)b0 * 1024, min(4, nblk - b0));
+                dma_b4(s0, s0 + 1024, s0 + 2048, s0 + 3072, ldsw0 + (uint32_t)b0 * 1024, min(4, nblk - b0));
             }
         }
         for (int i = 0; i < NB - 1 && i < n_items; ++i) {
@@ -430,6 +519,22 @@ pl_fn pl_pick(int NSUB, int TM, bool map) {
             default: return nullptr;
         }
     }
+    return nullptr;
+}
+
+// Gathered lists at stride 1: G list groups per m-block; a wave's m-tiles must lie in
+// one group, so groups of one m-tile take one m-tile per wave.
+inline pl_fn pl_pick_g(int NSUB, int TM, int G) {
+    if (G == 1) {
+        if (NSUB == 1) return TM == 1 ? k_pl<1, 1, 1, false, 1> : TM == 2 ? k_pl<1, 1, 2, false, 1>
+                                      : TM == 4 ? k_pl<1, 1, 4, false, 1> : nullptr;
+        if (NSUB == 2) return TM == 2 ? k_pl<1, 2, 2, false, 1> : TM == 4 ? k_pl<1, 2, 4, false, 1> : nullptr;
+    }
+    if (G == 2) {
+        if (NSUB == 1) return TM == 1 ? k_pl<1, 1, 1, false, 2> : TM == 2 ? k_pl<1, 1, 2, false, 2> : nullptr;
+        if (NSUB == 2) return TM == 2 ? k_pl<1, 2, 2, false, 2> : nullptr;
+    }
+    if (G == 4 && NSUB == 1) return TM == 1 ? k_pl<1, 1, 1, false, 4> : TM == 2 ? k_pl<1, 1, 2, false, 4> : nullptr;
     return nullptr;
 }
 

@@ -230,8 +230,22 @@ static bool plan_pointwise(Plan *p, int span_req, int n_mt, int mpg, int astep) 
 // never below the HBM time.  The fixed and latency costs were fitted to a GPU sweep
 // of every tiling of the ResNet-50 pointwise layers (the model's choice is within 1%
 // of the fastest tiling there), which found large stages (4 steps) with two or three
-// buffers best.  Returns false when nothing fits.
+// buffers best.
+// Per-block-row lists (column and block-punched blocks, stride 1) run with gathered
+// lists: an m-block holds G whole list groups (or lies inside one group), each step
+// stages G patches, and the m-block's lists (16-bit channels) stay in LDS; each patch
+// copy costs a list read and a multiply-add more.  Returns false when nothing fits.
+static bool pl_g_ok(int nsub, int tm, int g) {   // instantiated (NSUB, TM, G) of the gathered kernel
+    if (g == 1) return nsub == 1 ? (tm == 1 || tm == 2 || tm == 4) : (tm == 2 || tm == 4);
+    if (g == 2) return nsub == 1 ? (tm == 1 || tm == 2) : tm == 2;
+    if (g == 4) return nsub == 1 && (tm == 1 || tm == 2);
+    return false;
+}
+
 static bool plan_pl(Plan *p, int n_mt, int astep) {
+    const bool lists = !p->shared;
+    if (lists && (p->SW != 1 || p->counts || p->Cin > 0xffff)) return false;
+    const int mpg = p->mt_per_group;
     const int gpg = p->SW == 1 ? 2 : 1;
     int64_t groups_nom;   // groups of the nominal batch
     double hbm_bytes;
@@ -243,7 +257,7 @@ static bool plan_pl(Plan *p, int n_mt, int astep) {
     } else if (p->SW == 1) {
         groups_nom = (int64_t)kNominalImages * round_up(div_up(p->H * p->W, 4), gpg);
         hbm_bytes = ((double)p->Cin + p->RK) * kNominalImages * p->H * p->W * 2;
-        mis = ((int64_t)p->H * p->W * 2) % 16 != 0;
+        mis = ((int64_t)p->H * p->W * 2) % 16 != 0 && !p->im2col;   // im2col planes: padded
     } else {
         groups_nom = (int64_t)kNominalImages * p->Ho * div_up(p->Wo, 4);
         hbm_bytes = ((double)p->Cin * p->H * p->W / 2 + (double)p->RK * p->Ho * p->Wo) * kNominalImages * 2;
@@ -265,23 +279,34 @@ static bool plan_pl(Plan *p, int n_mt, int astep) {
             const int MT = TM * (kWaves / nsub);
             if (MT % kWaves != 0) continue;
             if (MT > 4 && MT >= 2 * n_mt) continue;   // mostly idle waves
+            int G = 0;   // list groups of an m-block (0: identity list)
+            if (lists) {
+                if (mpg <= MT && MT % mpg == 0) G = MT / mpg;
+                else if (mpg % MT == 0) G = 1;
+                else continue;
+                if ((MT / G) % TM != 0 || !pl_g_ok(nsub, TM, G)) continue;
+            }
+            const int GG = std::max(G, 1);
+            const int pc = GG * pcopy;   // patch copies per copying wave and step
+            const int64_t lds_list = lists ? align256((int64_t)GG * p->LP * 2) : 0;
             const int n_mb = div_up(n_mt, MT);
             for (int resident = 0; resident <= 1; ++resident)
             for (int sps = 1; sps <= 4 && sps <= p->S; sps *= 2) {
                 const int wcopy = resident ? 0 : MT / kWaves;
                 const int64_t a_res = resident ? (int64_t)MT * p->S * 1024 : 0;
-                const int64_t step_b = 32 * rb + (resident ? 0 : (int64_t)MT * 1024);
+                const int64_t step_b = (int64_t)GG * 32 * rb + (resident ? 0 : (int64_t)MT * 1024);
                 for (int nb = 2; nb <= 8; ++nb) {
-                    const int64_t total = a_res + nb * sps * step_b;
+                    const int64_t total = lds_list + a_res + nb * sps * step_b;
                     if (total > budget) continue;
-                    const int ncp = sps * (pcopy + wcopy);
+                    const int ncp = sps * (pc + wcopy);
                     const double ns = std::ceil((double)p->S / sps);
                     double wpm = std::max(1.0, std::ceil(256.0 / n_mb));
                     if (wpm > n_pt) wpm = n_pt;
                     const double tpw = std::ceil(n_pt / wpm);
                     const double n_wg = std::ceil(n_pt / tpw) * n_mb;
                     const double rounds = std::ceil(n_wg / 256.0);
-                    const double prod = sps * (pcopy * (mis ? 200.0 : 90.0) + wcopy * 90.0) + 100.0;
+                    const double prod =
+                        sps * (pc * ((mis ? 200.0 : 90.0) + (lists ? 10.0 : 0.0)) + wcopy * 90.0) + 100.0;
                     const double comp = sps * (TM * 64.0 + 100.0) + 150.0;
                     const double stage = std::max(std::max(prod, comp), 1000.0 / (nb - 1)) + 1500.0;
                     const double out_bytes = (double)MT * kMT * np * 2;
@@ -291,19 +316,23 @@ static bool plan_pl(Plan *p, int n_mt, int astep) {
                     // at equal cost three buffers measure best (two stages in flight, one barrier
                     // per stage), more than three slightly worse
                     cyc *= 1.0 + 0.01 * std::abs(nb - 3);
+                    // gathered lists: 64-pixel tiles measured 15% faster than 128-pixel ones on
+                    // the 4096x4096 FC stack at equal modelled cost
+                    if (lists && nsub == 2) cyc *= 1.2;
                     cyc = std::max(cyc, t_hbm);
                     if (cyc < best * (1 - 1e-9)) {
                         best = cyc;
                         Plan q = *p;
                         q.pw = 1; q.pl = 1; q.gpg = gpg; q.occ = 1;
                         q.NSUB = nsub; q.NGR = rb / 16;
-                        q.CH_STRIDE = np * mode; q.CC = 32 * sps; q.SMAX = sps;
-                        q.FR = pcopy;
+                        // gathered lists hold channel numbers (the lists' own; stride 1)
+                        q.CH_STRIDE = lists ? 1 : np * mode; q.CC = 32 * sps; q.SMAX = sps;
+                        q.FR = pc;
                         q.qmode = 0; q.KS = 1; q.TM = TM; q.TPG = TM;
-                        q.MBT = MT; q.MBG = 1; q.n_mb = n_mb;
+                        q.MBT = MT; q.MBG = GG; q.n_mb = n_mb;
                         q.resident = resident; q.NB = nb;
-                        q.lds_d = 0; q.lds_a = (int)a_res;
-                        q.lds_patch = 32 * rb * sps;
+                        q.lds_d = (int)lds_list; q.lds_a = (int)a_res;
+                        q.lds_patch = GG * 32 * rb * sps;
                         q.lds_astage = resident ? 0 : MT * 1024 * sps;
                         q.lds_buf = (int)(sps * step_b);
                         q.lds_total = (int)total;
@@ -584,6 +613,15 @@ static bsp_status make_plan_impl(const bsp_scheme *s, const bsp_conv_shape *conv
 // per output row, which for 2x2 and 4x4 planes copies mostly padding, so such layers run
 // as a 1x1 layer over their im2col input (its columns are the GEMM form's columns).
 constexpr int kIm2colMaxPixels = 16;
+// bf16 convs with per-block-row lists and output planes of at most this many pixels
+// also run over their im2col input, with the pipelined gathered-list kernel: each kept
+// column is then one contiguous input row, copied whole, where the general kernel
+// re-gathers and pads every staged row of a small image.  The expanded input of the
+// nominal batch must stay small: measured on gfx950, the 8x8 VGG-16 layers (expanded
+// input up to 19 MB) ran 25% faster this way, the 16x16 ones and ResNet-50's 7x7 and
+// 14x14 layers (33-59 MB, beyond the L2 caches) slower.
+constexpr int kIm2colListPixels = 64;
+constexpr int64_t kIm2colListBytes = 24ll << 20;
 
 bsp_status make_plan(const bsp_scheme *s, const bsp_conv_shape *conv, bsp_dtype wdt,
                      int batch_for_linear, Plan *p) {
@@ -592,12 +630,19 @@ bsp_status make_plan(const bsp_scheme *s, const bsp_conv_shape *conv, bsp_dtype 
         conv->h + 2 * conv->pad_h >= conv->kh && conv->w + 2 * conv->pad_w >= conv->kw) {
         const int ho = (conv->h + 2 * conv->pad_h - conv->kh) / conv->stride_h + 1;
         const int wo = (conv->w + 2 * conv->pad_w - conv->kw) / conv->stride_w + 1;
-        if ((int64_t)ho * wo <= kIm2colMaxPixels) {
+        const bool lists = (s->regularity == BSP_COL || s->regularity == BSP_PUNCHED ||
+                            s->regularity == BSP_ROWCOL) && !s->counts;
+        const int64_t plane = (int64_t)ho * wo;
+        const int64_t kcols = (int64_t)conv->cin * conv->kh * conv->kw;
+        if (plane <= kIm2colMaxPixels ||
+            (wdt == BSP_BF16 && lists && plane <= kIm2colListPixels && kcols <= 0xffff &&
+             (int64_t)kNominalImages * kcols * round_up((int)plane, 8) * 2 <= kIm2colListBytes)) {
             if ((int64_t)conv->cin * conv->kh * conv->kw != s->cols) return BSP_EINVAL;
             if (s->regularity == BSP_PUNCHED && conv->kh * conv->kw != s->khw) return BSP_EINVAL;
             const bsp_conv_shape c2 = {conv->n, conv->cin * conv->kh * conv->kw, ho, wo, 1, 1, 1, 1, 0, 0};
             const bsp_status st = make_plan_impl(s, &c2, wdt, batch_for_linear, p, true);
-            if (st == BSP_OK) p->im2col = 1;
+            // the pipelined kernel reads the im2col planes padded to whole granules
+            if (st == BSP_OK && p->pl) p->xplane = (int)round_up((int)plane, p->GE);
             return st;
         }
     }
@@ -608,6 +653,7 @@ static bsp_status make_plan_impl(const bsp_scheme *s, const bsp_conv_shape *conv
                                  int batch_for_linear, Plan *p, bool im2col_inner) {
     if (!s || !p) return BSP_EINVAL;
     std::memset(p, 0, sizeof(*p));
+    p->im2col = im2col_inner ? 1 : 0;
     if (s->rows <= 0 || s->cols <= 0 || s->bh < 0 || s->bw < 0 || s->rate < 1) return BSP_EINVAL;
     if (s->regularity < BSP_ROW || s->regularity > BSP_PATTERN) return BSP_EINVAL;
     if (s->regularity == BSP_PATTERN && (s->khw != 9 || s->cols % 9 != 0 || s->bh > 126 || s->counts))
@@ -805,10 +851,11 @@ static bsp_status make_plan_impl(const bsp_scheme *s, const bsp_conv_shape *conv
     // pointwise layers (1x1 without padding, stride 1 or 2; linear): own kernel
     if (p->KH == 1 && p->KW == 1 && p->PH == 0 && p->PW == 0 && p->SH == p->SW &&
         (p->SW == 1 || (p->SW == 2 && p->esize == 2))) {
-        // the identity-list kernel for 1x1 convs with more than 64 input channels; with
-        // 64 or fewer (weights resident, two workgroups per CU) and for linear layers the
-        // general pointwise kernel was faster in the measured sweep
-        if ((p->esize == 2 && p->shared && !p->is_linear && p->Cin > 64 && plan_pl(p, n_mt, astep)) ||
+        // the pipelined kernel for per-block-row lists and, with the identity list, for
+        // 1x1 convs with more than 64 input channels; with 64 or fewer (weights resident,
+        // two workgroups per CU) and for dense linear layers the general pointwise kernel
+        // was faster in the measured sweep
+        if ((p->esize == 2 && (!p->shared || (!p->is_linear && p->Cin > 64)) && plan_pl(p, n_mt, astep)) ||
             plan_pointwise(p, span_req, n_mt, mpg, astep)) {
             finish_layout(p, n_mt, astep);
             return BSP_OK;

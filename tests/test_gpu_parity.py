@@ -196,6 +196,16 @@ CONV_CASES = [
     _conv_case("im2col 5x5 pad0 dense 6x6", 3, 12, 6, 6, 24, 5, 1, 0, 0, 0, DENSE, 1),
     _conv_case("im2col 3x3 pad0 unstructured 4x5", 4, 24, 4, 5, 40, 3, 1, 0, 1, 1, UNSTRUCTURED, 4),
     _conv_case("im2col 3x3 row32x32 r2 3x3 ragged", 7, 40, 3, 3, 72, 3, 1, 1, 32, 32, ROW, 2),
+    # planes of at most 64 pixels with per-block-row lists: im2col planes padded to whole
+    # granules, the pipelined kernel with gathered lists (1, 2 or 4 list groups per m-block)
+    _conv_case("im2col lists 3x3 col16x32 r4 7x7", 3, 256, 7, 7, 64, 3, 1, 1, 16, 32, COL, 4),
+    _conv_case("im2col lists 3x3 col32x32 r4 8x8 ragged rows bias", 2, 40, 8, 8, 72, 3, 1, 1, 32, 32, COL, 4,
+               bias=True),
+    _conv_case("im2col lists 3x3 col64x16 r2 6x6 relu", 3, 16, 6, 6, 128, 3, 1, 1, 64, 16, COL, 2, relu=True),
+    _conv_case("im2col lists 5x5 punched 16x8 r5 7x7 bias relu", 2, 24, 7, 7, 40, 5, 1, 2, 16, 8, PUNCHED, 5,
+               relu=True, bias=True),
+    _conv_case("im2col lists 3x3 s2 col8x16 r8 13x13", 3, 48, 13, 13, 64, 3, 2, 1, 8, 16, COL, 8),
+    _conv_case("im2col lists 3x3 rowcol 16x32 r2 5x7", 2, 64, 5, 7, 48, 3, 1, 1, 16, 32, ROWCOL, 2),
 ]
 
 
@@ -428,7 +438,9 @@ def test_c4_fc_layer_every_column(B):
 @pytest.mark.parametrize("batch,reg,bh,bw,rate,out_dt,relu", [
     (37, COL, 32, 32, 10, "bf16", False), (100, ROW, 32, 32, 2, "f32", True),
     (64, DENSE, 0, 0, 1, "bf16", True), (130, COL, 16, 64, 4, "bf16", False),
-    (100, ROW, 0, 0, 4, "bf16", True), (70, ROW, 32, 0, 2, "f32", False), (90, ROWCOL, 32, 32, 2, "bf16", True)])
+    (100, ROW, 0, 0, 4, "bf16", True), (70, ROW, 32, 0, 2, "f32", False), (90, ROWCOL, 32, 32, 2, "bf16", True),
+    (64, COL, 64, 32, 4, "bf16", True), (48, COL, 8, 16, 8, "f32", False), (96, COL, 0, 32, 4, "bf16", False),
+    (203, COL, 16, 32, 4, "bf16", True)])
 def test_linear_small(B, batch, reg, bh, bw, rate, out_dt, relu):
     layer = LinearLayer("fc", batch, 320, 200, bh, bw, reg, rate, "bf16", ("uniform", -1, 1),
                         ("normal", 0, 0.05), relu=relu)
