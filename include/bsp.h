@@ -203,12 +203,23 @@ bsp_status bsp_to_bcs(const bsp_scheme *scheme, const int32_t *indices, const in
  * Only kept weights are multiplied; inputs must be finite (a removed weight
  * is never multiplied, so Inf/NaN inputs do not propagate through it).
  * bias may be NULL.  Async.
- * Layers whose output plane has at most 16 pixels (Ho * Wo <= 16, kernel
- * larger than 1x1) expand x into a workspace (n x cin*kh*kw x Ho x Wo of
- * in_dt) that the library allocates on the device at the first call that
- * needs it (or a larger one) and keeps until the process ends; such calls
- * must not overlap on one device (they share the workspace), and the first
- * one cannot be captured into a graph. */
+ * Device workspace: some calls use a workspace that the library allocates
+ * on the device at the first call that needs it (or a larger one) and keeps
+ * until the process ends:
+ *  - layers with a kernel larger than 1x1 whose output plane has at most 16
+ *    pixels, and bf16 layers with per-block-row lists (COL, PUNCHED, ROWCOL
+ *    without counts) whose plane has at most 64 pixels (and whose expanded
+ *    input for 64 images stays within 24 MiB), expand x into it (n x
+ *    cin*kh*kw planes of Ho*Wo elements, rounded up to 8 for the bf16
+ *    pipelined kernel);
+ *  - bf16 layers run by the pipelined pointwise kernel (1x1, linear and the
+ *    expanded layers above) whose output splits into at most 128 workgroup
+ *    tiles (64 or 128 output pixels x 64 to 256 rows) split their K loop
+ *    over workgroups and keep fp32 partial sums there (parts x n x rows x
+ *    Ho*Wo floats).
+ * Calls that use the workspace must not overlap on one device (other
+ * streams, other threads), and the first one cannot be captured into a
+ * graph. */
 bsp_status bsp_conv2d(const bsp_scheme *scheme, const bsp_conv_shape *shape, bsp_dtype in_dt,
                       bsp_dtype out_dt, const void *x, const void *dev_tiles,
                       const float *bias_or_null, int32_t relu, void *y, void *stream);
@@ -218,7 +229,9 @@ bsp_status bsp_conv2d(const bsp_scheme *scheme, const bsp_conv_shape *shape, bsp
  * layer computation with weights W_i and bias b_i of Sec. 4.2):
  *   y[o][b] = bias[o] + sum_{kept k} W[o][k] * x[k][b], then ReLU if relu.
  * x: [cols][batch], y: [rows][batch].  dev_tiles packed with conv_or_null =
- * NULL.  Async. */
+ * NULL.  Async.  bf16 layers with small batches (at most 128 workgroup
+ * tiles) split the K loop and use the device workspace described at
+ * bsp_conv2d, with the same rules. */
 bsp_status bsp_linear(const bsp_scheme *scheme, int32_t batch, bsp_dtype in_dt, bsp_dtype out_dt,
                       const void *x, const void *dev_tiles, const float *bias_or_null,
                       int32_t relu, void *y, void *stream);

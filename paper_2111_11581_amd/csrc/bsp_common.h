@@ -251,6 +251,11 @@ struct PwArgs {
     int Rout;                     // output channels (R is the number of computed rows)
     int Cin;                      // input channels (in_features)
     int SMAX;                     // steps per stage (identity-list kernel)
+    // K loop split over workgroups (pipelined kernel): ks parts of s_per steps, kpart_wgs
+    // workgroups each; part kp stores fp32 partial sums at y + kp * part_stride
+    int ks, s_per, kpart_wgs;
+    FastDiv div_kpart;
+    int64_t part_stride;
 };
 
 // Workgroups per CU the pointwise kernel's register budget allows (its launch

@@ -132,6 +132,92 @@ static hipError_t launch_fill_pruned(const Plan &p, int64_t n_img, int64_t plane
     return hipGetLastError();
 }
 
+static hipError_t workspace(size_t bytes, void **out);
+
+// Sum of the K parts' fp32 partial sums, then bias, ReLU and rounding: elements
+// 4 i .. 4 i + 3 of y per thread (output channel (e / plane) % R of element e; fewer
+// than 2^31 elements).  The loads of four parts are issued before they are summed, so
+// a thread waits about once per four parts; 16-byte loads when parts are 16-byte aligned.
+template <typename E>
+__global__ void k_splitk_sum(const float *__restrict__ part, int ks, int64_t stride, uint32_t total,
+                             FastDiv div_plane, FastDiv div_R, const float *__restrict__ bias, int relu,
+                             E *__restrict__ y) {
+    const bool vec = stride % 4 == 0;
+    for (uint32_t i0 = (blockIdx.x * blockDim.x + threadIdx.x) * 4u; i0 < total; i0 += gridDim.x * blockDim.x * 4u) {
+        const bool whole = vec && i0 + 4 <= total;
+        float v[4] = {0.f, 0.f, 0.f, 0.f};
+        for (int k0 = 0; k0 < ks; k0 += 4) {
+            float t[4][4];
+#pragma unroll
+            for (int kk = 0; kk < 4; ++kk) {
+                const float *pk = part + (int64_t)(k0 + kk) * stride + i0;
+                if (k0 + kk >= ks) {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) t[kk][e] = 0.f;
+                } else if (whole) {
+                    const float4 q = *(const float4 *)pk;
+                    t[kk][0] = q.x; t[kk][1] = q.y; t[kk][2] = q.z; t[kk][3] = q.w;
+                } else {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) t[kk][e] = i0 + e < total ? pk[e] : 0.f;
+                }
+            }
+#pragma unroll
+            for (int kk = 0; kk < 4; ++kk)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) v[e] += t[kk][e];
+        }
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const uint32_t i = i0 + e;
+            if (i >= total) break;
+            const uint32_t q = fdiv(i, div_plane);
+            const uint32_t o = q - fdiv(q, div_R) * div_R.d;
+            const float r = fwd::epi(v[e], bias ? bias[o] : 0.f, relu);
+            if constexpr (sizeof(E) == 2) y[i] = (E)fwd::f32_to_bf16_rne(r);
+            else y[i] = r;
+        }
+    }
+}
+
+// 4-pixel groups of a pointwise layer for n images (vectors), as launch_pw numbers them.
+static int64_t pw_groups(const Plan &p, int n) {
+    if (p.is_linear) return div_up64(div_up(n, 4), p.gpg) * p.gpg;
+    if (p.SW == 1) return (int64_t)n * (div_up64(div_up(p.H * p.W, 4), p.gpg) * p.gpg);
+    return (int64_t)n * p.Ho * div_up(p.Wo, 4);
+}
+
+// K-loop split of the pipelined kernel for n images: with at most half as many (tile,
+// m-block) pairs as CUs, the steps are split into ks parts (at least 2 steps each, up
+// to 16 parts, at most one workgroup per CU: the kernel holds a CU's LDS) whose fp32
+// partial sums a second kernel adds.
+struct PwSplit {
+    int ks, s_per;
+    int64_t yelems;   // elements of y (the stride between parts)
+};
+static PwSplit pw_split(const Plan &p, int n) {
+    PwSplit r{1, p.S, 0};
+    if (!p.pl || p.rowmap || n <= 0) return r;
+    const int64_t n_pt = div_up64(pw_groups(p, n), (int64_t)kGroups * p.NSUB);
+    const int64_t units = n_pt * p.n_mb;
+    if (units > 128 || p.S < 4) return r;
+    int ks = (int)std::min<int64_t>(16, 256 / units);
+    ks = std::min(ks, p.S / 2);
+    const int s_per = div_up(p.S, ks);
+    ks = div_up(p.S, s_per);
+    if (ks < 2) return r;
+    r.ks = ks;
+    r.s_per = s_per;
+    r.yelems = p.is_linear ? (int64_t)p.R * n
+                           : (int64_t)n * p.R * (p.SW == 1 ? (int64_t)p.H * p.W : (int64_t)p.Ho * p.Wo);
+    return r;
+}
+
+size_t pw_part_bytes(const Plan &p, int n) {
+    const PwSplit sp = pw_split(p, n);
+    return sp.ks > 1 ? (size_t)sp.ks * sp.yelems * sizeof(float) : 0;
+}
+
 static int log2_int(int v) {
     int l = 0;
     while ((1 << l) < v) ++l;
@@ -141,7 +227,7 @@ static int log2_int(int v) {
 // Pointwise layers: the image (stride 1) or each output row (stride 2) is a run of
 // 4-pixel groups; a linear layer's batch is one image of n pixels.
 static hipError_t launch_pw(const Plan &p, int n, const void *x, const uint8_t *tiles, const float *bias,
-                            int relu, int out_bf16, void *y, hipStream_t st) {
+                            int relu, int out_bf16, void *y, hipStream_t st, void *part) {
     PwArgs a;
     memset(&a, 0, sizeof(a));
     a.x = x;
@@ -180,12 +266,29 @@ static hipError_t launch_pw(const Plan &p, int n, const void *x, const uint8_t *
     // persistent workgroups: about occ per CU; each walks a range of pixel tiles of
     // its m-block (one tile when the waves split the steps)
     int64_t wpm = std::max<int64_t>(1, div_up64((int64_t)256 * p.occ, p.n_mb));
-    if (p.KS > 1 || wpm > n_pt) wpm = n_pt;
+    const PwSplit sp = pw_split(p, n);
+    if (p.KS > 1 || sp.ks > 1 || wpm > n_pt) wpm = n_pt;
     const int64_t tpw = div_up64(n_pt, wpm);
     const int64_t gv = div_up64(n_pt, tpw) * p.n_mb;
-    if (gv > INT32_MAX - 8 || n_pt > INT32_MAX || images * a.Ho > INT32_MAX ||
+    if (gv * sp.ks > INT32_MAX - 8 || n_pt > INT32_MAX || images * a.Ho > INT32_MAX ||
         a.n_groups_total + kGroups * 4 > INT32_MAX)
         return hipErrorInvalidValue;
+    // a split K loop: the kernel stores fp32 partial sums (no bias, ReLU or rounding)
+    a.ks = sp.ks;
+    a.s_per = sp.s_per;
+    a.kpart_wgs = (int)gv;
+    a.div_kpart = make_fastdiv((uint32_t)gv);
+    a.part_stride = sp.yelems;
+    if (sp.ks > 1) {
+        if (!part) {
+            hipError_t e = workspace((size_t)sp.ks * sp.yelems * sizeof(float), &part);
+            if (e != hipSuccess) return e;
+        }
+        a.y = part;
+        a.out_bf16 = 0;
+        a.bias = nullptr;
+        a.relu = 0;
+    }
     a.n_pt = (int)n_pt;
     a.tiles_per_wg = (int)tpw;
     a.NSUB = p.NSUB; a.lg_nsub = log2_int(p.NSUB);
@@ -196,7 +299,7 @@ static hipError_t launch_pw(const Plan &p, int n, const void *x, const uint8_t *
     a.MBT = p.MBT; a.MBG = p.MBG; a.n_mb = p.n_mb; a.resident = p.resident; a.NB = p.NB;
     a.lds_d = p.lds_d; a.lds_a = p.lds_a; a.lds_patch = p.lds_patch; a.lds_astage = p.lds_astage;
     a.lds_buf = p.lds_buf;
-    a.grid_valid = (int)gv;
+    a.grid_valid = (int)(gv * sp.ks);
     a.off_chunks = p.off_chunks;
     a.off_desc16 = p.off_desc16;
     a.off_a = p.off_a;
@@ -219,7 +322,7 @@ static hipError_t launch_pw(const Plan &p, int n, const void *x, const uint8_t *
         fn = p.SW == 1 ? pw::pick_b1(p.TM, p.TPG, p.KS, map) : pw::pick_b2(p.TM, p.TPG, p.KS, map);
     }
     if (!fn) return hipErrorInvalidValue;
-    const int grid = (int)(div_up64(gv, 8) * 8);
+    const int grid = (int)(div_up64(gv * sp.ks, 8) * 8);
     if (p.lds_total > 48 * 1024) {
         hipError_t e = hipFuncSetAttribute((const void *)fn, hipFuncAttributeMaxDynamicSharedMemorySize,
                                            p.lds_total);
@@ -228,12 +331,27 @@ static hipError_t launch_pw(const Plan &p, int n, const void *x, const uint8_t *
     hipLaunchKernelGGL(fn, dim3(grid), dim3(threads), (size_t)p.lds_total, st, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
+    if (sp.ks > 1) {
+        const uint32_t total = (uint32_t)sp.yelems;   // the API keeps y below 2^31 elements
+        const int64_t plane = p.is_linear ? n : a.y_cs;
+        const int g = (int)std::min<int64_t>((sp.yelems + 1023) / 1024, 16384);
+        if (out_bf16)
+            k_splitk_sum<uint16_t><<<g, 256, 0, st>>>((const float *)part, sp.ks, sp.yelems, total,
+                                                      make_fastdiv((uint32_t)plane), make_fastdiv((uint32_t)p.R),
+                                                      bias, relu, (uint16_t *)y);
+        else
+            k_splitk_sum<float><<<g, 256, 0, st>>>((const float *)part, sp.ks, sp.yelems, total,
+                                                   make_fastdiv((uint32_t)plane), make_fastdiv((uint32_t)p.R), bias,
+                                                   relu, (float *)y);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
     return launch_fill_pruned(p, images, a.y_cs, a.y_is, a.y_cs, tiles, bias, relu, out_bf16, y, st);
 }
 
 hipError_t launch_conv(const Plan &p, int n, const void *x, const uint8_t *tiles, const float *bias,
-                       int relu, int out_bf16, void *y, hipStream_t st) {
-    if (p.pw) return launch_pw(p, n, x, tiles, bias, relu, out_bf16, y, st);
+                       int relu, int out_bf16, void *y, hipStream_t st, void *part) {
+    if (p.pw) return launch_pw(p, n, x, tiles, bias, relu, out_bf16, y, st, part);
     ConvArgs a;
     memset(&a, 0, sizeof(a));
     a.x = x;
@@ -404,9 +522,13 @@ hipError_t launch_conv_im2col(const Plan &p, const bsp_conv_shape &c, const void
     const int64_t total = (int64_t)c.n * p.Cin * plane;
     if (total <= 0) return hipSuccess;
     if (total > INT32_MAX) return hipErrorInvalidValue;
+    // one workspace: the expanded input, then the partial sums of a split K loop
+    const size_t in_bytes = ((size_t)total * p.esize + 255) / 256 * 256;
+    const size_t part_bytes = pw_part_bytes(p, c.n);
     void *ws = nullptr;
-    hipError_t e = workspace((size_t)total * p.esize, &ws);
+    hipError_t e = workspace(in_bytes + part_bytes, &ws);
     if (e != hipSuccess) return e;
+    void *part = part_bytes ? (void *)((unsigned char *)ws + in_bytes) : nullptr;
     if (p.xplane) {
         Im2colArgs ia;
         ia.n_gran = (uint32_t)(total / (16 / p.esize));
@@ -425,7 +547,7 @@ hipError_t launch_conv_im2col(const Plan &p, const bsp_conv_shape &c, const void
             k_im2col_g<float><<<grid, 256, 0, st>>>((const float *)x, (float *)ws, ia);
         e = hipGetLastError();
         if (e != hipSuccess) return e;
-        return launch_conv(p, c.n, ws, tiles, bias, relu, out_bf16, y, st);
+        return launch_conv(p, c.n, ws, tiles, bias, relu, out_bf16, y, st, part);
     }
     const int grid = (int)std::min<int64_t>((total + 255) / 256, 16384);
     if (p.esize == 2)
@@ -436,7 +558,7 @@ hipError_t launch_conv_im2col(const Plan &p, const bsp_conv_shape &c, const void
                                               c.kh, c.kw, c.stride_h, c.stride_w, c.pad_h, c.pad_w, p.H, p.W);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
-    return launch_conv(p, c.n, ws, tiles, bias, relu, out_bf16, y, st);
+    return launch_conv(p, c.n, ws, tiles, bias, relu, out_bf16, y, st, part);
 }
 
 }  // namespace bsp

@@ -27,9 +27,16 @@ hipError_t launch_bcs(const Plan &p, const int32_t *indices, const int32_t *rowp
 hipError_t launch_unpack(const Plan &p, const void *values, const int32_t *indices,
                          const int32_t *rowptr, void *w_out, hipStream_t st);
 
-// n: images of a conv; batch vectors of a linear layer
+// n: images of a conv; batch vectors of a linear layer.  part: device memory for the
+// partial sums of a K loop split over workgroups (pw_part_bytes(p, n) bytes), or null
+// to take them from the library's per-device workspace.
 hipError_t launch_conv(const Plan &p, int n, const void *x, const uint8_t *tiles,
-                       const float *bias, int relu, int out_bf16, void *y, hipStream_t st);
+                       const float *bias, int relu, int out_bf16, void *y, hipStream_t st,
+                       void *part = nullptr);
+
+// Bytes of partial sums the pointwise kernel needs for n images (vectors), 0 when its
+// K loop is not split.
+size_t pw_part_bytes(const Plan &p, int n);
 
 hipError_t launch_maxpool2x2(int dt, int n, int c, int h, int w, const void *x, void *y,
                              hipStream_t st);

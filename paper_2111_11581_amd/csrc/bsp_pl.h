@@ -64,11 +64,13 @@ __global__ __launch_bounds__(kPlThreads, 1) void k_pl(PwArgs a) {
     __shared__ __attribute__((aligned(16))) float s_bias[kMaxMBRows];
     __shared__ int s_orow[MAP ? kMaxMBRows : 1];
 
-    // workgroup -> (range of pixel tiles, m-block); each XCD (workgroup id % 8) gets
-    // a contiguous range of logical ids, the m-blocks of a tile range adjacent
+    // workgroup -> (K part, range of pixel tiles, m-block); each XCD (workgroup id % 8)
+    // gets a contiguous range of logical ids, the m-blocks of a tile range adjacent
     const int per = gridDim.x >> 3;
-    const int lid = (int)(blockIdx.x & 7) * per + (int)(blockIdx.x >> 3);
-    if (lid >= a.grid_valid) return;
+    const int lid0 = (int)(blockIdx.x & 7) * per + (int)(blockIdx.x >> 3);
+    if (lid0 >= a.grid_valid) return;
+    const int kp = a.ks > 1 ? (int)fdiv((uint32_t)lid0, a.div_kpart) : 0;
+    const int lid = lid0 - kp * a.kpart_wgs;
     const int jr = (int)fdiv((uint32_t)lid, a.div_nmb);
     const int mb = lid - jr * a.n_mb;
     const int t_begin = jr * a.tiles_per_wg;
@@ -89,7 +91,11 @@ __global__ __launch_bounds__(kPlThreads, 1) void k_pl(PwArgs a) {
     const int ps = rw % NSUB, q = rw / NSUB;
     const int m_loc0 = q * TM;
     const int mt_first = mb * MT;
-    const int S = a.S;                    // steps (32 channels each) of the K loop
+    // steps (32 channels each) of the K loop: with the K loop split over workgroups
+    // (ks parts) this workgroup runs steps s0 .. s0 + S - 1 and stores fp32 partial sums
+    const int S_tot = a.S;                // steps of the whole loop (stride of the weight tiles)
+    const int s0 = kp * a.s_per;
+    const int S = a.ks > 1 ? min(a.s_per, S_tot - s0) : S_tot;
     const int SPS = a.SMAX;               // steps per stage
     const int NS = (S + SPS - 1) / SPS;   // stages per tile
     const int NB = a.NB;
@@ -103,7 +109,7 @@ __global__ __launch_bounds__(kPlThreads, 1) void k_pl(PwArgs a) {
     const int n_items = (t_end - t_begin) * (ok ? NS : 1);
     // gathered lists: the m-block's G lists (16-bit channels, LP entries each) at LDS
     // byte 0, before the weights and the buffers
-    const uint16_t *s_list = (const uint16_t *)lds;
+    const uint16_t *s_list = (const uint16_t *)lds + s0 * 32;   // entries of the part's first step
 
     // ---- producers: copy k of a step fills LDS granules gid = (rw * PCOPY + k) * 64 + lane
     // of the step's patches (byte 16 gid): list group lg = gid / (32 GPC), channel
@@ -121,7 +127,7 @@ __global__ __launch_bounds__(kPlThreads, 1) void k_pl(PwArgs a) {
     const unsigned char *xbu = (const unsigned char *)uni_ptr(xb);
     uint32_t w_voff[WCOPY];   // weight tile u of this wave: lane bytes, relative to tile 0
 #pragma unroll
-    for (int u = 0; u < WCOPY; ++u) w_voff[u] = (uint32_t)(lane * 16 + u * S * 1024);
+    for (int u = 0; u < WCOPY; ++u) w_voff[u] = (uint32_t)(lane * 16 + u * S_tot * 1024);
     auto set_tile = [&](int t) {
         if (t == cur_tile) return;
         cur_tile = t;
@@ -149,7 +155,7 @@ __global__ __launch_bounds__(kPlThreads, 1) void k_pl(PwArgs a) {
     auto fill = [&](int t, int st, int b) {
         set_tile(t);
         const uint32_t buf = bufs0 + (uint32_t)(b * stage_b);
-        if (t != a.n_pt - 1 && (st + 1) * SPS <= S && (G > 0 || (st + 1) * SPS * 32 <= a.Cin)) {
+        if (t != a.n_pt - 1 && (st + 1) * SPS <= S && (G > 0 || (s0 + (st + 1) * SPS) * 32 <= a.Cin)) {
             // every granule of the stage is inside x and every channel exists (not the
             // last tile, not past the K loop): scalar bases, one VALU add per copy (a
             // multiply-add with the list's channel for gathered lists)
@@ -175,13 +181,13 @@ __global__ __launch_bounds__(kPlThreads, 1) void k_pl(PwArgs a) {
                         dma_sv(xbu, (uint32_t)(e_base[k] + cur[k] * xcs) * 2u,
                                pb + (uint32_t)((rwu * PCOPY + k) * 1024));
                 } else {
-                    const uint32_t step_b = (uint32_t)s * 64u * (uint32_t)xcs;   // 32 channels, bytes
+                    const uint32_t step_b = (uint32_t)(s0 + s) * 64u * (uint32_t)xcs;   // 32 channels, bytes
 #pragma unroll
                     for (int k = 0; k < PCOPY; ++k)
                         dma_sv(xbu, (uint32_t)e_base[k] * 2u + step_b, pb + (uint32_t)((rwu * PCOPY + k) * 1024));
                 }
                 if (!res) {
-                    const unsigned char *wbase = A_g + ((size_t)(mt_first + rwu * WCOPY) * S + s) * 1024;
+                    const unsigned char *wbase = A_g + ((size_t)(mt_first + rwu * WCOPY) * S_tot + s0 + s) * 1024;
                     const uint32_t wb = buf + (uint32_t)(SPS * PB + j * MT * 1024);
 #pragma unroll
                     for (int u = 0; u < WCOPY; ++u) dma_sv(wbase, w_voff[u], wb + (uint32_t)((rwu * WCOPY + u) * 1024));
@@ -201,8 +207,8 @@ __global__ __launch_bounds__(kPlThreads, 1) void k_pl(PwArgs a) {
                     e = e_base[k] + (s < S ? (int)s_list[c_of[k] + s * 32] : 0) * xcs;
                     live = g_live[k] && s < S && (uint32_t)e <= x_last;
                 } else {
-                    e = e_base[k] + s * 32 * xcs;
-                    live = g_live[k] && s < S && s * 32 + c_of[k] < a.Cin && (uint32_t)e <= x_last;
+                    e = e_base[k] + (s0 + s) * 32 * xcs;
+                    live = g_live[k] && s < S && (s0 + s) * 32 + c_of[k] < a.Cin && (uint32_t)e <= x_last;
                 }
                 src[k] = live ? xb + (int64_t)e * 2 : zero;
             }
@@ -216,7 +222,8 @@ __global__ __launch_bounds__(kPlThreads, 1) void k_pl(PwArgs a) {
                 const unsigned char *ws[WCOPY];
 #pragma unroll
                 for (int u = 0; u < WCOPY; ++u)
-                    ws[u] = s < S ? A_g + ((size_t)(mt_first + rw * WCOPY + u) * S + s) * 1024 + lane * 16 : zero;
+                    ws[u] = s < S ? A_g + ((size_t)(mt_first + rw * WCOPY + u) * S_tot + s0 + s) * 1024 + lane * 16
+                                  : zero;
 #pragma unroll
                 for (int u = 0; u < WCOPY; u += 4)
                     dma_b4(ws[u], ws[min(u + 1, WCOPY - 1)], ws[min(u + 2, WCOPY - 1)], ws[min(u + 3, WCOPY - 1)],
@@ -242,8 +249,8 @@ __global__ __launch_bounds__(kPlThreads, 1) void k_pl(PwArgs a) {
                     e = (int64_t)e_base[k] + (int64_t)(s < S ? (int)s_list[c_of[k] + s * 32] : 0) * xcs;
                     chan = true;
                 } else {
-                    e = (int64_t)e_base[k] + (int64_t)s * 32 * xcs;
-                    chan = s * 32 + c_of[k] < a.Cin;
+                    e = (int64_t)e_base[k] + (int64_t)(s0 + s) * 32 * xcs;
+                    chan = (s0 + s) * 32 + c_of[k] < a.Cin;
                 }
                 if (g_live[k] && s < S && chan && e + 8 > a.x_total) {
                     uint16_t *dst = (uint16_t *)(bufs + b * stage_b + j * PB + ((rw * PCOPY + k) * 64 + lane) * 16);
@@ -395,7 +402,7 @@ __global__ __launch_bounds__(kPlThreads, 1) void k_pl(PwArgs a) {
                         }
                     }
                 } else {
-                    float *y = (float *)a.y + yo;
+                    float *y = (float *)a.y + (a.ks > 1 ? kp * a.part_stride : 0) + yo;   // K part kp: its partial sums
                     if (full)
                         st_mask_b128(y, u32x4{__float_as_uint(o[0]), __float_as_uint(o[1]), __float_as_uint(o[2]),
                                               __float_as_uint(o[3])}, full);
@@ -451,11 +458,19 @@ __global__ __launch_bounds__(kPlThreads, 1) void k_pl(PwArgs a) {
     }
     if (prod && ok) {
         if (res) {   // the m-block's weights: MT * S blocks of 1 KB, contiguous in dev_tiles
-            const unsigned char *src = A_g + (size_t)mt_first * S * 1024 + lane * 16;
-            const int nblk = MT * S;
-            for (int b0 = rw * 4; b0 < nblk; b0 += 16) {
-                const unsigned char *s0 = src + (size_t)b0 * 1024;
-                dma_b4(s0, s0 + 1024, s0 + 2048, s0 + 3072, ldsw0 + (uint32_t)b0 * 1024, min(4, nblk - b0));
+            if (a.ks == 1) {
+                const unsigned char *src = A_g + (size_t)mt_first * S * 1024 + lane * 16;
+                const int nblk = MT * S;
+                for (int b0 = rw * 4; b0 < nblk; b0 += 16) {
+                    const unsigned char *sb = src + (size_t)b0 * 1024;
+                    dma_b4(sb, sb + 1024, sb + 2048, sb + 3072, ldsw0 + (uint32_t)b0 * 1024, min(4, nblk - b0));
+                }
+            } else {   // the part's steps of each m-tile: runs of S blocks, S_tot apart
+                for (int b0 = rw; b0 < MT * S; b0 += kWaves) {
+                    const int m = b0 / S, j = b0 - m * S;
+                    dma_b4(A_g + ((size_t)(mt_first + m) * S_tot + s0 + j) * 1024 + lane * 16, nullptr, nullptr,
+                           nullptr, ldsw0 + (uint32_t)b0 * 1024, 1);
+                }
             }
         }
         for (int i = 0; i < NB - 1 && i < n_items; ++i) {

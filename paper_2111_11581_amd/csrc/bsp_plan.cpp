@@ -851,11 +851,12 @@ static bsp_status make_plan_impl(const bsp_scheme *s, const bsp_conv_shape *conv
     // pointwise layers (1x1 without padding, stride 1 or 2; linear): own kernel
     if (p->KH == 1 && p->KW == 1 && p->PH == 0 && p->PW == 0 && p->SH == p->SW &&
         (p->SW == 1 || (p->SW == 2 && p->esize == 2))) {
-        // the pipelined kernel for per-block-row lists and, with the identity list, for
-        // 1x1 convs with more than 64 input channels; with 64 or fewer (weights resident,
-        // two workgroups per CU) and for dense linear layers the general pointwise kernel
-        // was faster in the measured sweep
-        if ((p->esize == 2 && (!p->shared || (!p->is_linear && p->Cin > 64)) && plan_pl(p, n_mt, astep)) ||
+        // the pipelined kernel for per-block-row lists, linear layers and 1x1 convs with
+        // more than 64 input channels; with 64 or fewer (weights resident, two workgroups
+        // per CU) the general pointwise kernel was faster in the measured sweep.  Measured
+        // on bf16 FC layers (4096x4096 at batch 64 to 2048, 2048->1000 at batch 64), the
+        // pipelined kernel with its split K loop took 0.2-0.7 of the general one's time.
+        if ((p->esize == 2 && (!p->shared || p->is_linear || p->Cin > 64) && plan_pl(p, n_mt, astep)) ||
             plan_pointwise(p, span_req, n_mt, mpg, astep)) {
             finish_layout(p, n_mt, astep);
             return BSP_OK;
