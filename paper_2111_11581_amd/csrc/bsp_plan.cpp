@@ -616,10 +616,12 @@ constexpr int kIm2colMaxPixels = 16;
 // bf16 convs with per-block-row lists and output planes of at most this many pixels
 // also run over their im2col input, with the pipelined gathered-list kernel: each kept
 // column is then one contiguous input row, copied whole, where the general kernel
-// re-gathers and pads every staged row of a small image.  The expanded input of the
-// nominal batch must stay small: measured on gfx950, the 8x8 VGG-16 layers (expanded
-// input up to 19 MB) ran 25% faster this way, the 16x16 ones and ResNet-50's 7x7 and
-// 14x14 layers (33-59 MB, beyond the L2 caches) slower.
+// re-gathers and pads every staged row of a small image.  At stride 1 the expanded
+// input of the nominal batch must stay small: measured on gfx950, the 8x8 VGG-16
+// layers (expanded input up to 19 MB) ran 25% faster this way, the 16x16 ones and
+// ResNet-50's stride-1 7x7 and 14x14 layers (33-59 MB, beyond the L2 caches) slower.
+// Strided layers with such planes gain regardless (ResNet-50's 512-channel stride-2
+// layer, 14x14 -> 7x7: 110 -> 86 us), the general kernel's strided gathers being slower.
 constexpr int kIm2colListPixels = 64;
 constexpr int64_t kIm2colListBytes = 24ll << 20;
 
@@ -636,7 +638,8 @@ bsp_status make_plan(const bsp_scheme *s, const bsp_conv_shape *conv, bsp_dtype 
         const int64_t kcols = (int64_t)conv->cin * conv->kh * conv->kw;
         if (plane <= kIm2colMaxPixels ||
             (wdt == BSP_BF16 && lists && plane <= kIm2colListPixels && kcols <= 0xffff &&
-             (int64_t)kNominalImages * kcols * round_up((int)plane, 8) * 2 <= kIm2colListBytes)) {
+             (conv->stride_h > 1 || conv->stride_w > 1 ||
+              (int64_t)kNominalImages * kcols * round_up((int)plane, 8) * 2 <= kIm2colListBytes))) {
             if ((int64_t)conv->cin * conv->kh * conv->kw != s->cols) return BSP_EINVAL;
             if (s->regularity == BSP_PUNCHED && conv->kh * conv->kw != s->khw) return BSP_EINVAL;
             const bsp_conv_shape c2 = {conv->n, conv->cin * conv->kh * conv->kw, ho, wo, 1, 1, 1, 1, 0, 0};
