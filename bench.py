@@ -540,11 +540,20 @@ def main():
         step()
     torch.cuda.synchronize()
 
-    # plain copy kernel of known size: its HBM counters calibrate the forward kernels
+    # plain copy kernel of known size: its HBM counters calibrate the forward kernels, and
+    # its rate (bytes read + written per second) is what a plain streaming kernel reaches
+    # on this GPU, beside the nominal 8 TB/s
     cal_src = torch.zeros(CALIB_BYTES // 2, dtype=torch.bfloat16, device=dev)
     cal_dst = torch.empty_like(cal_src)
     torch.neg(cal_src, out=cal_dst)
     torch.cuda.synchronize()
+    c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    c0.record()
+    for _ in range(5):
+        torch.neg(cal_src, out=cal_dst)
+    c1.record()
+    torch.cuda.synchronize()
+    copy_gbs = 5 * 2 * CALIB_BYTES / (c0.elapsed_time(c1) * 1e-3) / 1e9
     del cal_src, cal_dst
 
     for _ in range(args.warmup):
@@ -601,7 +610,8 @@ def main():
             "frac": round(achieved_gbs * 1e9 / PEAK_HBM, 4), "traffic": None,
             "algorithmic_bytes_per_launch": round(b_alg / len(ops)),
             "algorithmic_bytes_per_step": int(b_alg),
-            "avg_launch_us": round(ms_per_step * 1e3 / len(ops), 3)}
+            "avg_launch_us": round(ms_per_step * 1e3 / len(ops), 3),
+            "copy_gbs": round(copy_gbs, 1), "frac_of_copy": round(achieved_gbs / copy_gbs, 4)}
     kept_util = f_kept / t_step / peak
     roof["mfma"] = {"peak_tflops": peak / 1e12, "kept_tflops": round(f_kept / t_step / 1e12, 3),
                     "kept_frac": round(kept_util, 4), "executed_tflops": None, "executed_frac": None,
