@@ -134,49 +134,26 @@ static hipError_t launch_fill_pruned(const Plan &p, int64_t n_img, int64_t plane
 
 static hipError_t workspace(size_t bytes, void **out);
 
-// Sum of the K parts' fp32 partial sums, then bias, ReLU and rounding: elements
-// 4 i .. 4 i + 3 of y per thread (output channel (e / plane) % R of element e; fewer
-// than 2^31 elements).  The loads of four parts are issued before they are summed, so
-// a thread waits about once per four parts; 16-byte loads when parts are 16-byte aligned.
+// Sum of the K parts' fp32 partial sums (at most 16 parts), then bias, ReLU and
+// rounding: one element of y per thread (output channel (i / plane) % R; fewer than
+// 2^31 elements), the loads of every part issued before they are summed, so a thread
+// waits once.
 template <typename E>
 __global__ void k_splitk_sum(const float *__restrict__ part, int ks, int64_t stride, uint32_t total,
                              FastDiv div_plane, FastDiv div_R, const float *__restrict__ bias, int relu,
                              E *__restrict__ y) {
-    const bool vec = stride % 4 == 0;
-    for (uint32_t i0 = (blockIdx.x * blockDim.x + threadIdx.x) * 4u; i0 < total; i0 += gridDim.x * blockDim.x * 4u) {
-        const bool whole = vec && i0 + 4 <= total;
-        float v[4] = {0.f, 0.f, 0.f, 0.f};
-        for (int k0 = 0; k0 < ks; k0 += 4) {
-            float t[4][4];
+    for (uint32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < total; i += gridDim.x * blockDim.x) {
+        float t[16];
 #pragma unroll
-            for (int kk = 0; kk < 4; ++kk) {
-                const float *pk = part + (int64_t)(k0 + kk) * stride + i0;
-                if (k0 + kk >= ks) {
+        for (int k = 0; k < 16; ++k) t[k] = k < ks ? part[(int64_t)k * stride + i] : 0.f;
+        float v = 0.f;
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) t[kk][e] = 0.f;
-                } else if (whole) {
-                    const float4 q = *(const float4 *)pk;
-                    t[kk][0] = q.x; t[kk][1] = q.y; t[kk][2] = q.z; t[kk][3] = q.w;
-                } else {
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) t[kk][e] = i0 + e < total ? pk[e] : 0.f;
-                }
-            }
-#pragma unroll
-            for (int kk = 0; kk < 4; ++kk)
-#pragma unroll
-                for (int e = 0; e < 4; ++e) v[e] += t[kk][e];
-        }
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const uint32_t i = i0 + e;
-            if (i >= total) break;
-            const uint32_t q = fdiv(i, div_plane);
-            const uint32_t o = q - fdiv(q, div_R) * div_R.d;
-            const float r = fwd::epi(v[e], bias ? bias[o] : 0.f, relu);
-            if constexpr (sizeof(E) == 2) y[i] = (E)fwd::f32_to_bf16_rne(r);
-            else y[i] = r;
-        }
+        for (int k = 0; k < 16; ++k) v += t[k];
+        const uint32_t q = fdiv(i, div_plane);
+        const uint32_t o = q - fdiv(q, div_R) * div_R.d;
+        const float r = fwd::epi(v, bias ? bias[o] : 0.f, relu);
+        if constexpr (sizeof(E) == 2) y[i] = (E)fwd::f32_to_bf16_rne(r);
+        else y[i] = r;
     }
 }
 
@@ -334,7 +311,7 @@ static hipError_t launch_pw(const Plan &p, int n, const void *x, const uint8_t *
     if (sp.ks > 1) {
         const uint32_t total = (uint32_t)sp.yelems;   // the API keeps y below 2^31 elements
         const int64_t plane = p.is_linear ? n : a.y_cs;
-        const int g = (int)std::min<int64_t>((sp.yelems + 1023) / 1024, 16384);
+        const int g = (int)std::min<int64_t>((sp.yelems + 255) / 256, 65536);
         if (out_bf16)
             k_splitk_sum<uint16_t><<<g, 256, 0, st>>>((const float *)part, sp.ks, sp.yelems, total,
                                                       make_fastdiv((uint32_t)plane), make_fastdiv((uint32_t)p.R),
