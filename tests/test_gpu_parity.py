@@ -317,6 +317,64 @@ def test_tiles_packed_for_another_geometry_give_nan(B, name, layer, with_bias):
     assert torch.isnan(y.float()).all()
 
 
+@pytest.mark.parametrize("reg,bh,bw,rate_pack,rate_run,batch", [
+    (COL, 32, 32, 4, 2, 64),    # gathered lists, split K loop
+    (COL, 16, 64, 4, 8, 512),   # gathered lists, unsplit
+    (ROW, 32, 32, 2, 4, 64),    # identity list, split K loop
+])
+def test_linear_tiles_of_another_scheme_give_nan(B, reg, bh, bw, rate_pack, rate_run, batch):
+    """A linear layer run with dev_tiles packed for another rate: every output is NaN
+    (the kernel reads nothing of such tiles past their header)."""
+    import torch
+    R, C = 192, 256
+    pack = B.Scheme(R, C, bh, bw, reg, rate_pack, 0)
+    run = B.Scheme(R, C, bh, bw, reg, rate_run, 0)
+    rng = np.random.default_rng(7)
+    w = torch.from_numpy(rng.normal(0, 0.05, (R, C)).astype(np.float32)).to(torch.bfloat16).cuda()
+    x = torch.from_numpy(rng.uniform(-1, 1, (C, batch)).astype(np.float32)).to(torch.bfloat16).cuda()
+    mask = torch.empty(R * C, dtype=torch.uint8, device="cuda")
+    B.bsp_prune(pack, B.BF16, w, mask)
+    nv, ni, nr, nb = B.bsp_packed_sizes(pack, None, B.BF16)
+    nb_run = B.bsp_packed_sizes(run, None, B.BF16)[3]
+    vals = torch.empty(max(nv, 1), dtype=torch.bfloat16, device="cuda")
+    idx = torch.empty(max(ni, 1), dtype=torch.int32, device="cuda")
+    rp = torch.empty(max(nr, 1), dtype=torch.int32, device="cuda")
+    tiles = torch.zeros(max(nb, nb_run), dtype=torch.uint8, device="cuda")
+    B.bsp_pack(pack, B.BF16, w, mask, vals, idx, rp, tiles)
+    y = torch.zeros(R, batch, dtype=torch.bfloat16, device="cuda")
+    bias = torch.ones(R, dtype=torch.float32, device="cuda")
+    B.bsp_linear(run, batch, B.BF16, B.BF16, x, tiles, bias, True, y)
+    torch.cuda.synchronize()
+    assert torch.isnan(y.float()).all()
+
+
+def test_small_plane_conv_tiles_of_another_scheme_give_nan(B):
+    """The im2col route (gathered lists, split K loop) run with dev_tiles packed for
+    another rate gives NaN everywhere.  (Tiles of a 1x1 plan over the expanded input do
+    not depend on the image size, so a rate, not a geometry, makes the mismatch.)"""
+    import torch
+    cout, cin, n, hw = 64, 64, 2, 7
+    shape = B.ConvShape(n, cin, hw, hw, 3, 3, 1, 1, 1, 1)
+    pack = B.Scheme(cout, cin * 9, 16, 32, COL, 4, 0)
+    run = B.Scheme(cout, cin * 9, 16, 32, COL, 2, 0)
+    rng = np.random.default_rng(8)
+    w = torch.from_numpy(rng.normal(0, 0.06, (cout, cin * 9)).astype(np.float32)).to(torch.bfloat16).cuda()
+    x = torch.from_numpy(rng.normal(0, 1, (n, cin, hw, hw)).astype(np.float32)).to(torch.bfloat16).cuda()
+    mask = torch.empty(cout * cin * 9, dtype=torch.uint8, device="cuda")
+    B.bsp_prune(pack, B.BF16, w, mask)
+    nv, ni, nr, nb = B.bsp_packed_sizes(pack, shape, B.BF16)
+    nb_run = B.bsp_packed_sizes(run, shape, B.BF16)[3]
+    vals = torch.empty(max(nv, 1), dtype=torch.bfloat16, device="cuda")
+    idx = torch.empty(max(ni, 1), dtype=torch.int32, device="cuda")
+    rp = torch.empty(max(nr, 1), dtype=torch.int32, device="cuda")
+    tiles = torch.zeros(max(nb, nb_run), dtype=torch.uint8, device="cuda")
+    B.bsp_pack(pack, B.BF16, w, mask, vals, idx, rp, tiles, shape)
+    y = torch.zeros(n, cout, hw, hw, dtype=torch.bfloat16, device="cuda")
+    B.bsp_conv2d(run, shape, B.BF16, B.BF16, x, tiles, None, False, y)
+    torch.cuda.synchronize()
+    assert torch.isnan(y.float()).all()
+
+
 # ------------------------------------------------- full-size workloads, sampled ---
 def _c3_distinct():
     seen, out = set(), []
