@@ -25,7 +25,7 @@ ARCH = "gfx950"
 
 SOURCES = ["bsp_pl_1.hip", "bsp_pl_2.hip", "bsp_pl_g.hip", "bsp_pw_b1.hip", "bsp_pw_b2.hip", "bsp_pw_f.hip", "bsp_fwd_b1_k1.hip", "bsp_fwd_b1_k24.hip", "bsp_fwd_b2.hip", "bsp_fwd_b3.hip", "bsp_fwd_b0.hip",
            "bsp_fwd_f.hip", "bsp_plan.cpp", "bsp_api.cpp", "bsp_prune.hip", "bsp_pack.hip",
-           "bsp_conv.hip", "bsp_glue.hip"]
+           "bsp_conv.hip", "bsp_glue.hip", "bsp_stem.hip"]
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-function",
           f"-I{os.path.join(ROOT, 'include')}", f"-I{CSRC}"]

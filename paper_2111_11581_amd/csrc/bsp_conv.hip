@@ -329,6 +329,7 @@ static hipError_t launch_pw(const Plan &p, int n, const void *x, const uint8_t *
 hipError_t launch_conv(const Plan &p, int n, const void *x, const uint8_t *tiles, const float *bias,
                        int relu, int out_bf16, void *y, hipStream_t st, void *part) {
     if (p.pw) return launch_pw(p, n, x, tiles, bias, relu, out_bf16, y, st, part);
+    if (stem_ok(p, x)) return launch_stem(p, n, x, tiles, bias, relu, out_bf16, y, st);
     ConvArgs a;
     memset(&a, 0, sizeof(a));
     a.x = x;

@@ -34,6 +34,13 @@ hipError_t launch_conv(const Plan &p, int n, const void *x, const uint8_t *tiles
                        const float *bias, int relu, int out_bf16, void *y, hipStream_t st,
                        void *part = nullptr);
 
+// Stem convolutions (stride 2, filters at most 8 wide, at most 32 (channel, filter
+// row) pairs, at most 64 filters, identity list, bf16, 16-byte aligned x) run on their
+// own kernel; launch_conv takes that route by itself when stem_ok holds.
+bool stem_ok(const Plan &p, const void *x);
+hipError_t launch_stem(const Plan &p, int n, const void *x, const uint8_t *tiles, const float *bias, int relu,
+                       int out_bf16, void *y, hipStream_t st);
+
 // Bytes of partial sums the pointwise kernel needs for n images (vectors), 0 when its
 // K loop is not split.
 size_t pw_part_bytes(const Plan &p, int n);

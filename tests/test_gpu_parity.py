@@ -206,6 +206,12 @@ CONV_CASES = [
                relu=True, bias=True),
     _conv_case("im2col lists 3x3 s2 col8x16 r8 13x13", 3, 48, 13, 13, 64, 3, 2, 1, 8, 16, COL, 8),
     _conv_case("im2col lists 3x3 rowcol 16x32 r2 5x7", 2, 64, 5, 7, 48, 3, 1, 1, 16, 32, ROWCOL, 2),
+    # stride-2 stems with an identity list: the stem kernel (output pixels as MFMA rows)
+    _conv_case("stem 7x7/2 dense relu bias f32out", 2, 3, 32, 48, 40, 7, 2, 3, 0, 0, DENSE, 1, relu=True,
+               bias=True, out="f32"),
+    _conv_case("stem 7x7/2 dense ragged row groups", 1, 3, 26, 64, 64, 7, 2, 3, 0, 0, DENSE, 1),
+    _conv_case("stem 3x3/2 row16x16 r2 zero-expanded 9 rows bias", 2, 8, 18, 16, 48, 3, 2, 1, 16, 16, ROW, 2,
+               bias=True),
 ]
 
 
@@ -313,6 +319,32 @@ def test_tiles_packed_for_another_geometry_give_nan(B, name, layer, with_bias):
     y = torch.zeros(layer.y_shape, dtype=torch.bfloat16, device="cuda")
     bd = torch.from_numpy(d["bias"].astype(np.float32)).cuda() if with_bias else None
     B.bsp_conv2d(scheme, shape, B.BF16, B.BF16, to_dev(d["x"], "bf16"), tiles, bd, True, y)
+    torch.cuda.synchronize()
+    assert torch.isnan(y.float()).all()
+
+
+def test_stem_tiles_of_another_geometry_give_nan(B):
+    """The stem kernel checks the tile header too: tiles packed for stride 1 used at
+    stride 2 give NaN everywhere."""
+    import torch
+    layer = ConvLayer("mm stem", 2, 3, 40, 40, 64, 7, 7, 2, 2, 3, 3, 0, 0, DENSE, 1, "bf16", ("normal", 0, 1.0),
+                      ("normal", 0, 0.1))
+    d = draw_layer(layer, 8, 1)
+    other = B.ConvShape(1, layer.cin, layer.h, layer.w, 7, 7, 1, 1, 3, 3)
+    shape = B.ConvShape(layer.n, layer.cin, layer.h, layer.w, 7, 7, 2, 2, 3, 3)
+    scheme = layer.scheme
+    nv, ni, nr, nb_other = B.bsp_packed_sizes(scheme, other, B.BF16)
+    nb = B.bsp_packed_sizes(scheme, shape, B.BF16)[3]
+    w = to_dev(d["w"].reshape(layer.cout, -1), "bf16")
+    mask = torch.empty(layer.cout * w.shape[1], dtype=torch.uint8, device="cuda")
+    B.bsp_prune(scheme, B.BF16, w, mask)
+    vals = torch.empty(max(nv, 1), dtype=torch.bfloat16, device="cuda")
+    idx = torch.empty(max(ni, 1), dtype=torch.int32, device="cuda")
+    rp = torch.empty(max(nr, 1), dtype=torch.int32, device="cuda")
+    tiles = torch.zeros(max(nb, nb_other), dtype=torch.uint8, device="cuda")
+    B.bsp_pack(scheme, B.BF16, w, mask, vals, idx, rp, tiles, other)
+    y = torch.zeros(layer.y_shape, dtype=torch.bfloat16, device="cuda")
+    B.bsp_conv2d(scheme, shape, B.BF16, B.BF16, to_dev(d["x"], "bf16"), tiles, None, True, y)
     torch.cuda.synchronize()
     assert torch.isnan(y.float()).all()
 
