@@ -41,7 +41,9 @@ PEAK = {"bf16": 2516.6e12, "f32": 157.3e12}   # dense MFMA, FLOP/s
 PEAK_HBM = 8.0e12         # bytes/s
 N_SIMD = 1024             # 256 CUs x 4 SIMDs
 N_XCD = 8                 # GRBM_GUI_ACTIVE reads as the sum over the 8 XCDs
-KERNEL_TAGS = ("bsp::fwd::k_fwd<", "bsp::pw::k_pw<", "bsp::pl::k_pl<")   # forward kernels: general, pointwise, pipelined pointwise
+# forward kernels: general, pointwise, pipelined pointwise, stride-2 stem
+KERNEL_TAGS = ("bsp::fwd::k_fwd<", "bsp::pw::k_pw<", "bsp::pl::k_pl<", "bsp::stem::k_stem(")
+AUX_TAGS = ("k_im2col", "k_splitk_sum")   # expansion and partial-sum kernels some layers add to a step
 CALIB_BYTES = 256 << 20   # plain copy kernel (torch.neg on bf16) that calibrates the HBM counters
 COLD_BYTES = 512 << 20    # buffer sets rotated through for cold-cache layer times (2x the last-level cache)
 COUNTERS_FILE = os.path.join(ROOT, "profiles", "forward_resnet50_b64_hbm_counters.txt")
@@ -203,7 +205,7 @@ def _pmc_per_launch(d: str, counter: str, n_layers: int):
 
 
 def _short(nm: str) -> str:
-    return nm.replace("void ", "").replace("bsp::fwd::", "").replace("bsp::pw::", "").replace("bsp::pl::", "").split("(")[0]
+    return nm.replace("void ", "").replace("bsp::fwd::", "").replace("bsp::pw::", "").replace("bsp::pl::", "").replace("bsp::stem::", "").split("(")[0]
 
 
 def _layer_counters(d: str, n_layers: int):
@@ -242,7 +244,7 @@ def summarize(args):
         conv = [r for r in stats if is_forward(r["Name"])]
         calls = sum(int(r["Calls"]) for r in conv)
         total_ns = sum(float(r["TotalDurationNs"]) for r in conv)
-        lines += ["# Forward kernels (k_fwd: conv1 and the 3x3 layers; k_pl: 1x1 layers with more than 64 input channels; "
+        lines += ["# Forward kernels (k_stem: conv1; k_fwd: the 3x3 layers; k_pl: 1x1 layers with more than 64 input channels; "
                   "k_pw: the other 1x1 layers and fc) on the "
                   "ResNet-50 v1.5 layer pass (batch 64, bf16, %d launches per step)" % n_layers, "",
                   "Kernel trace statistics (rocprofv3 --kernel-trace --stats), command:", "",
@@ -254,8 +256,12 @@ def summarize(args):
             lines.append("| %s | %s | %.1f | %.3f | %.3f | %.3f |" % (
                 short, r["Calls"], float(r["TotalDurationNs"]) / 1e3, float(r["AverageNs"]) / 1e3,
                 float(r["MinNs"]) / 1e3, float(r["MaxNs"]) / 1e3))
+        aux_ns = sum(float(r["TotalDurationNs"]) for r in stats if any(t in r["Name"] for t in AUX_TAGS))
+        n_steps = calls / n_layers
         lines += ["", "Forward kernels, all instantiations: %d calls, average %.3f us per launch, %.1f us per step "
-                  "of %d launches" % (calls, total_ns / calls / 1e3, total_ns / calls * n_layers / 1e3, n_layers), ""]
+                  "of %d launches" % (calls, total_ns / calls / 1e3, total_ns / calls * n_layers / 1e3, n_layers),
+                  "", "Expansion (im2col) and split-K sum kernels of the layers that take them: %.1f us per step; "
+                  "all kernels of a step: %.1f us" % (aux_ns / n_steps / 1e3, (total_ns + aux_ns) / n_steps / 1e3), ""]
         kv["kernel_avg_us_trace"] = "%.3f" % (total_ns / calls / 1e3)
         if args.pmc_fetch and args.pmc_write:
             f_kib, nf, f_cal = _pmc_per_launch(args.pmc_fetch, "FETCH_SIZE", n_layers)
@@ -605,7 +611,7 @@ def main():
                       indent=1)
 
     roof = {"bound": "hbm",
-            "kernel": "forward kernels k_fwd + k_pl + k_pw (all instantiations, %d launches per step)" % len(ops),
+            "kernel": "forward kernels k_stem + k_fwd + k_pl + k_pw (all instantiations, %d launches per step; the step time also holds the im2col expansion and split-K sums of the layers that take them)" % len(ops),
             "achieved": round(achieved_gbs, 1), "peak": PEAK_HBM / 1e9, "unit": "GB/s",
             "frac": round(achieved_gbs * 1e9 / PEAK_HBM, 4), "traffic": None,
             "algorithmic_bytes_per_launch": round(b_alg / len(ops)),
