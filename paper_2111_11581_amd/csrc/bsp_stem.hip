@@ -125,35 +125,6 @@ __global__ __launch_bounds__(kStemThreads, 2) void k_stem(StemArgs a) {
     const bool ok = hdr->magic == kMagic && hdr->fp_lo == a.fp_lo && hdr->fp_hi == a.fp_hi;
     const uint16_t *A = (const uint16_t *)(a.tiles + a.off_a);
 
-    // weight fragments [ks][mt][lane]: filter columns 0..7 of pair 4 ks + lane / 16 and
-    // output channel 16 mt + lane % 16, read from the packed tiles (m-tile co / 16, step
-    // t / 32, lane co % 16 + 16 (t % 32 / 8), element t % 8 for GEMM column t); kB
-    // loads of a thread in flight together
-    constexpr int kB = 8;
-    uint16_t *s_w16 = (uint16_t *)lds;
-    const int nw = a.kst * 4 * 64 * 8;
-    for (int i0 = tid; i0 < nw; i0 += kStemThreads * kB) {
-        uint16_t v[kB];
-        // every load is issued (zero weights read the header) and selected afterwards, so
-        // that the kB loads are in flight together
-        bool use[kB];
-#pragma unroll
-        for (int u = 0; u < kB; ++u) {
-            const int i = i0 + u * kStemThreads;
-            const int j = i & 7, l = (i >> 3) & 63, mt = (i >> 9) & 3, ks = i >> 11;
-            const int p = 4 * ks + (l >> 4), co = 16 * mt + (l & 15);
-            const int t = p * a.KW + j;
-            use[u] = ok && i < nw && p < a.npair && j < a.KW && co < a.R;
-            const uint16_t *src =
-                use[u] ? A + (((int64_t)(co >> 4) * a.S + (t >> 5)) * 64 + (co & 15) + 16 * ((t & 31) >> 3)) * 8 + (t & 7)
-                       : (const uint16_t *)a.tiles;
-            v[u] = *src;
-        }
-#pragma unroll
-        for (int u = 0; u < kB; ++u)
-            if (i0 + u * kStemThreads < nw) s_w16[i0 + u * kStemThreads] = use[u] ? v[u] : (uint16_t)0;
-    }
-
     // input rows [c][r] (input row 2 oh0 - PH + r), then one zero row.  Task q of a row
     // writes dwords d_lo + 4 q .. + 3: elements 8 q - 1 .. 8 q + 6 of the row, realigned
     // by two bytes from granule q and the dword before it; the other dwords of a row
@@ -193,6 +164,63 @@ __global__ __launch_bounds__(kStemThreads, 2) void k_stem(StemArgs a) {
     };
     int rg = blockIdx.x;
     if (rg < a.n_rg) load(rg);
+
+    // weight fragments [ks][mt][lane]: filter columns 0..7 of pair p = 4 ks + lane / 16
+    // and output channel co = 16 mt + lane % 16, i.e. GEMM columns p KW .. p KW + 7 of
+    // row co.  The packed tiles hold 8 consecutive columns of a row in 16 bytes (chunk q:
+    // m-tile co / 16, step q / 4, lane co % 16 + 16 (q % 4)), so a fragment is the two
+    // chunks around its first column, shifted by that column's place in the chunk.  All
+    // loads of a thread are issued first (zero fragments read the header).
+    {
+        const int nfrag = a.kst * 4 * 64;
+        uint4 c0[kMaxKst], c1[kMaxKst];
+        bool use[kMaxKst];
+#pragma unroll
+        for (int u = 0; u < kMaxKst; ++u) {
+            const int f = tid + u * kStemThreads;
+            const int l = f & 63, mt = (f >> 6) & 3, ks = f >> 8;
+            const int p = 4 * ks + (l >> 4), co = 16 * mt + (l & 15);
+            const int q0 = p * a.KW >> 3;
+            use[u] = ok && f < nfrag && p < a.npair && co < a.R;
+            const int64_t row = (int64_t)(co >> 4) * a.S;
+            const bool v0 = use[u] && (q0 >> 2) < a.S, v1 = use[u] && ((q0 + 1) >> 2) < a.S;
+            const uint16_t *s0 = v0 ? A + ((row + (q0 >> 2)) * 64 + (co & 15) + 16 * (q0 & 3)) * 8
+                                    : (const uint16_t *)a.tiles;
+            const uint16_t *s1 = v1 ? A + ((row + ((q0 + 1) >> 2)) * 64 + (co & 15) + 16 * ((q0 + 1) & 3)) * 8
+                                    : (const uint16_t *)a.tiles;
+            c0[u] = *(const uint4 *)s0;
+            c1[u] = *(const uint4 *)s1;
+            if (!v1) c1[u] = make_uint4(0u, 0u, 0u, 0u);
+        }
+        uint32_t km[4];   // filter columns 2 k, 2 k + 1 that exist
+#pragma unroll
+        for (int k = 0; k < 4; ++k) km[k] = (2 * k < a.KW ? 0xffffu : 0u) | (2 * k + 1 < a.KW ? 0xffff0000u : 0u);
+        uint4 *s_wf = (uint4 *)lds;
+#pragma unroll
+        for (int u = 0; u < kMaxKst; ++u) {
+            const int f = tid + u * kStemThreads;
+            if (f >= nfrag) continue;
+            const int l = f & 63, ks = f >> 8;
+            const int t0 = (4 * ks + (l >> 4)) * a.KW;
+            const int base = (t0 & 7) >> 1;        // first dword of the fragment in the chunk pair
+            const bool odd = (t0 & 1) != 0;        // the fragment starts in the upper half of it
+            const uint32_t d[8] = {c0[u].x, c0[u].y, c0[u].z, c0[u].w, c1[u].x, c1[u].y, c1[u].z, c1[u].w};
+            auto pick = [&](int i) {   // d[i], i in 0..7
+                const uint32_t a01 = i & 1 ? d[1] : d[0], a23 = i & 1 ? d[3] : d[2];
+                const uint32_t a45 = i & 1 ? d[5] : d[4], a67 = i & 1 ? d[7] : d[6];
+                const uint32_t b03 = i & 2 ? a23 : a01, b47 = i & 2 ? a67 : a45;
+                return i & 4 ? b47 : b03;
+            };
+            uint32_t r[4];
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const uint32_t lo = pick(base + k), hi = pick(min(base + k + 1, 7));
+                r[k] = (odd ? __builtin_amdgcn_alignbyte(hi, lo, 2) : lo) & km[k];
+            }
+            s_wf[f] = use[u] ? make_uint4(r[0], r[1], r[2], r[3]) : make_uint4(0u, 0u, 0u, 0u);
+        }
+    }
+
     for (; rg < a.n_rg; rg += gridDim.x) {
 #pragma unroll
         for (int u = 0; u < kMaxT; ++u) {
