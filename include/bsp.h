@@ -209,7 +209,9 @@ bsp_status bsp_to_bcs(const bsp_scheme *scheme, const int32_t *indices, const in
  *  - layers with a kernel larger than 1x1 whose output plane has at most 16
  *    pixels, and bf16 layers with per-block-row lists (COL, PUNCHED, ROWCOL
  *    without counts) whose plane has at most 64 pixels (strided, or whose
- *    expanded input for 64 images stays within 24 MiB), expand x into it
+ *    expanded input for 64 images stays within 24 MiB), and bf16 1x1
+ *    stride-2 layers without padding over one identity list (ROW or DENSE
+ *    without counts) whose plane has at most 196 pixels, expand x into it
  *    (n x cin*kh*kw planes of Ho*Wo elements, rounded up to 8 for the bf16
  *    pipelined kernel);
  *  - bf16 layers run by the pipelined pointwise kernel (1x1, linear and the
