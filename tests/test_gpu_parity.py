@@ -206,7 +206,13 @@ CONV_CASES = [
                relu=True, bias=True),
     _conv_case("im2col lists 3x3 s2 col8x16 r8 13x13", 3, 48, 13, 13, 64, 3, 2, 1, 8, 16, COL, 8),
     _conv_case("im2col lists 3x3 rowcol 16x32 r2 5x7", 2, 64, 5, 7, 48, 3, 1, 1, 16, 32, ROWCOL, 2),
-    # stride-2 stems with an identity list: the stem kernel (output pixels as MFMA rows)
+    # 1x1 stride-2 layers over one identity list: planes of at most 196 pixels run over the
+    # subsampled input (stride-1 pointwise kernel), larger ones on the strided kernel
+    _conv_case("subsample 1x1/2 dense odd 15x13 relu bias f32out", 3, 48, 15, 13, 40, 1, 2, 0, 0, 0, DENSE, 1,
+               relu=True, bias=True, out="f32"),
+    _conv_case("subsample 1x1/2 row16x16 r2 28x28 (196-pixel plane)", 2, 64, 28, 28, 96, 1, 2, 0, 16, 16, ROW, 2),
+    _conv_case("strided 1x1/2 row16x16 r2 30x30 (225-pixel plane)", 2, 64, 30, 30, 96, 1, 2, 0, 16, 16, ROW, 2),
+    # stride-2 stems with an identity list: the stem kernel (output channels as MFMA rows)
     _conv_case("stem 7x7/2 dense relu bias f32out", 2, 3, 32, 48, 40, 7, 2, 3, 0, 0, DENSE, 1, relu=True,
                bias=True, out="f32"),
     _conv_case("stem 7x7/2 dense ragged row groups", 1, 3, 26, 64, 64, 7, 2, 3, 0, 0, DENSE, 1),
